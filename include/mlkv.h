@@ -1,0 +1,202 @@
+/*
+ * mlkv.h — MLKV decode attention on AMD Instinct MI355X (gfx950).
+ *
+ * Multi-Layer Key-Value sharing (arXiv 2406.09297): query head i of layer n
+ * attends to a KV head that is shared by a group of query heads inside the
+ * layer (GQA grouping, Section 2.3, Eq. 12) and by a group of consecutive
+ * layers (Section 3, Eqs. 13-17).  Only the layer that owns a KV head appends
+ * the newest token's key/value to the cache (Section 2.4 caching; the shared
+ * head comes from the bottom layer of its group, Figure 2).
+ *
+ * Everything here is a plain C ABI: device pointers, sizes and a HIP stream.
+ * All entry points are synchronous on the host only for argument validation;
+ * device work is enqueued on `stream` and nothing synchronizes.  No entry
+ * point throws; each returns an mlkv_status and mlkv_last_error() gives a
+ * thread-local message for the last failure.  Argument errors are detected
+ * before any HIP call is made.
+ *
+ * Data types: bf16 storage for q, k, v and the cache (raw 16-bit patterns),
+ * fp32 accumulation, output fp32 or bf16.
+ */
+#ifndef MLKV_H_
+#define MLKV_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ----------------------------------------------------------------------- */
+/* Status                                                                    */
+/* ----------------------------------------------------------------------- */
+
+typedef enum {
+  MLKV_OK = 0,
+  MLKV_ERR_INVALID_ARG = 1, /* null pointer, non-positive size, bad enum     */
+  MLKV_ERR_BAD_MAP = 2,     /* layer->KV-head map violates the rules below   */
+  MLKV_ERR_ALIGNMENT = 3,   /* a device pointer is not 16-byte aligned       */
+  MLKV_ERR_UNSUPPORTED = 4, /* head_dim or query-group size not supported    */
+  MLKV_ERR_CAPACITY = 5,    /* capacity / max_len_hint / lengths out of range */
+  MLKV_ERR_WORKSPACE = 6,   /* workspace missing or too small                */
+  MLKV_ERR_HIP = 7          /* a HIP runtime call or launch failed           */
+} mlkv_status;
+
+typedef enum { MLKV_OUT_F32 = 0, MLKV_OUT_BF16 = 1 } mlkv_out_dtype;
+
+/* Static string naming the status.  Never NULL. */
+const char* mlkv_status_string(mlkv_status status);
+/* Message of the last failing call on this thread ("" if none).  Owned by the
+ * library, valid until the next call on the same thread. */
+const char* mlkv_last_error(void);
+
+/* ----------------------------------------------------------------------- */
+/* Layer -> KV-head map (Section 2.3 Eq. 12, Section 3 Eqs. 15 and 17)       */
+/* ----------------------------------------------------------------------- */
+
+typedef struct mlkv_map mlkv_map; /* opaque, host-only, owned by the library */
+
+/*
+ * Uniform MLKV map: l layers with h query heads; m of the layers own g KV
+ * heads each (n_kv = m*g).  In 0-indexed form of the paper's formulas, layer n
+ * belongs to layer-group k = n / (l/m) and its query head i uses in-layer
+ * group j = i / (h/g); the global KV head is k*g + j, owned (appended) by the
+ * bottom layer of the group, k*(l/m).
+ * m = l, g = h gives MHA; m = l, g = 1 gives MQA; m = l gives GQA.
+ * Errors: MLKV_ERR_INVALID_ARG if any argument is <= 0, if m does not divide l
+ * or g does not divide h, or out is NULL.
+ */
+mlkv_status mlkv_map_create_uniform(int l, int h, int m, int g, mlkv_map** out);
+
+/*
+ * General map from explicit tables (e.g. non-uniform cross-layer patterns).
+ * kv_of [l*h]: KV head of query head i in layer n at kv_of[n*h + i].
+ * owner_of [n_kv]: the layer that appends KV head kv.
+ * The arrays are copied; the caller keeps ownership.  Rules (else
+ * MLKV_ERR_BAD_MAP):
+ *   - every entry in range; every KV head is read by at least one layer;
+ *   - in each layer the heads read form a contiguous range of KV heads
+ *     [kv_begin, kv_begin + c) with c dividing h, and query head i reads
+ *     kv_begin + i / (h/c)  (GQA grouping within the layer);
+ *   - owner_of[kv] <= every layer that reads kv (the owner appends first);
+ *   - each layer owns a contiguous range of KV heads.
+ */
+mlkv_status mlkv_map_create(int l, int h, int n_kv, const int32_t* kv_of,
+                            const int32_t* owner_of, mlkv_map** out);
+void mlkv_map_destroy(mlkv_map* map); /* NULL is ignored */
+
+int mlkv_map_num_layers(const mlkv_map* map);
+int mlkv_map_num_q_heads(const mlkv_map* map);
+int mlkv_map_num_kv_heads(const mlkv_map* map);              /* m*g for uniform maps */
+int mlkv_map_kv_head(const mlkv_map* map, int layer, int q_head); /* -1 if out of range */
+int mlkv_map_owner_layer(const mlkv_map* map, int kv);            /* -1 if out of range */
+/* Number of KV heads layer `layer` reads (g for uniform maps), -1 if out of range. */
+int mlkv_map_layer_kv_count(const mlkv_map* map, int layer);
+/* Number of KV heads layer `layer` appends (0 for non-owning layers). */
+int mlkv_map_layer_owned_count(const mlkv_map* map, int layer);
+/* First KV head layer `layer` appends (-1 if it owns none). */
+int mlkv_map_layer_owned_begin(const mlkv_map* map, int layer);
+
+/* ----------------------------------------------------------------------- */
+/* KV cache                                                                  */
+/* ----------------------------------------------------------------------- */
+
+/*
+ * Caller-owned device memory (e.g. torch tensors); the library never frees it.
+ * capacity must be a multiple of 32; head_dim 64 or 128; both planes 16-byte
+ * aligned.  Element (kv, b, t, d), t < capacity, lives at
+ *   K: k[((kv*batch + b)*capacity + t)*head_dim + d]
+ *      (each sequence's keys are contiguous token rows)
+ *   V: v[((kv*batch + b)*capacity + (t & ~31))*head_dim + d*32 + (t & 31)]
+ *      (values in blocks of 32 tokens, channel-major inside a block, so a
+ *      block is the transposed 32 x head_dim tile)
+ * Both planes hold n_kv*batch*capacity*head_dim bf16 values.
+ */
+typedef struct {
+  void* k;
+  void* v;
+  int n_kv;
+  int batch;
+  int capacity;
+  int head_dim;
+} mlkv_cache;
+
+/* Bytes of one cache (both planes): 2 * batch * capacity * n_kv * head_dim * 2,
+ * the paper's 2*b*s*m*g*d_k elements (Section 3, Table 1) in bf16.
+ * Returns 0 for invalid arguments. */
+size_t mlkv_cache_bytes(const mlkv_map* map, int batch, int capacity, int head_dim);
+
+/* Device workspace needed by mlkv_decode_attention / mlkv_decode_step for any
+ * max_len_hint <= capacity (split-K partial results).  0 for invalid args. */
+size_t mlkv_workspace_bytes(const mlkv_map* map, int batch, int capacity, int head_dim);
+
+/*
+ * Append the newest token of `layer` (Section 2.4) into the KV heads that
+ * layer owns; a no-op returning MLKV_OK for layers that own none.
+ *   k_new, v_new: device bf16, row b at k_new + b*new_row_stride elements,
+ *                 holding the owned heads' rows back to back
+ *                 ([owned_count][head_dim]); 16-byte aligned,
+ *                 new_row_stride a multiple of 8 and >= owned_count*head_dim.
+ *   positions:    device int32 [batch]; the token goes to slot positions[b].
+ *                 Slots outside [0, capacity) are skipped (no write).
+ * Bit copy: nothing else in the cache changes.
+ */
+mlkv_status mlkv_cache_append(int layer, const mlkv_map* map, const mlkv_cache* cache,
+                              const void* k_new, const void* v_new, int new_row_stride,
+                              const int32_t* positions, hipStream_t stream);
+
+/*
+ * Decode attention of one layer (Eqs. 1-3 with the MLKV head map, Eq. 14):
+ *   out[b][i][:] = softmax(q[b][i] . K_kv[b][t]^T / sqrt(head_dim))_t V_kv[b][t]
+ * over t in [0, L_b), kv = kv head of (layer, i), L_b = seq_lens[b] (device
+ * int32 [batch]) clamped to [0, capacity]; L_b = 0 gives zeros.
+ *   q:   device bf16 [batch][h][head_dim], 16-byte aligned.
+ *   out: device [batch][h][head_dim], fp32 or bf16 per out_dtype.
+ *   max_len_hint: an upper bound of every L_b (<= 0 means capacity); it sizes
+ *        the split-K grid.  Lengths above it are truncated to it.
+ *   workspace: device memory of at least mlkv_workspace_bytes(...) bytes,
+ *        16-byte aligned; contents need no initialisation and are clobbered.
+ * Every query head mapped to one KV head is served from a single pass over
+ * that head's cache rows.
+ */
+mlkv_status mlkv_decode_attention(int layer, const void* q, const mlkv_cache* cache,
+                                  const mlkv_map* map, const int32_t* seq_lens, void* out,
+                                  mlkv_out_dtype out_dtype, int max_len_hint, void* workspace,
+                                  size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * One decode step over all layers (Eq. 17): for n = 0..l-1, append the newest
+ * token into the heads layer n owns (slot ctx_lens[b]), then attend every
+ * query head of layer n over ctx_lens[b] + 1 positions.
+ *   q_all:   device bf16 [l][batch][h][head_dim]
+ *   k_new_all, v_new_all: device bf16 [batch][n_kv][head_dim]
+ *   ctx_lens: device int32 [batch], tokens cached before the step; the caller
+ *             increments them after the step.
+ *   out_all: device [l][batch][h][head_dim], fp32 or bf16.
+ *   max_len_hint: bound of ctx_lens[b] + 1 (<= 0 means capacity).
+ */
+mlkv_status mlkv_decode_step(const void* q_all, const void* k_new_all, const void* v_new_all,
+                             const mlkv_cache* cache, const mlkv_map* map,
+                             const int32_t* ctx_lens, void* out_all, mlkv_out_dtype out_dtype,
+                             int max_len_hint, void* workspace, size_t workspace_bytes,
+                             hipStream_t stream);
+
+/* ----------------------------------------------------------------------- */
+/* Introspection (tests and benchmarks)                                      */
+/* ----------------------------------------------------------------------- */
+
+/* Split-K plan that mlkv_decode_attention uses for `layer` at this max length:
+ * tokens per split (a multiple of 32) and number of splits.  Returns
+ * MLKV_ERR_* on invalid arguments.  Env MLKV_SPLIT_TOKENS overrides the
+ * tokens per split (rounded to a multiple of 128, at least 128). */
+mlkv_status mlkv_plan_splits(const mlkv_map* map, int layer, int batch, int capacity,
+                             int head_dim, int max_len, int* tokens_per_split, int* n_splits);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MLKV_H_ */

@@ -1,0 +1,485 @@
+// C ABI of the MLKV decode library: map construction and validation, argument
+// checks, split-K planning and the per-layer / per-step launch sequences.
+// Every argument error is reported before any HIP call.
+#include "mlkv.h"
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "kernels.h"
+
+struct mlkv_map {
+  int l = 0, h = 0, n_kv = 0;
+  std::vector<int32_t> kv_of;     // [l*h]
+  std::vector<int32_t> owner_of;  // [n_kv]
+  // per layer: the KV heads read form [kv_begin, kv_begin + kv_count), G = h / kv_count
+  std::vector<int> kv_begin, kv_count, group;
+  // per layer: the KV heads appended form [own_begin, own_begin + own_count)
+  std::vector<int> own_begin, own_count;
+};
+
+namespace {
+
+thread_local std::string g_last_error;
+
+mlkv_status fail(mlkv_status s, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+mlkv_status fail(mlkv_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return s;
+}
+
+mlkv_status ok() {
+  g_last_error.clear();
+  return MLKV_OK;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+bool aligned4(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
+
+constexpr int kTileTokens = 32;
+constexpr int kWaves = 4;
+constexpr int kMinTilesPerSplit = kWaves;  // every wave of a workgroup gets a tile
+constexpr int kTargetWorkgroups = 1024;    // ~4 per CU on a 256-CU MI355X
+
+// Derive the per-layer structure of a map; returns an error message or "".
+std::string analyse(mlkv_map& m) {
+  const int l = m.l, h = m.h, n_kv = m.n_kv;
+  m.kv_begin.assign(l, 0);
+  m.kv_count.assign(l, 0);
+  m.group.assign(l, 0);
+  m.own_begin.assign(l, -1);
+  m.own_count.assign(l, 0);
+  std::vector<int> first_reader(n_kv, l);
+  for (int n = 0; n < l; ++n) {
+    const int32_t* row = &m.kv_of[static_cast<size_t>(n) * h];
+    int lo = row[0], hi = row[0];
+    for (int i = 0; i < h; ++i) {
+      if (row[i] < 0 || row[i] >= n_kv) return "kv_of entry out of range";
+      lo = row[i] < lo ? row[i] : lo;
+      hi = row[i] > hi ? row[i] : hi;
+    }
+    const int c = hi - lo + 1;
+    if (h % c != 0) return "a layer reads a number of KV heads that does not divide h";
+    const int G = h / c;
+    for (int i = 0; i < h; ++i)
+      if (row[i] != lo + i / G)
+        return "query heads of a layer must read KV heads kv_begin + i/(h/c) (GQA grouping)";
+    m.kv_begin[n] = lo;
+    m.kv_count[n] = c;
+    m.group[n] = G;
+    for (int kv = lo; kv <= hi; ++kv) first_reader[kv] = n < first_reader[kv] ? n : first_reader[kv];
+  }
+  for (int kv = 0; kv < n_kv; ++kv) {
+    if (first_reader[kv] == l) return "a KV head is read by no layer";
+    const int o = m.owner_of[kv];
+    if (o < 0 || o >= l) return "owner_of entry out of range";
+    if (o > first_reader[kv]) return "a KV head is read before its owner layer appends it";
+  }
+  for (int kv = 0; kv < n_kv; ++kv) {
+    const int o = m.owner_of[kv];
+    if (m.own_count[o] == 0) {
+      m.own_begin[o] = kv;
+      m.own_count[o] = 1;
+    } else if (m.own_begin[o] + m.own_count[o] == kv) {
+      ++m.own_count[o];
+    } else {
+      return "the KV heads a layer owns must be contiguous";
+    }
+  }
+  return "";
+}
+
+mlkv_status check_map(const mlkv_map* map) {
+  if (!map) return fail(MLKV_ERR_INVALID_ARG, "map is NULL");
+  return MLKV_OK;
+}
+
+mlkv_status check_cache(const mlkv_cache* c, const mlkv_map* map) {
+  if (!c) return fail(MLKV_ERR_INVALID_ARG, "cache is NULL");
+  if (!c->k || !c->v) return fail(MLKV_ERR_INVALID_ARG, "cache planes must be non-NULL");
+  if (!aligned16(c->k) || !aligned16(c->v))
+    return fail(MLKV_ERR_ALIGNMENT, "cache planes must be 16-byte aligned");
+  if (c->batch <= 0 || c->capacity <= 0)
+    return fail(MLKV_ERR_INVALID_ARG, "cache batch and capacity must be positive");
+  if (c->capacity % kTileTokens != 0)
+    return fail(MLKV_ERR_CAPACITY, "cache capacity %d is not a multiple of 32", c->capacity);
+  if (c->head_dim != 64 && c->head_dim != 128)
+    return fail(MLKV_ERR_UNSUPPORTED, "head_dim %d not supported (64 or 128)", c->head_dim);
+  if (c->n_kv != map->n_kv)
+    return fail(MLKV_ERR_INVALID_ARG, "cache has %d KV heads, map has %d", c->n_kv, map->n_kv);
+  const double elems = 2.0 * c->n_kv * c->batch * static_cast<double>(c->capacity) * c->head_dim;
+  if (elems > 9.0e18) return fail(MLKV_ERR_CAPACITY, "cache too large");
+  return MLKV_OK;
+}
+
+int tiles_of(int len) { return (len + kTileTokens - 1) / kTileTokens; }
+
+void plan(const mlkv_map* map, int layer, int batch, int max_len, int* tps_out, int* ns_out) {
+  const int max_tiles = tiles_of(max_len < 1 ? 1 : max_len);
+  const long units = static_cast<long>(batch) * map->kv_count[layer];
+  int tps = kMinTilesPerSplit;
+  const char* env = std::getenv("MLKV_SPLIT_TOKENS");
+  if (env && *env) {
+    int tok = std::atoi(env);
+    tps = tok / kTileTokens;
+    tps = (tps / kMinTilesPerSplit) * kMinTilesPerSplit;
+    if (tps < kMinTilesPerSplit) tps = kMinTilesPerSplit;
+  } else {
+    for (int cand = 64; cand >= kMinTilesPerSplit; cand /= 2) {
+      const long splits = (max_tiles + cand - 1) / cand;
+      if (units * splits >= kTargetWorkgroups) {
+        tps = cand;
+        break;
+      }
+    }
+  }
+  int ns = (max_tiles + tps - 1) / tps;
+  if (ns < 1) ns = 1;
+  if (ns == 1) tps = max_tiles < 1 ? 1 : max_tiles;  // one split: exactly the needed tiles
+  *tps_out = tps;
+  *ns_out = ns;
+}
+
+size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// Workspace layout for one call: part_acc then (256-aligned) part_ml.
+size_t workspace_need(int batch, int h, int head_dim, int n_split) {
+  if (n_split <= 1) return 0;
+  const size_t rows = static_cast<size_t>(batch) * h * n_split;
+  return align_up(rows * head_dim * sizeof(float), 256) + rows * 2 * sizeof(float);
+}
+
+mlkv_status check_lengths_if_requested(const int32_t* lens, int batch, int offset, int limit,
+                                       hipStream_t stream) {
+  const char* env = std::getenv("MLKV_CHECK");
+  if (!env || std::strcmp(env, "1") != 0) return MLKV_OK;
+  std::vector<int32_t> host(batch);
+  if (hipStreamSynchronize(stream) != hipSuccess ||
+      hipMemcpy(host.data(), lens, sizeof(int32_t) * batch, hipMemcpyDeviceToHost) != hipSuccess)
+    return fail(MLKV_ERR_HIP, "MLKV_CHECK: could not read lengths back");
+  for (int b = 0; b < batch; ++b) {
+    const long L = static_cast<long>(host[b]) + offset;
+    if (L < 0 || L > limit)
+      return fail(MLKV_ERR_CAPACITY, "MLKV_CHECK: sequence %d attends %ld positions, limit %d", b,
+                  L, limit);
+  }
+  return MLKV_OK;
+}
+
+mlkv_status attention_impl(int layer, const void* q, const mlkv_cache* cache, const mlkv_map* map,
+                           const int32_t* lens, int len_offset, void* out, mlkv_out_dtype dt,
+                           int max_len_hint, void* ws, size_t ws_bytes, hipStream_t stream) {
+  const int B = cache->batch, S = cache->capacity, D = cache->head_dim;
+  const int max_len = max_len_hint <= 0 ? S : max_len_hint;
+  int tps = 0, ns = 0;
+  plan(map, layer, B, max_len, &tps, &ns);
+  const size_t need = workspace_need(B, map->h, D, ns);
+  if (need > 0 && (!ws || ws_bytes < need))
+    return fail(MLKV_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need,
+                ws ? ws_bytes : 0);
+  if (need > 0 && !aligned16(ws)) return fail(MLKV_ERR_ALIGNMENT, "workspace not 16-byte aligned");
+  mlkv::AttnParams p{};
+  p.q = static_cast<const uint16_t*>(q);
+  p.k = static_cast<const uint16_t*>(cache->k);
+  p.v = static_cast<const uint16_t*>(cache->v);
+  p.lens = lens;
+  p.out = out;
+  const size_t rows = static_cast<size_t>(B) * map->h * ns;
+  p.part_acc = need ? static_cast<float*>(ws) : nullptr;
+  p.part_ml = need ? reinterpret_cast<float*>(static_cast<char*>(ws) +
+                                              align_up(rows * D * sizeof(float), 256))
+                   : nullptr;
+  p.B = B;
+  p.h = map->h;
+  p.S = S;
+  p.kv_begin = map->kv_begin[layer];
+  p.G = map->group[layer];
+  p.n_groups = map->kv_count[layer];
+  p.n_split = ns;
+  p.tiles_per_split = tps;
+  p.len_offset = len_offset;
+  p.out_bf16 = dt == MLKV_OUT_BF16 ? 1 : 0;
+  p.scale_log2 = static_cast<float>(1.4426950408889634 / std::sqrt(static_cast<double>(D)));
+  const hipError_t err = mlkv::launch_attention(p, D, stream);
+  if (err != hipSuccess) return fail(MLKV_ERR_HIP, "attention launch: %s", hipGetErrorString(err));
+  return MLKV_OK;
+}
+
+mlkv_status append_impl(int layer, const mlkv_map* map, const mlkv_cache* cache, const void* k_new,
+                        const void* v_new, int row_stride, const int32_t* positions,
+                        hipStream_t stream) {
+  const int owned = map->own_count[layer];
+  if (owned == 0) return MLKV_OK;
+  mlkv::AppendParams p{};
+  p.k_new = static_cast<const uint16_t*>(k_new);
+  p.v_new = static_cast<const uint16_t*>(v_new);
+  p.positions = positions;
+  p.k = static_cast<uint16_t*>(cache->k);
+  p.v = static_cast<uint16_t*>(cache->v);
+  p.B = cache->batch;
+  p.S = cache->capacity;
+  p.kv_begin = map->own_begin[layer];
+  p.row_stride = row_stride;
+  const hipError_t err = mlkv::launch_append(p, cache->head_dim, owned, stream);
+  if (err != hipSuccess) return fail(MLKV_ERR_HIP, "append launch: %s", hipGetErrorString(err));
+  return MLKV_OK;
+}
+
+mlkv_status check_group_size(const mlkv_map* map, int layer) {
+  if (map->group[layer] > 16)
+    return fail(MLKV_ERR_UNSUPPORTED,
+                "layer %d maps %d query heads to one KV head; at most 16 are supported", layer,
+                map->group[layer]);
+  return MLKV_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* mlkv_status_string(mlkv_status s) {
+  switch (s) {
+    case MLKV_OK: return "MLKV_OK";
+    case MLKV_ERR_INVALID_ARG: return "MLKV_ERR_INVALID_ARG";
+    case MLKV_ERR_BAD_MAP: return "MLKV_ERR_BAD_MAP";
+    case MLKV_ERR_ALIGNMENT: return "MLKV_ERR_ALIGNMENT";
+    case MLKV_ERR_UNSUPPORTED: return "MLKV_ERR_UNSUPPORTED";
+    case MLKV_ERR_CAPACITY: return "MLKV_ERR_CAPACITY";
+    case MLKV_ERR_WORKSPACE: return "MLKV_ERR_WORKSPACE";
+    case MLKV_ERR_HIP: return "MLKV_ERR_HIP";
+  }
+  return "MLKV_ERR_UNKNOWN";
+}
+
+const char* mlkv_last_error(void) { return g_last_error.c_str(); }
+
+mlkv_status mlkv_map_create_uniform(int l, int h, int m, int g, mlkv_map** out) {
+  if (!out) return fail(MLKV_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  if (l <= 0 || h <= 0 || m <= 0 || g <= 0)
+    return fail(MLKV_ERR_INVALID_ARG, "l, h, m, g must be positive");
+  if (l % m != 0 || h % g != 0)
+    return fail(MLKV_ERR_INVALID_ARG, "uniform map needs m | l and g | h (l=%d h=%d m=%d g=%d)", l,
+                h, m, g);
+  if (static_cast<long>(l) * h > (1L << 24))
+    return fail(MLKV_ERR_INVALID_ARG, "too many query heads");
+  mlkv_map* map = new (std::nothrow) mlkv_map;
+  if (!map) return fail(MLKV_ERR_INVALID_ARG, "out of host memory");
+  map->l = l;
+  map->h = h;
+  map->n_kv = m * g;
+  map->kv_of.resize(static_cast<size_t>(l) * h);
+  map->owner_of.resize(map->n_kv);
+  const int layers_per_group = l / m, heads_per_kv = h / g;
+  for (int n = 0; n < l; ++n)
+    for (int i = 0; i < h; ++i)
+      map->kv_of[static_cast<size_t>(n) * h + i] = (n / layers_per_group) * g + i / heads_per_kv;
+  for (int kv = 0; kv < map->n_kv; ++kv) map->owner_of[kv] = (kv / g) * layers_per_group;
+  const std::string err = analyse(*map);
+  if (!err.empty()) {
+    delete map;
+    return fail(MLKV_ERR_BAD_MAP, "%s", err.c_str());
+  }
+  *out = map;
+  return ok();
+}
+
+mlkv_status mlkv_map_create(int l, int h, int n_kv, const int32_t* kv_of, const int32_t* owner_of,
+                            mlkv_map** out) {
+  if (!out) return fail(MLKV_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  if (l <= 0 || h <= 0 || n_kv <= 0) return fail(MLKV_ERR_INVALID_ARG, "l, h, n_kv must be positive");
+  if (!kv_of || !owner_of) return fail(MLKV_ERR_INVALID_ARG, "kv_of and owner_of must be non-NULL");
+  if (static_cast<long>(l) * h > (1L << 24))
+    return fail(MLKV_ERR_INVALID_ARG, "too many query heads");
+  mlkv_map* map = new (std::nothrow) mlkv_map;
+  if (!map) return fail(MLKV_ERR_INVALID_ARG, "out of host memory");
+  map->l = l;
+  map->h = h;
+  map->n_kv = n_kv;
+  map->kv_of.assign(kv_of, kv_of + static_cast<size_t>(l) * h);
+  map->owner_of.assign(owner_of, owner_of + n_kv);
+  const std::string err = analyse(*map);
+  if (!err.empty()) {
+    delete map;
+    return fail(MLKV_ERR_BAD_MAP, "%s", err.c_str());
+  }
+  *out = map;
+  return ok();
+}
+
+void mlkv_map_destroy(mlkv_map* map) { delete map; }
+
+int mlkv_map_num_layers(const mlkv_map* map) { return map ? map->l : -1; }
+int mlkv_map_num_q_heads(const mlkv_map* map) { return map ? map->h : -1; }
+int mlkv_map_num_kv_heads(const mlkv_map* map) { return map ? map->n_kv : -1; }
+
+int mlkv_map_kv_head(const mlkv_map* map, int layer, int q_head) {
+  if (!map || layer < 0 || layer >= map->l || q_head < 0 || q_head >= map->h) return -1;
+  return map->kv_of[static_cast<size_t>(layer) * map->h + q_head];
+}
+
+int mlkv_map_owner_layer(const mlkv_map* map, int kv) {
+  if (!map || kv < 0 || kv >= map->n_kv) return -1;
+  return map->owner_of[kv];
+}
+
+int mlkv_map_layer_kv_count(const mlkv_map* map, int layer) {
+  if (!map || layer < 0 || layer >= map->l) return -1;
+  return map->kv_count[layer];
+}
+
+int mlkv_map_layer_owned_count(const mlkv_map* map, int layer) {
+  if (!map || layer < 0 || layer >= map->l) return -1;
+  return map->own_count[layer];
+}
+
+int mlkv_map_layer_owned_begin(const mlkv_map* map, int layer) {
+  if (!map || layer < 0 || layer >= map->l) return -1;
+  return map->own_begin[layer];
+}
+
+size_t mlkv_cache_bytes(const mlkv_map* map, int batch, int capacity, int head_dim) {
+  if (!map || batch <= 0 || capacity <= 0 || head_dim <= 0) return 0;
+  return 2ull * static_cast<size_t>(batch) * capacity * map->n_kv * head_dim * 2ull;
+}
+
+size_t mlkv_workspace_bytes(const mlkv_map* map, int batch, int capacity, int head_dim) {
+  if (!map || batch <= 0 || capacity <= 0 || (head_dim != 64 && head_dim != 128)) return 0;
+  // The most splits any plan can produce: minimum tiles per split over the capacity.
+  const int ns_max = (tiles_of(capacity) + kMinTilesPerSplit - 1) / kMinTilesPerSplit;
+  return workspace_need(batch, map->h, head_dim, ns_max);
+}
+
+mlkv_status mlkv_plan_splits(const mlkv_map* map, int layer, int batch, int capacity, int head_dim,
+                             int max_len, int* tokens_per_split, int* n_splits) {
+  if (check_map(map) != MLKV_OK) return MLKV_ERR_INVALID_ARG;
+  if (layer < 0 || layer >= map->l) return fail(MLKV_ERR_INVALID_ARG, "layer out of range");
+  if (batch <= 0 || capacity <= 0 || !tokens_per_split || !n_splits)
+    return fail(MLKV_ERR_INVALID_ARG, "bad arguments");
+  if (head_dim != 64 && head_dim != 128) return fail(MLKV_ERR_UNSUPPORTED, "head_dim");
+  if (max_len <= 0) max_len = capacity;
+  if (max_len > capacity) return fail(MLKV_ERR_CAPACITY, "max_len above capacity");
+  int tps = 0, ns = 0;
+  plan(map, layer, batch, max_len, &tps, &ns);
+  *tokens_per_split = tps * kTileTokens;
+  *n_splits = ns;
+  return ok();
+}
+
+mlkv_status mlkv_cache_append(int layer, const mlkv_map* map, const mlkv_cache* cache,
+                              const void* k_new, const void* v_new, int new_row_stride,
+                              const int32_t* positions, hipStream_t stream) {
+  mlkv_status s;
+  if ((s = check_map(map)) != MLKV_OK) return s;
+  if (layer < 0 || layer >= map->l) return fail(MLKV_ERR_INVALID_ARG, "layer %d out of range", layer);
+  if ((s = check_cache(cache, map)) != MLKV_OK) return s;
+  const int owned = map->own_count[layer];
+  if (owned == 0) return ok();
+  if (!k_new || !v_new || !positions)
+    return fail(MLKV_ERR_INVALID_ARG, "k_new, v_new and positions must be non-NULL");
+  if (!aligned16(k_new) || !aligned16(v_new))
+    return fail(MLKV_ERR_ALIGNMENT, "k_new and v_new must be 16-byte aligned");
+  if (!aligned4(positions)) return fail(MLKV_ERR_ALIGNMENT, "positions must be 4-byte aligned");
+  if (new_row_stride % 8 != 0 || new_row_stride < owned * cache->head_dim)
+    return fail(MLKV_ERR_INVALID_ARG, "new_row_stride %d must be a multiple of 8 and >= %d",
+                new_row_stride, owned * cache->head_dim);
+  if ((s = append_impl(layer, map, cache, k_new, v_new, new_row_stride, positions, stream)) !=
+      MLKV_OK)
+    return s;
+  return ok();
+}
+
+mlkv_status mlkv_decode_attention(int layer, const void* q, const mlkv_cache* cache,
+                                  const mlkv_map* map, const int32_t* seq_lens, void* out,
+                                  mlkv_out_dtype out_dtype, int max_len_hint, void* workspace,
+                                  size_t workspace_bytes, hipStream_t stream) {
+  mlkv_status s;
+  if ((s = check_map(map)) != MLKV_OK) return s;
+  if (layer < 0 || layer >= map->l) return fail(MLKV_ERR_INVALID_ARG, "layer %d out of range", layer);
+  if ((s = check_cache(cache, map)) != MLKV_OK) return s;
+  if ((s = check_group_size(map, layer)) != MLKV_OK) return s;
+  if (!q || !seq_lens || !out) return fail(MLKV_ERR_INVALID_ARG, "q, seq_lens, out must be non-NULL");
+  if (!aligned16(q) || !aligned16(out)) return fail(MLKV_ERR_ALIGNMENT, "q and out must be 16-byte aligned");
+  if (!aligned4(seq_lens)) return fail(MLKV_ERR_ALIGNMENT, "seq_lens must be 4-byte aligned");
+  if (out_dtype != MLKV_OUT_F32 && out_dtype != MLKV_OUT_BF16)
+    return fail(MLKV_ERR_INVALID_ARG, "bad out_dtype");
+  if (max_len_hint > cache->capacity)
+    return fail(MLKV_ERR_CAPACITY, "max_len_hint %d above capacity %d", max_len_hint,
+                cache->capacity);
+  const int limit = max_len_hint <= 0 ? cache->capacity : max_len_hint;
+  if ((s = check_lengths_if_requested(seq_lens, cache->batch, 0, limit, stream)) != MLKV_OK) return s;
+  if ((s = attention_impl(layer, q, cache, map, seq_lens, 0, out, out_dtype, max_len_hint,
+                          workspace, workspace_bytes, stream)) != MLKV_OK)
+    return s;
+  return ok();
+}
+
+mlkv_status mlkv_decode_step(const void* q_all, const void* k_new_all, const void* v_new_all,
+                             const mlkv_cache* cache, const mlkv_map* map, const int32_t* ctx_lens,
+                             void* out_all, mlkv_out_dtype out_dtype, int max_len_hint,
+                             void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  mlkv_status s;
+  if ((s = check_map(map)) != MLKV_OK) return s;
+  if ((s = check_cache(cache, map)) != MLKV_OK) return s;
+  for (int n = 0; n < map->l; ++n)
+    if ((s = check_group_size(map, n)) != MLKV_OK) return s;
+  if (!q_all || !k_new_all || !v_new_all || !ctx_lens || !out_all)
+    return fail(MLKV_ERR_INVALID_ARG, "q_all, k_new_all, v_new_all, ctx_lens, out_all must be non-NULL");
+  if (!aligned16(q_all) || !aligned16(k_new_all) || !aligned16(v_new_all) || !aligned16(out_all))
+    return fail(MLKV_ERR_ALIGNMENT, "q_all, k/v_new_all and out_all must be 16-byte aligned");
+  if (!aligned4(ctx_lens)) return fail(MLKV_ERR_ALIGNMENT, "ctx_lens must be 4-byte aligned");
+  if (out_dtype != MLKV_OUT_F32 && out_dtype != MLKV_OUT_BF16)
+    return fail(MLKV_ERR_INVALID_ARG, "bad out_dtype");
+  if (max_len_hint > cache->capacity)
+    return fail(MLKV_ERR_CAPACITY, "max_len_hint %d above capacity %d", max_len_hint,
+                cache->capacity);
+  const int B = cache->batch, h = map->h, D = cache->head_dim, n_kv = map->n_kv;
+  // Workspace check up front so that no layer is half-launched.
+  {
+    const int max_len = max_len_hint <= 0 ? cache->capacity : max_len_hint;
+    for (int n = 0; n < map->l; ++n) {
+      int tps = 0, ns = 0;
+      plan(map, n, B, max_len, &tps, &ns);
+      const size_t need = workspace_need(B, h, D, ns);
+      if (need > 0 && (!workspace || workspace_bytes < need))
+        return fail(MLKV_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need,
+                    workspace ? workspace_bytes : 0);
+    }
+    if (workspace && !aligned16(workspace))
+      return fail(MLKV_ERR_ALIGNMENT, "workspace not 16-byte aligned");
+  }
+  const int limit = (max_len_hint <= 0 ? cache->capacity : max_len_hint);
+  if ((s = check_lengths_if_requested(ctx_lens, B, 1, limit, stream)) != MLKV_OK) return s;
+  const size_t layer_elems = static_cast<size_t>(B) * h * D;
+  const size_t out_elem_bytes = out_dtype == MLKV_OUT_BF16 ? 2 : 4;
+  const uint16_t* k_new = static_cast<const uint16_t*>(k_new_all);
+  const uint16_t* v_new = static_cast<const uint16_t*>(v_new_all);
+  for (int n = 0; n < map->l; ++n) {
+    if (map->own_count[n] > 0) {
+      const size_t col = static_cast<size_t>(map->own_begin[n]) * D;
+      if ((s = append_impl(n, map, cache, k_new + col, v_new + col, n_kv * D, ctx_lens, stream)) !=
+          MLKV_OK)
+        return s;
+    }
+    const void* q = static_cast<const uint16_t*>(q_all) + layer_elems * n;
+    void* out = static_cast<char*>(out_all) + layer_elems * out_elem_bytes * n;
+    if ((s = attention_impl(n, q, cache, map, ctx_lens, 1, out, out_dtype, max_len_hint, workspace,
+                            workspace_bytes, stream)) != MLKV_OK)
+      return s;
+  }
+  return ok();
+}
+
+}  // extern "C"

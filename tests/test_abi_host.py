@@ -1,0 +1,155 @@
+"""Host-side checks of the C-ABI library that need no GPU: it loads, exports
+every symbol include/mlkv.h declares, builds maps that agree with the oracle,
+and rejects bad arguments before any HIP call."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+from test_oracle import _read_table
+
+mlkv = pytest.importorskip("paper_2406_09297_amd")
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _header_symbols():
+    text = open(os.path.join(ROOT, "include", "mlkv.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(mlkv_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    L = mlkv.lib()
+    declared = _header_symbols()
+    assert len(declared) >= 19
+    for name in declared:
+        assert hasattr(L, name), f"{name} declared in mlkv.h but not exported"
+    assert sorted(mlkv.EXPORTS) == declared
+
+
+@pytest.mark.parametrize("row", _read_table("table2_variants.txt"), ids=lambda r: r[0])
+def test_uniform_map_agrees_with_oracle(row):
+    l, h, m, g, mg = map(int, row[1:])
+    mp = mlkv.Map.uniform(l, h, m, g)
+    kv_of, owner_of = oracle.map_uniform(l, h, m, g)
+    assert mp.n_kv == mg
+    assert np.array_equal(mp.kv_of(), kv_of)
+    assert np.array_equal(mp.owner_of(), owner_of)
+    for n in range(l):
+        assert mp.layer_kv_count(n) == g
+        begin, count = mp.layer_owned(n)
+        owned = [kv for kv in range(mg) if owner_of[kv] == n]
+        assert count == len(owned)
+        if owned:
+            assert begin == owned[0]
+    assert mp.cache_bytes(8, 1024, 64) == 2 * oracle.cache_elements("mlkv", 8, 1024, l, h, 64, m=m, g=g)
+
+
+def test_general_map_accepts_nonuniform_layer_sharing():
+    # 5 layers: KV head 0 shared by layers 0-1, head 1 by 2-4 (two-head GQA in layer 2..4)
+    kv_of = np.array([[0, 0, 0, 0], [0, 0, 0, 0], [1, 1, 2, 2], [1, 1, 2, 2], [1, 1, 2, 2]])
+    mp = mlkv.Map.from_tables(kv_of, [0, 2, 2])
+    assert mp.n_kv == 3 and mp.layer_owned(2) == (1, 2) and mp.layer_owned(1) == (-1, 0)
+
+
+@pytest.mark.parametrize("kv_of,owner_of,why", [
+    ([[0, 0], [1, 1]], [1, 1], "reader before owner"),
+    ([[0, 1], [1, 0]], [0, 0], "non-contiguous grouping"),
+    ([[0, 0], [0, 0]], [0, 0], "head 1 never read"),
+    ([[0, 0], [2, 2]], [0, 1], "out of range"),
+    ([[0, 0, 0], [1, 2, 3]], [0, 1, 1, 1], "3 KV heads do not divide h=3? (they do) but owner ok"),
+])
+def test_general_map_rejections(kv_of, owner_of, why):
+    kv_of = np.array(kv_of)
+    if why.startswith("3 KV heads"):
+        mp = mlkv.Map.from_tables(kv_of, owner_of)  # valid: h=3, c=3, G=1
+        assert mp.layer_kv_count(1) == 3
+        return
+    with pytest.raises(mlkv.MLKVError) as e:
+        mlkv.Map.from_tables(kv_of, owner_of)
+    assert e.value.status_name == "MLKV_ERR_BAD_MAP", why
+
+
+def test_owned_heads_must_be_contiguous():
+    kv_of = np.array([[0, 1], [2, 2], [0, 1]])
+    with pytest.raises(mlkv.MLKVError):
+        mlkv.Map.from_tables(kv_of, [0, 1, 0])
+
+
+def _fake_cache(n_kv=4, B=2, S=64, D=64, k=0x10000, v=0x20000):
+    c = mlkv._Cache(k, v, n_kv, B, S, D)
+    return ctypes.byref(c), c
+
+
+@pytest.mark.parametrize("mutate,expect", [
+    (dict(S=48), "MLKV_ERR_CAPACITY"),
+    (dict(D=96), "MLKV_ERR_UNSUPPORTED"),
+    (dict(k=0x10008), "MLKV_ERR_ALIGNMENT"),
+    (dict(v=0), "MLKV_ERR_INVALID_ARG"),
+    (dict(n_kv=3), "MLKV_ERR_INVALID_ARG"),
+    (dict(B=0), "MLKV_ERR_INVALID_ARG"),
+])
+def test_decode_attention_rejects_bad_cache_before_any_hip_call(mutate, expect):
+    mp = mlkv.Map.uniform(12, 12, 4, 1)
+    args = dict(n_kv=4, B=2, S=64, D=64, k=0x10000, v=0x20000)
+    args.update(mutate)
+    ref, _keep = _fake_cache(**args)
+    L = mlkv.lib()
+    st = L.mlkv_decode_attention(0, 0x30000, ref, mp.handle, 0x40000, 0x50000, 0, 0, 0x60000,
+                                 1 << 30, None)
+    assert mlkv.STATUS_NAMES[st] == expect
+    assert L.mlkv_last_error().decode()
+
+
+def test_entry_points_reject_bad_arguments():
+    mp = mlkv.Map.uniform(12, 12, 4, 1)
+    ref, _keep = _fake_cache()
+    L = mlkv.lib()
+    names = mlkv.STATUS_NAMES
+    # null map / layer out of range / null pointers / misalignment / bad dtype / hint > capacity
+    assert names[L.mlkv_decode_attention(0, 0x30000, ref, None, 0x40000, 0x50000, 0, 0, 0x60000, 1 << 30, None)] == "MLKV_ERR_INVALID_ARG"
+    assert names[L.mlkv_decode_attention(12, 0x30000, ref, mp.handle, 0x40000, 0x50000, 0, 0, 0x60000, 1 << 30, None)] == "MLKV_ERR_INVALID_ARG"
+    assert names[L.mlkv_decode_attention(0, None, ref, mp.handle, 0x40000, 0x50000, 0, 0, 0x60000, 1 << 30, None)] == "MLKV_ERR_INVALID_ARG"
+    assert names[L.mlkv_decode_attention(0, 0x30004, ref, mp.handle, 0x40000, 0x50000, 0, 0, 0x60000, 1 << 30, None)] == "MLKV_ERR_ALIGNMENT"
+    assert names[L.mlkv_decode_attention(0, 0x30000, ref, mp.handle, 0x40002, 0x50000, 0, 0, 0x60000, 1 << 30, None)] == "MLKV_ERR_ALIGNMENT"
+    assert names[L.mlkv_decode_attention(0, 0x30000, ref, mp.handle, 0x40000, 0x50000, 7, 0, 0x60000, 1 << 30, None)] == "MLKV_ERR_INVALID_ARG"
+    assert names[L.mlkv_decode_attention(0, 0x30000, ref, mp.handle, 0x40000, 0x50000, 0, 65, 0x60000, 1 << 30, None)] == "MLKV_ERR_CAPACITY"
+    # a workspace that is too small is refused (B=2, 64 tokens plans 1 split: no workspace)
+    big = mlkv._Cache(0x10000, 0x20000, 4, 2, 4096, 64)
+    assert names[L.mlkv_decode_attention(0, 0x30000, ctypes.byref(big), mp.handle, 0x40000, 0x50000, 0, 0, 0x60000, 16, None)] == "MLKV_ERR_WORKSPACE"
+    assert names[L.mlkv_decode_step(0x30000, 0x30000, 0x30000, ctypes.byref(big), mp.handle, 0x40000, 0x50000, 0, 0, None, 0, None)] == "MLKV_ERR_WORKSPACE"
+    # append: null pointers and bad row stride on an owning layer; non-owner is a no-op
+    assert names[L.mlkv_cache_append(0, mp.handle, ref, None, 0x30000, 64, 0x40000, None)] == "MLKV_ERR_INVALID_ARG"
+    assert names[L.mlkv_cache_append(0, mp.handle, ref, 0x30000, 0x30000, 60, 0x40000, None)] == "MLKV_ERR_INVALID_ARG"
+    assert names[L.mlkv_cache_append(0, mp.handle, ref, 0x30008, 0x30000, 64, 0x40000, None)] == "MLKV_ERR_ALIGNMENT"
+    assert names[L.mlkv_cache_append(1, mp.handle, ref, None, None, 0, None, None)] == "MLKV_OK"
+    # group size above 16 query heads per KV head is reported as unsupported
+    mq = mlkv.Map.uniform(2, 32, 2, 1)
+    c2 = mlkv._Cache(0x10000, 0x20000, 2, 2, 64, 64)
+    assert names[L.mlkv_decode_attention(0, 0x30000, ctypes.byref(c2), mq.handle, 0x40000, 0x50000, 0, 0, 0x60000, 1 << 30, None)] == "MLKV_ERR_UNSUPPORTED"
+
+
+def test_workspace_covers_every_plan():
+    mp = mlkv.Map.uniform(12, 12, 4, 1)
+    for B, S in [(1, 160), (8, 32832), (128, 2112), (32, 2112)]:
+        ws = mp.workspace_bytes(B, S, 64)
+        for max_len in [x for x in (1, 31, 33, 129, 511, 513, S // 2, S) if x <= S]:
+            tps, ns = mp.plan_splits(0, B, S, 64, max_len)
+            assert tps % 32 == 0 and ns >= 1 and tps * ns >= max_len
+            need = 0 if ns == 1 else B * 12 * ns * (64 + 2) * 4
+            assert need <= ws
+
+
+def test_layout_reference_matches_binding_packer():
+    rng = np.random.default_rng(0)
+    n_kv, B, S, D = 2, 3, 64, 64
+    rows = rng.integers(0, 65535, size=(n_kv, B, S, D), dtype=np.uint16)
+    import layout_ref
+    packed = mlkv.pack_value_rows(rows)
+    assert np.array_equal(layout_ref.unpack_v(packed, n_kv, B, S, D), rows)
+    for _ in range(100):
+        kv, b, t, d = rng.integers(n_kv), rng.integers(B), rng.integers(S), rng.integers(D)
+        assert packed.reshape(-1)[layout_ref.v_index(kv, b, t, d, B, S, D)] == rows[kv, b, t, d]

@@ -1,0 +1,269 @@
+"""GPU parity of the HIP path against the fp64 oracle, through the C ABI.
+
+Cache writes are compared bit for bit; attention outputs within the
+tolerances stated in gpu_util.  Every case prints its name before touching the
+GPU so that a failure names it.
+"""
+import os
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+import oracle  # noqa: E402
+import synth  # noqa: E402
+from gpu_util import DeviceWorkload, check_close, f64, say  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+mlkv = pytest.importorskip("paper_2406_09297_amd")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    mlkv.lib()
+    yield
+
+
+def small(name, **kw):
+    return synth.get_workload(name).scaled(**kw)
+
+
+# ------------------------------------------------------------------ append --
+
+@pytest.mark.parametrize("wname,kw", [
+    ("mlkv4_b128_ragged", dict(B=5, ctx=300)),
+    ("7b_mlkv8x8", dict(B=3, ctx=100)),
+    ("sweep_b32", dict(B=2, ctx=70)),
+])
+def test_append_bit_exact(wname, kw):
+    w = small(wname, **kw)
+    say(f"append {w.name} B={w.B} D={w.D} n_kv={w.n_kv}")
+    dw = DeviceWorkload(w, fill=synth.BF16_NAN)
+    k_ref, v_ref = dw.host["k_cache"].copy(), dw.host["v_cache"].copy()
+    pos = dw.host["ctx"].copy()
+    pos[0] = -1           # skipped
+    if w.B > 1:
+        pos[1] = dw.S     # skipped (out of range)
+    pos_d = torch.from_numpy(pos).cuda()
+    for layer in range(w.l):
+        begin, count = dw.map.layer_owned(layer)
+        if count:
+            kn = dw.k_new[:, begin:begin + count].contiguous()
+            vn = dw.v_new[:, begin:begin + count].contiguous()
+            mlkv.cache_append(layer, dw.map, dw.cache, kn, vn, pos_d)
+        oracle.append(layer, k_ref, v_ref, dw.host["k_new"], dw.host["v_new"], dw.owner_of, pos)
+    k_gpu, v_gpu = dw.read_cache()
+    assert np.array_equal(k_gpu, k_ref)
+    assert np.array_equal(v_gpu, v_ref)
+
+
+# ----------------------------------------------------------- one layer ------
+
+@pytest.mark.parametrize("wname,kw,layers", [
+    ("mlkv2_b1", {}, [0, 5, 6, 11]),
+    ("mlkv4_b128_ragged", dict(B=16, ctx=700), [0, 1, 4]),
+    ("mlkv4_b8_long", dict(B=2, ctx=3000), [0, 7]),
+    ("7b_mlkv8x8", dict(B=4, ctx=600), [0, 3, 29]),
+])
+def test_decode_attention_matches_oracle(wname, kw, layers):
+    w = small(wname, **kw)
+    dw = DeviceWorkload(w)
+    lens = dw.host["ctx"].copy()
+    lens_d = torch.from_numpy(lens).cuda()
+    for n in layers:
+        say(f"decode_attention {w.name} layer={n} B={w.B} D={w.D} G={w.h // w.g}")
+        out = torch.empty((w.B, w.h, w.D), dtype=torch.float32, device="cuda")
+        mlkv.decode_attention(n, dw.q[n], dw.cache, dw.map, lens_d, out, ws=dw.ws)
+        torch.cuda.synchronize()
+        ref = oracle.decode_attention(n, dw.host["q"][n], dw.host["k_cache"], dw.host["v_cache"],
+                                      dw.kv_of, lens)
+        check_close(out.cpu().numpy(), ref, f"{w.name} L{n}")
+
+
+def _sweep_workload(D, m, g, lens, h=12, l=4, k_scale=1.0, seed=99):
+    B = len(lens)
+    w = synth.Workload("sweep", l=l, h=h, m=m, g=g, D=D, B=B, ctx=int(max(lens)), k_scale=k_scale,
+                       seed=seed)
+    return w
+
+
+LEN_SWEEP = [1, 2, 7, 31, 32, 33, 63, 64, 65, 96, 127, 128, 129, 160, 191, 255, 256, 257, 300]
+
+
+@pytest.mark.parametrize("D,m,g", [(64, 4, 1), (64, 4, 3), (128, 2, 4), (64, 2, 12)])
+def test_length_sweep_across_tile_boundaries(D, m, g):
+    w = _sweep_workload(D, m, g, LEN_SWEEP)
+    dw = DeviceWorkload(w)
+    lens = np.array(LEN_SWEEP, dtype=np.int32)
+    lens_d = torch.from_numpy(lens).cuda()
+    for split_tokens in ("", "128", "256"):
+        os.environ["MLKV_SPLIT_TOKENS"] = split_tokens
+        try:
+            for n in (0, w.l - 1):
+                say(f"length sweep D={D} m={m} g={g} layer={n} split={split_tokens or 'auto'}")
+                out = torch.empty((w.B, w.h, w.D), dtype=torch.float32, device="cuda")
+                mlkv.decode_attention(n, dw.q[n], dw.cache, dw.map, lens_d, out, ws=dw.ws)
+                torch.cuda.synchronize()
+                ref = oracle.decode_attention(n, dw.host["q"][n], dw.host["k_cache"],
+                                              dw.host["v_cache"], dw.kv_of, lens)
+                check_close(out.cpu().numpy(), ref, f"sweep D{D} g{g} L{n} s{split_tokens}")
+        finally:
+            os.environ.pop("MLKV_SPLIT_TOKENS", None)
+
+
+def test_split_count_invariance_and_determinism():
+    w = small("mlkv4_b8_long", B=2, ctx=5000)
+    dw = DeviceWorkload(w)
+    lens_d = torch.from_numpy(dw.host["ctx"]).cuda()
+    outs = {}
+    for split_tokens in ("128", "512", "2048", "8192", ""):
+        os.environ["MLKV_SPLIT_TOKENS"] = split_tokens
+        try:
+            say(f"split invariance split={split_tokens or 'auto'}")
+            o = torch.empty((w.B, w.h, w.D), dtype=torch.float32, device="cuda")
+            mlkv.decode_attention(2, dw.q[2], dw.cache, dw.map, lens_d, o, ws=dw.ws)
+            o2 = torch.empty_like(o)
+            mlkv.decode_attention(2, dw.q[2], dw.cache, dw.map, lens_d, o2, ws=dw.ws)
+            torch.cuda.synchronize()
+            assert torch.equal(o, o2), "run-to-run results differ"
+            outs[split_tokens] = o.cpu().numpy().astype(np.float64)
+        finally:
+            os.environ.pop("MLKV_SPLIT_TOKENS", None)
+    ref = oracle.decode_attention(2, dw.host["q"][2], dw.host["k_cache"], dw.host["v_cache"],
+                                  dw.kv_of, dw.host["ctx"])
+    for k, o in outs.items():
+        check_close(o, ref, f"split {k or 'auto'}")
+
+
+def test_single_position_and_empty():
+    """L = 1 returns v exactly (one weight of exactly 1); L = 0 returns zeros."""
+    w = _sweep_workload(64, 2, 3, [1, 0, 1, 0], h=6, l=2)
+    dw = DeviceWorkload(w)
+    lens = np.array([1, 0, 1, 0], np.int32)
+    say("single position / empty")
+    out = torch.full((w.B, w.h, w.D), 7.0, dtype=torch.float32, device="cuda")
+    mlkv.decode_attention(1, dw.q[1], dw.cache, dw.map, torch.from_numpy(lens).cuda(), out,
+                          ws=dw.ws)
+    torch.cuda.synchronize()
+    out = out.cpu().numpy()
+    for b in range(w.B):
+        for i in range(w.h):
+            kv = dw.kv_of[1, i]
+            if lens[b] == 1:
+                assert np.array_equal(out[b, i], f64(dw.host["v_cache"][kv, b, 0]).astype(np.float32))
+            else:
+                assert np.all(out[b, i] == 0)
+
+
+@pytest.mark.parametrize("pos_kind", ["first", "tile_end", "tile_start", "split_edge", "last"])
+def test_needle_token(pos_kind):
+    """A key aligned with q and scaled up takes (almost) all weight: o = v_needle
+    to bf16 weight precision.  Catches dropped or duplicated tokens."""
+    L = 1200
+    w = _sweep_workload(64, 1, 1, [L, L], h=12, l=1, seed=123)
+    dw = DeviceWorkload(w)
+    pos = {"first": 0, "tile_end": 31, "tile_start": 32, "split_edge": 511, "last": L - 1}[pos_kind]
+    b, head = 1, 7
+    q = dw.host["q"][0, b, head]
+    kc = dw.host["k_cache"]
+    kc[0, b, pos] = synth.f32_to_bf16(synth.bf16_to_f32(q) * 4.0)
+    dw.cache.load_rows(kc, dw.host["v_cache"])
+    os.environ["MLKV_SPLIT_TOKENS"] = "512"
+    try:
+        say(f"needle at {pos} ({pos_kind})")
+        out = torch.empty((w.B, w.h, w.D), dtype=torch.float32, device="cuda")
+        lens = np.array([L, L], np.int32)
+        mlkv.decode_attention(0, dw.q[0], dw.cache, dw.map, torch.from_numpy(lens).cuda(), out,
+                              ws=dw.ws)
+        torch.cuda.synchronize()
+    finally:
+        os.environ.pop("MLKV_SPLIT_TOKENS", None)
+    ref = oracle.decode_attention(0, dw.host["q"][0], kc, dw.host["v_cache"], dw.kv_of, lens)
+    _, alpha = oracle.attend_one(q, kc[0, b, :L], dw.host["v_cache"][0, b, :L])
+    assert alpha[pos] > 0.99
+    check_close(out.cpu().numpy(), ref, f"needle {pos_kind}")
+
+
+def test_bf16_output_is_the_rounded_fp32_result():
+    """bf16 output mode returns exactly the RNE rounding of the fp32 result of the
+    same (deterministic) computation, and stays within the tolerances of the
+    oracle once its own rounding (half a bf16 ulp) is allowed for."""
+    w = small("mlkv4_b128_ragged", B=8, ctx=900)
+    dw = DeviceWorkload(w)
+    lens = torch.from_numpy(dw.host["ctx"]).cuda()
+    say("bf16 output")
+    out16 = torch.empty((w.B, w.h, w.D), dtype=torch.bfloat16, device="cuda")
+    out32 = torch.empty((w.B, w.h, w.D), dtype=torch.float32, device="cuda")
+    mlkv.decode_attention(3, dw.q[3], dw.cache, dw.map, lens, out16, ws=dw.ws)
+    mlkv.decode_attention(3, dw.q[3], dw.cache, dw.map, lens, out32, ws=dw.ws)
+    torch.cuda.synchronize()
+    bits = mlkv.bf16_bits(out16)
+    assert np.array_equal(bits, synth.f32_to_bf16(out32.cpu().numpy()))
+    ref = oracle.decode_attention(3, dw.host["q"][3], dw.host["k_cache"], dw.host["v_cache"],
+                                  dw.kv_of, dw.host["ctx"])
+    got = f64(bits)
+    d = np.abs(got - ref)
+    assert np.all(d <= 1e-2 + np.abs(ref) * 2.0**-8), d.max()
+    assert d.mean() <= 1e-3
+
+
+# -------------------------------------------------------------- whole step --
+
+def _run_step(dw, out_dtype=torch.float32):
+    w = dw.w
+    out = torch.empty((w.l, w.B, w.h, w.D), dtype=out_dtype, device="cuda")
+    mlkv.decode_step(dw.q, dw.k_new, dw.v_new, dw.cache, dw.map, dw.ctx, out, ws=dw.ws)
+    torch.cuda.synchronize()
+    return out
+
+
+def _oracle_step(dw):
+    k, v = dw.host["k_cache"].copy(), dw.host["v_cache"].copy()
+    out = oracle.decode_step(dw.host["q"], k, v, dw.host["k_new"], dw.host["v_new"], dw.kv_of,
+                             dw.owner_of, dw.host["ctx"])
+    return out, k, v
+
+
+def test_step_mlkv2_empty_context_outputs_new_value_exactly():
+    w = synth.Workload("mlkv2_ctx0", l=12, h=12, m=2, g=1, D=64, B=3, ctx=0, seed=5)
+    dw = DeviceWorkload(w)
+    say("step MLKV-2 ctx=0")
+    out = _run_step(dw).cpu().numpy()
+    for n in range(12):
+        for b in range(3):
+            for i in range(12):
+                assert np.array_equal(out[n, b, i],
+                                      f64(dw.host["v_new"][b, n // 6]).astype(np.float32))
+
+
+@pytest.mark.parametrize("wname", ["mlkv2_b1", "mlkv4_b128_ragged", "mlkv4_b8_long"])
+def test_full_size_step_matches_oracle(wname):
+    """Full-size workloads in the launch configuration the benchmark times."""
+    w = synth.get_workload(wname)
+    say(f"full step {wname}: uploading")
+    dw = DeviceWorkload(w)
+    say(f"full step {wname}: running")
+    out = _run_step(dw).cpu().numpy()
+    k_gpu, v_gpu = dw.read_cache()
+    say(f"full step {wname}: oracle")
+    ref, k_ref, v_ref = _oracle_step(dw)
+    assert np.array_equal(k_gpu, k_ref) and np.array_equal(v_gpu, v_ref), "cache differs"
+    check_close(out, ref, f"step {wname}")
+
+
+@pytest.mark.parametrize("mg", [(12, 12), (12, 4), (12, 1), (6, 1), (4, 1), (1, 1)])
+def test_map_sweep_full_size(mg):
+    w = synth.get_workload("sweep_b32").with_map(*mg)
+    say(f"sweep step {w.name}: uploading")
+    dw = DeviceWorkload(w)
+    say(f"sweep step {w.name}: running")
+    out = _run_step(dw).cpu().numpy()
+    k_gpu, v_gpu = dw.read_cache()
+    say(f"sweep step {w.name}: oracle")
+    ref, k_ref, v_ref = _oracle_step(dw)
+    assert np.array_equal(k_gpu, k_ref) and np.array_equal(v_gpu, v_ref), "cache differs"
+    check_close(out, ref, f"step {w.name}")
