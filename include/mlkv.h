@@ -130,8 +130,15 @@ typedef struct {
 size_t mlkv_cache_bytes(const mlkv_map* map, int batch, int capacity, int head_dim);
 
 /* Device workspace needed by mlkv_decode_attention / mlkv_decode_step for any
- * max_len_hint <= capacity (split-K partial results).  0 for invalid args. */
+ * max_len_hint <= capacity (split-K partial results and per-sequence split
+ * counters).  0 for invalid args. */
 size_t mlkv_workspace_bytes(const mlkv_map* map, int batch, int capacity, int head_dim);
+
+/* Zero-fill a workspace before its first use (a fill kernel enqueued on
+ * `stream`, no memset, so it may be captured in a graph).  Every decode call
+ * leaves the workspace's counters at zero again, so this is needed once per
+ * allocation.  Calls that share one workspace must be ordered on one stream. */
+mlkv_status mlkv_workspace_init(void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
  * Append the newest token of `layer` (Section 2.4) into the KV heads that
@@ -158,9 +165,12 @@ mlkv_status mlkv_cache_append(int layer, const mlkv_map* map, const mlkv_cache* 
  *   max_len_hint: an upper bound of every L_b (<= 0 means capacity); it sizes
  *        the split-K grid.  Lengths above it are truncated to it.
  *   workspace: device memory of at least mlkv_workspace_bytes(...) bytes,
- *        16-byte aligned; contents need no initialisation and are clobbered.
+ *        16-byte aligned, zeroed once by mlkv_workspace_init (the split
+ *        counters must start at zero; each call returns them to zero).
  * Every query head mapped to one KV head is served from a single pass over
- * that head's cache rows.
+ * that head's cache rows; long sequences are split across workgroups and the
+ * last workgroup of a sequence to finish merges the splits in a fixed order
+ * (results are bitwise reproducible).
  */
 mlkv_status mlkv_decode_attention(int layer, const void* q, const mlkv_cache* cache,
                                   const mlkv_map* map, const int32_t* seq_lens, void* out,

@@ -19,7 +19,8 @@ import numpy as np
 import torch  # loaded first: the library then binds to torch's HIP runtime
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libmlkv.so")
+# MLKV_LIBRARY may name another build of the same library (e.g. for A/B timing).
+LIB_PATH = os.environ.get("MLKV_LIBRARY") or os.path.join(_HERE, "libmlkv.so")
 
 MLKV_OK = 0
 STATUS_NAMES = ["MLKV_OK", "MLKV_ERR_INVALID_ARG", "MLKV_ERR_BAD_MAP", "MLKV_ERR_ALIGNMENT",
@@ -35,7 +36,7 @@ EXPORTS = [
     "mlkv_map_kv_head", "mlkv_map_owner_layer", "mlkv_map_layer_kv_count",
     "mlkv_map_layer_owned_count", "mlkv_map_layer_owned_begin", "mlkv_cache_bytes",
     "mlkv_workspace_bytes", "mlkv_cache_append", "mlkv_decode_attention", "mlkv_decode_step",
-    "mlkv_plan_splits",
+    "mlkv_plan_splits", "mlkv_workspace_init",
 ]
 
 
@@ -84,6 +85,7 @@ def lib():
             "mlkv_decode_attention": ([I, P, P, P, P, P, I, I, P, Z, P], S),
             "mlkv_decode_step": ([P, P, P, P, P, P, P, I, I, P, Z, P], S),
             "mlkv_plan_splits": ([P, I, I, I, I, I, ctypes.POINTER(I), ctypes.POINTER(I)], S),
+            "mlkv_workspace_init": ([P, Z, P], S),
         }
         for name, (args, res) in sig.items():
             f = getattr(L, name)
@@ -252,9 +254,13 @@ def bf16_bits(t: torch.Tensor) -> np.ndarray:
     return t.detach().contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
 
 
-def workspace(map_: Map, batch: int, capacity: int, head_dim: int, device="cuda") -> torch.Tensor:
+def workspace(map_: Map, batch: int, capacity: int, head_dim: int, device="cuda",
+              stream=None) -> torch.Tensor:
+    """Allocate and initialise (mlkv_workspace_init) a decode workspace."""
     n = map_.workspace_bytes(batch, capacity, head_dim)
-    return torch.empty(max(n, 16), dtype=torch.uint8, device=device)
+    ws = torch.empty(max(n, 16), dtype=torch.uint8, device=device)
+    _check(lib().mlkv_workspace_init(ws.data_ptr(), ws.numel(), _stream(stream)))
+    return ws
 
 
 # --------------------------------------------------------------- entry points

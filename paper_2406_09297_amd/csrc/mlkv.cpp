@@ -125,25 +125,37 @@ mlkv_status check_cache(const mlkv_cache* c, const mlkv_map* map) {
 
 int tiles_of(int len) { return (len + kTileTokens - 1) / kTileTokens; }
 
+// Split-K plan for one layer.  Each workgroup (four waves) streams one split
+// of tiles_per_split 32-token tiles of one (sequence, KV head).  Short
+// sequences (<= 16 tiles) take one split: no partials, no merge.  Otherwise
+// the split is the longest of 64/32/16/8/4 tiles that still gives at least
+// kTargetWorkgroups workgroups, lengthened again while a sequence would have
+// more than kPreferredMaxSplits splits (merge cost grows with the count).
+constexpr int kPreferredMaxSplits = 64;
+constexpr int kMaxSplits = 256;  // the attention kernel's per-sequence limit
+
 void plan(const mlkv_map* map, int layer, int batch, int max_len, int* tps_out, int* ns_out) {
   const int max_tiles = tiles_of(max_len < 1 ? 1 : max_len);
   const long units = static_cast<long>(batch) * map->kv_count[layer];
-  int tps = kMinTilesPerSplit;
+  int tps;
   const char* env = std::getenv("MLKV_SPLIT_TOKENS");
   if (env && *env) {
-    int tok = std::atoi(env);
-    tps = tok / kTileTokens;
+    tps = std::atoi(env) / kTileTokens;
     tps = (tps / kMinTilesPerSplit) * kMinTilesPerSplit;
     if (tps < kMinTilesPerSplit) tps = kMinTilesPerSplit;
+  } else if (max_tiles <= 4 * kMinTilesPerSplit) {
+    tps = max_tiles;
   } else {
+    tps = kMinTilesPerSplit;
     for (int cand = 64; cand >= kMinTilesPerSplit; cand /= 2) {
-      const long splits = (max_tiles + cand - 1) / cand;
-      if (units * splits >= kTargetWorkgroups) {
+      if (units * ((max_tiles + cand - 1) / cand) >= kTargetWorkgroups) {
         tps = cand;
         break;
       }
     }
+    while ((max_tiles + tps - 1) / tps > kPreferredMaxSplits) tps *= 2;
   }
+  while ((max_tiles + tps - 1) / tps > kMaxSplits) tps *= 2;
   int ns = (max_tiles + tps - 1) / tps;
   if (ns < 1) ns = 1;
   if (ns == 1) tps = max_tiles < 1 ? 1 : max_tiles;  // one split: exactly the needed tiles
@@ -153,11 +165,19 @@ void plan(const mlkv_map* map, int layer, int batch, int max_len, int* tps_out, 
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
-// Workspace layout for one call: part_acc then (256-aligned) part_ml.
+// Workspace layout of one call (nothing when every sequence fits one split):
+//   counters  int32 [batch * h]                 (256-byte aligned blocks)
+//   part_acc  fp32  [batch * h * n_split][head_dim]
+//   part_ml   fp32  [batch * h * n_split][2]
+size_t counters_bytes(int batch, int h) {
+  return align_up(static_cast<size_t>(batch) * h * sizeof(int32_t), 256);
+}
+
 size_t workspace_need(int batch, int h, int head_dim, int n_split) {
   if (n_split <= 1) return 0;
   const size_t rows = static_cast<size_t>(batch) * h * n_split;
-  return align_up(rows * head_dim * sizeof(float), 256) + rows * 2 * sizeof(float);
+  return counters_bytes(batch, h) + align_up(rows * head_dim * sizeof(float), 256) +
+         rows * 2 * sizeof(float);
 }
 
 mlkv_status check_lengths_if_requested(const int32_t* lens, int batch, int offset, int limit,
@@ -196,9 +216,11 @@ mlkv_status attention_impl(int layer, const void* q, const mlkv_cache* cache, co
   p.lens = lens;
   p.out = out;
   const size_t rows = static_cast<size_t>(B) * map->h * ns;
-  p.part_acc = need ? static_cast<float*>(ws) : nullptr;
-  p.part_ml = need ? reinterpret_cast<float*>(static_cast<char*>(ws) +
-                                              align_up(rows * D * sizeof(float), 256))
+  char* base = static_cast<char*>(ws);
+  const size_t cnt = counters_bytes(B, map->h);
+  p.counters = need ? reinterpret_cast<int*>(base) : nullptr;
+  p.part_acc = need ? reinterpret_cast<float*>(base + cnt) : nullptr;
+  p.part_ml = need ? reinterpret_cast<float*>(base + cnt + align_up(rows * D * sizeof(float), 256))
                    : nullptr;
   p.B = B;
   p.h = map->h;
@@ -211,6 +233,11 @@ mlkv_status attention_impl(int layer, const void* q, const mlkv_cache* cache, co
   p.len_offset = len_offset;
   p.out_bf16 = dt == MLKV_OUT_BF16 ? 1 : 0;
   p.scale_log2 = static_cast<float>(1.4426950408889634 / std::sqrt(static_cast<double>(D)));
+  // Split merge: a separate combine kernel by default; MLKV_COMBINE=fused lets
+  // the last workgroup of each sequence merge in place where the partials fit.
+  const bool fits = static_cast<long>(ns) * map->group[layer] * D <= mlkv::fused_partial_capacity();
+  const char* comb = std::getenv("MLKV_COMBINE");
+  p.fused_combine = fits && comb && std::strcmp(comb, "fused") == 0 ? 1 : 0;
   const hipError_t err = mlkv::launch_attention(p, D, stream);
   if (err != hipSuccess) return fail(MLKV_ERR_HIP, "attention launch: %s", hipGetErrorString(err));
   return MLKV_OK;
@@ -357,9 +384,20 @@ size_t mlkv_cache_bytes(const mlkv_map* map, int batch, int capacity, int head_d
 
 size_t mlkv_workspace_bytes(const mlkv_map* map, int batch, int capacity, int head_dim) {
   if (!map || batch <= 0 || capacity <= 0 || (head_dim != 64 && head_dim != 128)) return 0;
-  // The most splits any plan can produce: minimum tiles per split over the capacity.
-  const int ns_max = (tiles_of(capacity) + kMinTilesPerSplit - 1) / kMinTilesPerSplit;
+  // The most splits any plan can produce.
+  int ns_max = (tiles_of(capacity) + kMinTilesPerSplit - 1) / kMinTilesPerSplit;
+  ns_max = ns_max > kMaxSplits ? kMaxSplits : ns_max;
   return workspace_need(batch, map->h, head_dim, ns_max);
+}
+
+mlkv_status mlkv_workspace_init(void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  if (!workspace && workspace_bytes > 0) return fail(MLKV_ERR_INVALID_ARG, "workspace is NULL");
+  if (workspace_bytes == 0) return ok();
+  if (!aligned16(workspace)) return fail(MLKV_ERR_ALIGNMENT, "workspace not 16-byte aligned");
+  const hipError_t err = mlkv::launch_fill(static_cast<uint32_t*>(workspace), workspace_bytes / 4,
+                                           0u, stream);
+  if (err != hipSuccess) return fail(MLKV_ERR_HIP, "fill launch: %s", hipGetErrorString(err));
+  return ok();
 }
 
 mlkv_status mlkv_plan_splits(const mlkv_map* map, int layer, int batch, int capacity, int head_dim,

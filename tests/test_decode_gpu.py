@@ -133,6 +133,9 @@ def test_split_count_invariance_and_determinism():
             outs[split_tokens] = o.cpu().numpy().astype(np.float64)
         finally:
             os.environ.pop("MLKV_SPLIT_TOKENS", None)
+    # every call hands the split counters (head of the workspace) back at zero
+    counters = dw.ws[: w.B * w.h * 4].view(torch.int32).cpu().numpy()
+    assert np.all(counters == 0)
     ref = oracle.decode_attention(2, dw.host["q"][2], dw.host["k_cache"], dw.host["v_cache"],
                                   dw.kv_of, dw.host["ctx"])
     for k, o in outs.items():
