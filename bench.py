@@ -82,7 +82,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--cold", action="store_true",
-                    help="flush caches (512 MB write) before each timed attention launch")
+                    help="also time attention launches after a 1 GiB read evicts the caches")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     args = ap.parse_args()
 
@@ -143,32 +143,48 @@ def main():
     torch.cuda.synchronize()
     ms_step = e0.elapsed_time(e1) / args.steps
 
-    # Per-launch duration of the dominant kernel (split-K attention; the
-    # combine is launched only when a sequence spans several splits), HIP
-    # events on the launch stream around each call, natural layer order.
-    log("[bench] per-launch attention timing")
-    flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev) if args.cold else None
-    reps = max(3, min(20, args.steps // 5))
-    starts = [torch.cuda.Event(enable_timing=True) for _ in range(reps * w.l)]
-    ends = [torch.cuda.Event(enable_timing=True) for _ in range(reps * w.l)]
-    lens_attn = (ctx + 1).to(torch.int32)
-    out_l = torch.empty((w.B, w.h, w.D), dtype=torch.float32, device=dev)
-    i = 0
-    for _ in range(reps):
-        for n in range(w.l):
-            if flush is not None:
-                flush.fill_(i & 0xFF)
-            starts[i].record(stream)
+    # Per-launch duration of the dominant kernel (split-K attention), from HIP
+    # event pairs the library records on the launch stream around each
+    # attention kernel, over a second timed region of the same steps.
+    log("[bench] timing attention kernels (event pairs)")
+    mlkv.profile_enable(args.steps * w.l)
+    torch.cuda.synchronize()
+    e2, e3 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e2.record(stream)
+    for _ in range(args.steps):
+        one_step()
+    e3.record(stream)
+    torch.cuda.synchronize()
+    n_launch, tot_ms, min_ms, max_ms = mlkv.profile_read()
+    mlkv.profile_disable()
+    ms_step_profiled = e2.elapsed_time(e3) / args.steps
+    avg = tot_ms * 1e-3 / n_launch
+    attn_bytes = float(np.mean([x["kv"] + x["q"] + x["out"] for x in per_layer]))
+    achieved = attn_bytes / avg / 1e9
+    cold = None
+    if args.cold:
+        # Cold-cache attention launches: a 1 GiB read evicts the 256 MB
+        # Infinity Cache (clean lines, no write-back) before each launch.
+        log("[bench] cold attention launches")
+        flush = torch.ones(1 << 28, dtype=torch.float32, device=dev)
+        lens_attn = (ctx + 1).to(torch.int32)
+        out_l = torch.empty((w.B, w.h, w.D), dtype=torch.float32, device=dev)
+        reps = 3 * w.l
+        mlkv.profile_enable(reps)
+        sink = torch.zeros((), device=dev)
+        for i in range(reps):
+            n = i % w.l
+            sink += flush.sum()
             mlkv.decode_attention(n, q[n], cache, mp, lens_attn, out_l, max_len_hint=max_len,
                                   ws=ws)
-            ends[i].record(stream)
-            i += 1
-    torch.cuda.synchronize()
-    durs = np.array([s.elapsed_time(e) for s, e in zip(starts, ends)]) * 1e-3  # seconds
-    attn_bytes = np.mean([x["kv"] + x["q"] + x["out"] for x in per_layer])
-    avg = float(durs.mean())
-    achieved = attn_bytes / avg / 1e9
-    tps, ns = mp.plan_splits(0, w.B, S, w.D, max_len)
+        torch.cuda.synchronize()
+        c_n, c_tot, c_min, c_max = mlkv.profile_read()
+        mlkv.profile_disable()
+        c_avg = c_tot * 1e-3 / c_n
+        cold = {"avg_launch_us": round(c_avg * 1e6, 3),
+                "achieved": round(attn_bytes / c_avg / 1e9, 1),
+                "frac": round(attn_bytes / c_avg / 1e9 / HBM_PEAK_GBS, 4)}
+    workgroups, max_parts = mp.plan(0, w.B, S, w.D, max_len)
 
     result = {
         "metric": "decode-attention HBM GB/s (% of peak) + decode steps/s, MLKV Pythia-160M shape",
@@ -190,14 +206,18 @@ def main():
                    "batch": w.B, "ctx": w.ctx if w.ctx is not None else list(w.ctx_range),
                    "ctx_sum": int(inp["ctx"].sum()), "capacity": S,
                    "bytes_per_step": int(step_total), "kv_bytes_per_step": int(kv_total),
-                   "split_tokens_layer0": tps, "splits_layer0": ns},
+                   "workgroups_layer0": workgroups},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
-                     "kernel": "attn_partial_kernel (+ combine when split)",
+                     "kernel": "attention_kernel",
                      "avg_launch_us": round(avg * 1e6, 3),
+                     "min_launch_us": round(min_ms * 1e3, 3),
+                     "max_launch_us": round(max_ms * 1e3, 3),
+                     "launches": n_launch,
                      "bytes_per_launch": int(attn_bytes),
-                     "cache_state": "cold (512 MB flush before each launch)" if args.cold
-                     else "warm (natural layer order)"},
+                     "cache_state": "natural layer order, back-to-back steps",
+                     "ms_per_step_while_timed": round(ms_step_profiled, 5),
+                     "cold": cold},
     }
     if not args.no_cpu_baseline:
         log("[bench] cpu baseline (oracle)")

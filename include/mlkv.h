@@ -163,14 +163,16 @@ mlkv_status mlkv_cache_append(int layer, const mlkv_map* map, const mlkv_cache* 
  *   q:   device bf16 [batch][h][head_dim], 16-byte aligned.
  *   out: device [batch][h][head_dim], fp32 or bf16 per out_dtype.
  *   max_len_hint: an upper bound of every L_b (<= 0 means capacity); it sizes
- *        the split-K grid.  Lengths above it are truncated to it.
+ *        the work plan.  Lengths above it are truncated to it.
+ *   batch: at most 4096 sequences (else MLKV_ERR_UNSUPPORTED).
  *   workspace: device memory of at least mlkv_workspace_bytes(...) bytes,
  *        16-byte aligned, zeroed once by mlkv_workspace_init (the split
  *        counters must start at zero; each call returns them to zero).
  * Every query head mapped to one KV head is served from a single pass over
- * that head's cache rows; long sequences are split across workgroups and the
- * last workgroup of a sequence to finish merges the splits in a fixed order
- * (results are bitwise reproducible).
+ * that head's cache rows.  The tiles of all sequences are shared equally by
+ * the workgroups (ragged batches stay balanced); a sequence spread over
+ * several workgroups is merged by a second kernel in a fixed order, so
+ * results are bitwise reproducible.
  */
 mlkv_status mlkv_decode_attention(int layer, const void* q, const mlkv_cache* cache,
                                   const mlkv_map* map, const int32_t* seq_lens, void* out,
@@ -198,12 +200,33 @@ mlkv_status mlkv_decode_step(const void* q_all, const void* k_new_all, const voi
 /* Introspection (tests and benchmarks)                                      */
 /* ----------------------------------------------------------------------- */
 
-/* Split-K plan that mlkv_decode_attention uses for `layer` at this max length:
- * tokens per split (a multiple of 32) and number of splits.  Returns
- * MLKV_ERR_* on invalid arguments.  Env MLKV_SPLIT_TOKENS overrides the
- * tokens per split (rounded to a multiple of 128, at least 128). */
-mlkv_status mlkv_plan_splits(const mlkv_map* map, int layer, int batch, int capacity,
-                             int head_dim, int max_len, int* tokens_per_split, int* n_splits);
+/* Work plan mlkv_decode_attention uses for `layer` at this max length: the
+ * 32-token tiles of all (sequence, KV head) pairs form one flat list shared
+ * equally by `workgroups` workgroups (the device's resident capacity, capped
+ * at 32 per (sequence, KV head) and at one per 4 tiles; one workgroup for at
+ * most 16 tiles); `max_parts` bounds the workgroups covering one sequence.
+ * Env MLKV_WORKGROUPS overrides the resident capacity used.  Returns
+ * MLKV_ERR_* on invalid arguments. */
+mlkv_status mlkv_plan(const mlkv_map* map, int layer, int batch, int capacity, int head_dim,
+                      int max_len, int* workgroups, int* max_parts);
+
+/* ----------------------------------------------------------------------- */
+/* Kernel timing (benchmarks)                                                */
+/* ----------------------------------------------------------------------- */
+
+/* While enabled (on the calling thread), every split-K attention kernel that
+ * mlkv_decode_attention / mlkv_decode_step launches is bracketed by a pair of
+ * HIP events recorded on its launch stream (the merge kernel, when one runs,
+ * and the append kernel are outside the pair).  Up to max_launches launches
+ * are recorded; later ones are not timed.  Creates the events (host call, not
+ * for capture).  Errors: MLKV_ERR_INVALID_ARG (max_launches <= 0),
+ * MLKV_ERR_HIP. */
+mlkv_status mlkv_profile_enable(int max_launches);
+/* Synchronizes on the recorded events and reports the number of timed
+ * launches and the sum, minimum and maximum of their durations (ms). */
+mlkv_status mlkv_profile_read(int* launches, double* total_ms, double* min_ms, double* max_ms);
+/* Stops timing and destroys the events. */
+void mlkv_profile_disable(void);
 
 #ifdef __cplusplus
 }

@@ -36,7 +36,8 @@ EXPORTS = [
     "mlkv_map_kv_head", "mlkv_map_owner_layer", "mlkv_map_layer_kv_count",
     "mlkv_map_layer_owned_count", "mlkv_map_layer_owned_begin", "mlkv_cache_bytes",
     "mlkv_workspace_bytes", "mlkv_cache_append", "mlkv_decode_attention", "mlkv_decode_step",
-    "mlkv_plan_splits", "mlkv_workspace_init",
+    "mlkv_plan", "mlkv_workspace_init", "mlkv_profile_enable", "mlkv_profile_read",
+    "mlkv_profile_disable",
 ]
 
 
@@ -84,8 +85,11 @@ def lib():
             "mlkv_cache_append": ([I, P, P, P, P, I, P, P], S),
             "mlkv_decode_attention": ([I, P, P, P, P, P, I, I, P, Z, P], S),
             "mlkv_decode_step": ([P, P, P, P, P, P, P, I, I, P, Z, P], S),
-            "mlkv_plan_splits": ([P, I, I, I, I, I, ctypes.POINTER(I), ctypes.POINTER(I)], S),
+            "mlkv_plan": ([P, I, I, I, I, I, ctypes.POINTER(I), ctypes.POINTER(I)], S),
             "mlkv_workspace_init": ([P, Z, P], S),
+            "mlkv_profile_enable": ([I], S),
+            "mlkv_profile_read": ([ctypes.POINTER(I)] + [ctypes.POINTER(ctypes.c_double)] * 3, S),
+            "mlkv_profile_disable": ([], None),
         }
         for name, (args, res) in sig.items():
             f = getattr(L, name)
@@ -190,11 +194,12 @@ class Map:
     def workspace_bytes(self, batch: int, capacity: int, head_dim: int) -> int:
         return lib().mlkv_workspace_bytes(self._h, batch, capacity, head_dim)
 
-    def plan_splits(self, layer: int, batch: int, capacity: int, head_dim: int, max_len: int = 0):
-        tps, ns = ctypes.c_int(), ctypes.c_int()
-        _check(lib().mlkv_plan_splits(self._h, layer, batch, capacity, head_dim, max_len,
-                                      ctypes.byref(tps), ctypes.byref(ns)))
-        return tps.value, ns.value
+    def plan(self, layer: int, batch: int, capacity: int, head_dim: int, max_len: int = 0):
+        """(workgroups, max_parts) of mlkv_plan."""
+        wg, mp = ctypes.c_int(), ctypes.c_int()
+        _check(lib().mlkv_plan(self._h, layer, batch, capacity, head_dim, max_len,
+                               ctypes.byref(wg), ctypes.byref(mp)))
+        return wg.value, mp.value
 
 
 # ------------------------------------------------------------------- cache ---
@@ -304,3 +309,23 @@ def decode_step(q_all: torch.Tensor, k_new_all: torch.Tensor, v_new_all: torch.T
                                   map_.handle, _dev_ptr(ctx_lens, torch.int32, "ctx_lens"),
                                   _dev_ptr(out_all, out_all.dtype, "out_all"), out_dt,
                                   max_len_hint, ws_ptr, ws_n, _stream(stream)))
+
+
+# ------------------------------------------------------------------ timing ---
+
+def profile_enable(max_launches: int):
+    """Bracket the next attention kernels with HIP events (mlkv_profile_enable)."""
+    _check(lib().mlkv_profile_enable(max_launches))
+
+
+def profile_read():
+    """(launches, total_ms, min_ms, max_ms) of the timed attention kernels."""
+    n = ctypes.c_int()
+    tot, lo, hi = ctypes.c_double(), ctypes.c_double(), ctypes.c_double()
+    _check(lib().mlkv_profile_read(ctypes.byref(n), ctypes.byref(tot), ctypes.byref(lo),
+                                   ctypes.byref(hi)))
+    return n.value, tot.value, lo.value, hi.value
+
+
+def profile_disable():
+    lib().mlkv_profile_disable()

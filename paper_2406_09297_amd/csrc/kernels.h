@@ -21,21 +21,35 @@ struct AttnParams {
   const uint16_t* v;         // value plane [n_kv][B][S/32][D][32]
   const int32_t* lens;       // [B]; attended length = lens[b] + len_offset
   void* out;                 // [B][h][D] fp32 or bf16
-  float* part_acc;           // [B*n_groups][n_split][G][D]  unnormalised partial outputs
-  float* part_ml;            // [B*n_groups][n_split][G][2]  (max in log2 units, denominator)
-  int* counters;             // [B * n_groups] finished splits per sequence (zero between calls)
-  int B, h, S;
+  int* runs;                 // [B] runs per unit of sequence b (written by workgroup 0)
+  void* plan;                // [n_blocks] run items from plan_kernel, or null: schedule in-kernel
+  int* counters;             // [B*n_groups] finished runs per unit (zero between calls)
+  float* part_acc;           // [B*n_groups][max_parts][G][D]  unnormalised partial outputs
+  float* part_ml;            // [B*n_groups][max_parts][G][2]  (max in log2 units, denominator)
+  int B, h, S, D;
   int kv_begin, G, n_groups; // KV heads [kv_begin, kv_begin+n_groups), G query heads each
-  int n_split, tiles_per_split;
+  int max_len;               // attended lengths are clamped to this (<= S)
+  int n_blocks;              // workgroups launched (runs beyond the schedule's count exit)
+  int min_tiles;             // least tiles per run
+  int max_parts;             // partial slots per unit (bound on its runs)
   int len_offset, out_bf16;
-  int fused_combine;         // 1: last workgroup of a sequence merges; 0: combine kernel
+  int fused;                 // 1: the last run of a unit merges its partials when they fit LDS
   float scale_log2;          // log2(e) / sqrt(D)
 };
 
 hipError_t launch_append(const AppendParams& p, int head_dim, int owned_count,
                          hipStream_t stream);
-hipError_t launch_attention(const AttnParams& p, int head_dim, hipStream_t stream);
-int fused_partial_capacity();  // floats of partial output the fused combine can stage
+// The split-K attention kernel, then (when splits are merged by a separate
+// kernel) the merge.
+// start/stop: optional events recorded around the attention dispatch.
+hipError_t launch_attention_main(const AttnParams& p, int head_dim, hipStream_t stream,
+                                 hipEvent_t start, hipEvent_t stop);
+hipError_t launch_attention_merge(const AttnParams& p, int head_dim, hipStream_t stream);
+// One workgroup computing the run schedule into p.plan (and p.runs).
+hipError_t launch_plan(const AttnParams& p, hipStream_t stream);
+int max_batch();
+int stage_floats();  // partial-output floats one workgroup can merge in place                     // sequences one call may hold
+int resident_workgroups(int head_dim); // attention workgroups the device holds at once (0: none)
 hipError_t launch_fill(uint32_t* dst, size_t n_words, uint32_t value, hipStream_t stream);
 
 }  // namespace mlkv

@@ -1,12 +1,17 @@
 // HIP kernels of MLKV decode attention for CDNA4 (gfx950, wave64, MFMA).
 //
 //   append_kernel     newest token's K/V rows -> cache slot (bit copy)
-//   attention_kernel  split-K attention of one layer: each workgroup owns one
-//                     (sequence, KV head, token range) and serves every query
-//                     head mapped to that KV head from one pass over the range;
-//                     the last workgroup of a sequence to finish merges the
-//                     split partials (log-sum-exp) and writes the output
-//   fill_kernel       zeroes the workspace's split counters
+//   attention_kernel  split-K attention of one layer.  Each (sequence, KV
+//                     head) unit is cut into runs of the same number of
+//                     32-token tiles, the run length chosen on the device from
+//                     the actual lengths so that the runs of all units fill
+//                     the launched workgroups (ragged batches stay balanced);
+//                     a workgroup takes one run and serves every query head
+//                     mapped to the KV head from one pass over it.  A unit of
+//                     one run is finished in place; otherwise each run leaves
+//                     a partial (max, denominator, output)
+//   combine_kernel    log-sum-exp merge of a unit's partials, fixed order
+//   fill_kernel       zero fill of a workspace
 //
 // Math (paper Section 2.1 Eqs. 1-3; MLKV head map Section 3 Eqs. 13-17):
 //   o = sum_t softmax_t(q.k_t / sqrt(D)) v_t.  Scores are kept in the log2
@@ -28,8 +33,11 @@
 // is exactly the lane that must supply them as P^T k-slots: no shuffles
 // between the two products.  Each wave keeps the next tile's loads in flight
 // while it computes the current one.
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+
+#include <atomic>
 
 #include "kernels.h"
 
@@ -42,14 +50,8 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 constexpr int kTile = 32;     // tokens per wave iteration
 constexpr int kWaves = 4;     // waves per workgroup
 constexpr int kThreads = kWaves * 64;
-constexpr int kMaxSplits = 256;  // most splits one sequence may have (host plans within it)
-// The last workgroup of a sequence merges the splits itself when their partial
-// outputs fit in LDS (kFusedPartialFloats floats); otherwise combine_kernel runs.
-constexpr int kFusedPartialFloats = 8192;
-constexpr int kStageBatch = 32;  // partial loads in flight per thread while staging
-template <int D>
-constexpr int kLdsFloats = (kWaves * 16 * (D + 4)) > kFusedPartialFloats ? (kWaves * 16 * (D + 4))
-                                                                         : kFusedPartialFloats;
+constexpr int kMaxBatch = 2048;  // sequences one call may hold (schedule tables in LDS)
+// A sequence has at most 256 splits (the host planner keeps within that).
 
 __device__ __forceinline__ u16x8 load16(const uint16_t* p) {
   return *reinterpret_cast<const u16x8*>(p);
@@ -63,10 +65,10 @@ __device__ __forceinline__ f32x4 mfma_bf16(bf16x8 a, bf16x8 b, f32x4 c) {
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
-// Device-scope (all XCDs) stores and loads of the split partials.  On CDNA3/4
-// the scope travels with each access (SC bits), so partials written and read
-// this way need no L2 writeback or invalidate, only completion of the stores
-// before the split counter is bumped.
+// Device-scope (all XCDs) stores and loads for partials merged inside the
+// attention kernel: on CDNA3/4 the scope travels with each access (SC bits),
+// so no L2 writeback or invalidate is needed, only completion of the stores
+// before the unit's counter is bumped.
 __device__ __forceinline__ void store_device(float* p, float v) {
   __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
@@ -83,14 +85,15 @@ __device__ __forceinline__ float bf16_bits_to_f32(uint16_t u) {
   return __builtin_bit_cast(float, static_cast<uint32_t>(u) << 16);
 }
 
-// Attended length of sequence b (clamped to the cache and to the split grid).
+// Attended length of sequence b: lens[b] + len_offset, clamped to [0, max_len]
+// (max_len <= capacity bounds the work list and the workspace).
 __device__ __forceinline__ int attended_len(const AttnParams& p, int b) {
   int L = p.lens[b] + p.len_offset;
   L = L < 0 ? 0 : L;
-  L = L > p.S ? p.S : L;
-  const int cap = p.n_split * p.tiles_per_split * kTile;
-  return L > cap ? cap : L;
+  return L > p.max_len ? p.max_len : L;
 }
+
+__device__ __forceinline__ int tiles_of(int L) { return (L + kTile - 1) / kTile; }
 
 // ---------------------------------------------------------------------------
 // Cache append (Section 2.4): one workgroup per (sequence b, owned head c),
@@ -114,8 +117,7 @@ __global__ __launch_bounds__(D / 8) void append_kernel(AppendParams p) {
 }
 
 // ---------------------------------------------------------------------------
-// Split-K attention with in-kernel combine.
-// Grid: x = split, y = sequence * n_groups + group.
+// Split-K attention over a balanced flat tile list.
 // ---------------------------------------------------------------------------
 template <int D>
 struct Tile {
@@ -144,10 +146,15 @@ __device__ __forceinline__ void load_tile(Tile<D>& t, const uint16_t* kbase,
 
 template <int D>
 struct WaveState {
-  float m = -INFINITY;  // running max of this lane's head (log2 domain)
-  float l = 0.f;        // this lane's share of the running denominator
+  float m = -INFINITY;  // reference max of this lane's head (log2 domain)
+  f32x4 den;            // softmax denominator of this lane's head (all four equal)
   f32x4 acc[Tile<D>::DB];
 };
+
+// The reference max is only moved when a tile's max exceeds it by more than
+// kLazyRescale (log2 units): weights stay <= 2^kLazyRescale, and most tiles
+// skip rescaling the accumulators.  Any reference gives the same softmax.
+constexpr float kLazyRescale = 8.f;
 
 template <int D>
 __device__ __forceinline__ void process_tile(WaveState<D>& st, Tile<D>& t, const bf16x8* qf,
@@ -160,11 +167,11 @@ __device__ __forceinline__ void process_tile(WaveState<D>& st, Tile<D>& t, const
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) s[sb] = mfma_bf16(as_bf16(t.k[sb][kk]), qf[kk], s[sb]);
   }
-  float x[8];
+  float x[8];  // raw scores q.k of tokens 8*grp + e
 #pragma unroll
   for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
-    for (int i = 0; i < 4; ++i) x[sb * 4 + i] = s[sb][i] * scale_log2;
+    for (int i = 0; i < 4; ++i) x[sb * 4 + i] = s[sb][i];
 
   if (t0 + kTile > L) {  // ragged tail: positions >= L take no weight and no value
     const int first = t0 + grp * 8;
@@ -178,30 +185,32 @@ __device__ __forceinline__ void process_tile(WaveState<D>& st, Tile<D>& t, const
     }
   }
 
-  float tmax = x[0];
-#pragma unroll
-  for (int e = 1; e < 8; ++e) tmax = fmaxf(tmax, x[e]);
+  float tmax = fmaxf(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])),
+                     fmaxf(fmaxf(x[4], x[5]), fmaxf(x[6], x[7])));
   tmax = fmaxf(tmax, __shfl_xor(tmax, 16));
   tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
-  const float m_new = fmaxf(st.m, tmax);
-  const float alpha = fast_exp2(st.m - m_new);
+  tmax *= scale_log2;
+  const bool raise = tmax > st.m + kLazyRescale;
+  if (__ballot(raise)) {  // some head of this wave needs a new reference max
+    const float m_new = raise ? tmax : st.m;
+    const float alpha = fast_exp2(st.m - m_new);  // 0 on the first tile, 1 if unchanged
+    st.m = m_new;
+    st.den *= alpha;
+#pragma unroll
+    for (int db = 0; db < DB; ++db) st.acc[db] *= alpha;
+  }
 
   u16x8 pbits;
-  float psum = 0.f;
+  const float neg_m = -st.m;
 #pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    const uint16_t pb = f32_to_bf16_bits(fast_exp2(x[e] - m_new));
-    pbits[e] = pb;
-    psum += bf16_bits_to_f32(pb);  // denominator from the rounded weights
-  }
-  st.l = st.l * alpha + psum;
-  st.m = m_new;
+  for (int e = 0; e < 8; ++e) pbits[e] = f32_to_bf16_bits(fast_exp2(fmaf(x[e], scale_log2, neg_m)));
   const bf16x8 pf = as_bf16(pbits);
+  // Denominator from the same rounded weights, on the matrix core: a row of
+  // ones times P^T sums the 32 weights of each head.
+  const u16x8 ones = {0x3F80, 0x3F80, 0x3F80, 0x3F80, 0x3F80, 0x3F80, 0x3F80, 0x3F80};
+  st.den = mfma_bf16(as_bf16(ones), pf, st.den);
 #pragma unroll
-  for (int db = 0; db < DB; ++db) {
-    st.acc[db] *= alpha;
-    st.acc[db] = mfma_bf16(as_bf16(t.v[db]), pf, st.acc[db]);
-  }
+  for (int db = 0; db < DB; ++db) st.acc[db] = mfma_bf16(as_bf16(t.v[db]), pf, st.acc[db]);
 }
 
 template <int D>
@@ -224,36 +233,185 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
+__device__ __forceinline__ int wave_sum_int(int v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
+  return v;
+}
+
+struct SchedShared {
+  int q[kMaxBatch + 1];  // first run (workgroup) of each sequence, in runs of all its units
+  int len[kMaxBatch];    // attended lengths
+  int sched[3];          // run length R, run count N, sequence of this workgroup's run
+};
+
+// Partial outputs the last run of a unit can stage in LDS to merge in place.
+constexpr int kStageFloats = 8192;
+constexpr int kStageMl = 512;
+
+template <int D>
+struct AttnShared {
+  union {  // phases: schedule, then the waves' merge, then (last run only) staging
+    SchedShared sc;
+    struct {
+      float acc[kWaves][16][D + 4];
+      float m[kWaves][16];
+      float l[kWaves][16];
+    };
+    float stage[kStageFloats];
+  };
+  float stage_ml[kStageMl];
+  int last;
+};
+
+// A run of the plan: sequence b, KV group r, run j of nb of that unit,
+// attended length L, tiles [k0, k1).  b < 0 marks a workgroup with no run.
+struct RunItem {
+  int b, r, j, nb;
+  int L, k0, k1, pad;
+};
+
+// ceil(x / y) for 0 <= x < 2^21, 1 <= y < 2^21 without the integer-division
+// routine: a float estimate (off by at most one) and one correction each way.
+__device__ __forceinline__ int div_up(int x, int y) {
+  int q = static_cast<int>(static_cast<float>(x) * __builtin_amdgcn_rcpf(static_cast<float>(y)));
+  q -= q * y > x ? 1 : 0;
+  q += (q + 1) * y <= x ? 1 : 0;  // now q = floor(x / y)
+  return q + (q * y < x ? 1 : 0);
+}
+
+// ceil(x / y) for 0 <= x < 2^50, 1 <= y: a double estimate and corrections.
+__device__ __forceinline__ long div_up64(long x, long y) {
+  long q = static_cast<long>(static_cast<double>(x) * __builtin_amdgcn_rcp(static_cast<double>(y)));
+  q -= q * y > x ? 1 : 0;
+  q += (q + 1) * y <= x ? 1 : 0;  // now q = floor(x / y)
+  return q + (q * y < x ? 1 : 0);
+}
+
+// The run schedule every workgroup derives identically from the lengths
+// (computed by wave 0; the other waves wait at the barrier that follows):
+// tiles t_b = ceil(L_b / 32); run length R is the least of ceil(T / W), +1,
+// +2 (T = all tiles, W = workgroups) whose run count N(R) = n_groups *
+// sum_b ceil(t_b / R) fits W, else ceil(T / (W - U)) (U = non-empty units),
+// which always fits; never below min_tiles.  Leaves sm.q[b] = runs before
+// sequence b, sm.len, and sm.sched = {R, N, sequence of run g}.
+__device__ void schedule_wave0(const AttnParams& p, SchedShared& sm, int g) {
+  const int lane = threadIdx.x;
+  const int per = (p.B + 63) / 64;  // sequences per lane
+  const int b0 = lane * per;
+  const int b1 = b0 + per < p.B ? b0 + per : p.B;
+  int tot = 0, nonempty = 0;
+  for (int b = b0; b < b1; ++b) {
+    const int L = attended_len(p, b);
+    sm.len[b] = L;
+    const int t = tiles_of(L);
+    tot += t;
+    nonempty += t > 0 ? 1 : 0;
+  }
+  tot = wave_sum_int(tot);
+  nonempty = wave_sum_int(nonempty);
+  const long T = static_cast<long>(tot) * p.n_groups;
+  const long U = static_cast<long>(nonempty) * p.n_groups;
+  const long W = p.n_blocks;
+  int R = static_cast<int>(div_up64(T, W));
+  R = R < p.min_tiles ? p.min_tiles : R;
+  int n0 = 0, n1 = 0, n2 = 0;
+  for (int b = b0; b < b1; ++b) {
+    const int t = tiles_of(sm.len[b]);
+    n0 += div_up(t, R);
+    n1 += div_up(t, R + 1);
+    n2 += div_up(t, R + 2);
+  }
+  n0 = wave_sum_int(n0);
+  n1 = wave_sum_int(n1);
+  n2 = wave_sum_int(n2);
+  if (static_cast<long>(n0) * p.n_groups <= W) {
+  } else if (static_cast<long>(n1) * p.n_groups <= W) {
+    R += 1;
+  } else if (static_cast<long>(n2) * p.n_groups <= W) {
+    R += 2;
+  } else {
+    const long spare = W - U;  // > 0 whenever the host launches W > units
+    R = spare > 0 ? static_cast<int>(div_up64(T, spare)) : p.max_len;
+    R = R < p.min_tiles ? p.min_tiles : R;
+  }
+  // Exclusive scan of runs per sequence (times n_groups) across the wave.
+  int local = 0;
+  for (int b = b0; b < b1; ++b) local += div_up(tiles_of(sm.len[b]), R);
+  local *= p.n_groups;
+  int x = local;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int y = __shfl_up(x, off);
+    if (lane >= off) x += y;
+  }
+  int excl = x - local;
+  for (int b = b0; b < b1; ++b) {
+    const int runs = p.n_groups * div_up(tiles_of(sm.len[b]), R);
+    sm.q[b] = excl;
+    if (excl <= g && g < excl + runs) sm.sched[2] = b;  // exactly one sequence holds run g
+    excl += runs;
+  }
+  if (lane == 63) {
+    sm.q[p.B] = excl;
+    sm.sched[0] = R;
+    sm.sched[1] = excl;
+  }
+}
+
 template <int D>
 __global__ __launch_bounds__(kThreads) void attention_kernel(AttnParams p) {
   constexpr int KK = Tile<D>::KK, DB = Tile<D>::DB;
-  constexpr int LDS_STRIDE = D + 4;
-
+  __shared__ AttnShared<D> sm;
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int col = lane & 15;  // query head inside the group / MFMA row
   const int grp = lane >> 4;  // k-slot group: tokens 8*grp .. 8*grp+7 of a tile
+  const int g = blockIdx.x;
 
-  // Grid x runs over (sequence, KV head) units and y over splits, so the
-  // dispatcher hands out every sequence's first splits before any later
-  // split: workgroups of splits past a sequence's end come last and leave at
-  // once.  Consecutive units land on different XCDs, and all splits of one
-  // unit share an XCD (workgroup id modulo 8), keeping its partials in one L2.
-  const int unit = blockIdx.x;
-  const int split = blockIdx.y;
-  const int b = unit / p.n_groups;
-  const int r = unit - b * p.n_groups;
+  int b, r, j, nb, L, k0, k1;
+  if (p.plan) {  // the step's plan was computed once by plan_kernel
+    const RunItem item = reinterpret_cast<const RunItem*>(p.plan)[g];
+    if (item.b < 0) return;
+    b = item.b;
+    r = item.r;
+    j = item.j;
+    nb = item.nb;
+    L = item.L;
+    k0 = item.k0;
+    k1 = item.k1;
+  } else {
+    if (wave == 0) schedule_wave0(p, sm.sc, g);
+    __syncthreads();
+    const int R = sm.sc.sched[0];
+    const int n_runs = sm.sc.sched[1];
+    if (g == 0 && p.runs)  // runs per sequence, for the merge kernel
+      for (int bb = threadIdx.x; bb < p.B; bb += kThreads)
+        p.runs[bb] = div_up(tiles_of(sm.sc.len[bb]), R);
+    for (int bb = g; bb < p.B; bb += p.n_blocks) {  // sequences with nothing to attend
+      if (sm.sc.len[bb] > 0) continue;
+      for (int i = threadIdx.x; i < p.h * D; i += kThreads)
+        store_out<D>(p, static_cast<size_t>(bb) * p.h, i, 0.f);
+    }
+    if (g >= n_runs) return;
+    // Run g: sequence b, KV group r, run j of that unit.
+    b = sm.sc.sched[2];
+    L = sm.sc.len[b];
+    const int tiles_b = tiles_of(L);
+    nb = div_up(tiles_b, R);  // runs of each unit of sequence b
+    const int rem = g - sm.sc.q[b];
+    r = div_up(rem + 1, nb) - 1;  // floor(rem / nb)
+    j = rem - r * nb;
+    k0 = j * R;
+    k1 = k0 + R < tiles_b ? k0 + R : tiles_b;
+  }
+
   const int kv = p.kv_begin + r;
   const int head0 = r * p.G;
-  const int chunk = p.tiles_per_split * kTile;
-  const int t_begin = split * chunk;
-
   const size_t seq = static_cast<size_t>(kv) * p.B + b;
   const uint16_t* kbase = p.k + seq * p.S * D;
   const uint16_t* vbase = p.v + seq * p.S * D;
 
-  // The query loads go out before the sequence length is known.
-  Tile<D> ta, tb;
   bf16x8 qf[KK];
   {
     const bool valid = col < p.G;
@@ -261,138 +419,128 @@ __global__ __launch_bounds__(kThreads) void attention_kernel(AttnParams p) {
         p.q + (static_cast<size_t>(b) * p.h + head0 + (valid ? col : p.G - 1)) * D + grp * 8;
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
-      u16x8 v = load16(qrow + kk * 32);
+      const u16x8 v = load16(qrow + kk * 32);
       const u16x8 zero = {0, 0, 0, 0, 0, 0, 0, 0};
       qf[kk] = as_bf16(valid ? v : zero);  // padded heads score zero
     }
   }
-
-  const int L = attended_len(p, b);
-  int ns = (L + chunk - 1) / chunk;  // active splits of this sequence
-  ns = ns < 1 ? 1 : ns;
-  if (split >= ns) return;  // empty split: nothing to contribute
-  int n_tiles = (L - t_begin + kTile - 1) / kTile;
-  n_tiles = n_tiles < 0 ? 0 : (n_tiles > p.tiles_per_split ? p.tiles_per_split : n_tiles);
-
+  Tile<D> ta, tb;
+  int it = k0 + wave;
   WaveState<D> st;
+  st.den = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int db = 0; db < DB; ++db) st.acc[db] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // Two tile buffers: the loads of tile it+kWaves are issued before tile it
-  // is consumed.  The prefetch is never skipped (past the last tile it re-reads
-  // the current, cache-resident tile) so that the wait before each tile only
-  // covers that tile's own loads.
-  int it = wave;
-  if (it < n_tiles) {
-    load_tile(ta, kbase, vbase, t_begin + it * kTile, col, grp);
+  // The loads of tile it+kWaves are issued before tile it is consumed; the
+  // prefetch is never skipped (past the last tile it re-reads the current,
+  // cache-resident tile) so that the wait before each tile covers only that
+  // tile's own loads.
+  if (it < k1) {
+    load_tile(ta, kbase, vbase, it * kTile, col, grp);
     for (;;) {
       int nxt = it + kWaves;
-      load_tile(tb, kbase, vbase, t_begin + (nxt < n_tiles ? nxt : it) * kTile, col, grp);
-      process_tile(st, ta, qf, t_begin + it * kTile, L, grp, p.scale_log2);
+      load_tile(tb, kbase, vbase, (nxt < k1 ? nxt : it) * kTile, col, grp);
+      process_tile(st, ta, qf, it * kTile, L, grp, p.scale_log2);
       it = nxt;
-      if (it >= n_tiles) break;
+      if (it >= k1) break;
       nxt = it + kWaves;
-      load_tile(ta, kbase, vbase, t_begin + (nxt < n_tiles ? nxt : it) * kTile, col, grp);
-      process_tile(st, tb, qf, t_begin + it * kTile, L, grp, p.scale_log2);
+      load_tile(ta, kbase, vbase, (nxt < k1 ? nxt : it) * kTile, col, grp);
+      process_tile(st, tb, qf, it * kTile, L, grp, p.scale_log2);
       it = nxt;
-      if (it >= n_tiles) break;
+      if (it >= k1) break;
     }
   }
 
-  // ---- merge the four waves of the workgroup through LDS ----
-  // sm_buf first holds the four waves' accumulators, later (last workgroup of
-  // a sequence only) the staged partials of every split.
-  __shared__ float sm_buf[kLdsFloats<D>];
-  __shared__ float sm_m[kWaves][16];
-  __shared__ float sm_l[kWaves][16];
-  __shared__ float sm_ml[kFusedPartialFloats / 8];
-  __shared__ int sm_last;
-  float(*sm_acc)[16][LDS_STRIDE] = reinterpret_cast<float(*)[16][LDS_STRIDE]>(sm_buf);
-  float l_tot = st.l + __shfl_xor(st.l, 16);
-  l_tot += __shfl_xor(l_tot, 32);
+  // Merge the four waves through LDS.
   if (grp == 0) {
-    sm_m[wave][col] = st.m;
-    sm_l[wave][col] = l_tot;
+    sm.m[wave][col] = st.m;
+    sm.l[wave][col] = st.den[0];
   }
 #pragma unroll
   for (int db = 0; db < DB; ++db)
-    *reinterpret_cast<f32x4*>(&sm_acc[wave][col][db * 16 + grp * 4]) = st.acc[db];
+    *reinterpret_cast<f32x4*>(&sm.acc[wave][col][db * 16 + grp * 4]) = st.acc[db];
   __syncthreads();
 
   const int GD = p.G * D;
   const size_t out_row0 = static_cast<size_t>(b) * p.h + head0;
-  const size_t slot = static_cast<size_t>(unit) * p.n_split + split;
+  const size_t unit = static_cast<size_t>(b) * p.n_groups + r;
+  const size_t slot = unit * p.max_parts + j;
+  const bool fuse = nb > 1 && p.fused && nb * GD <= kStageFloats && nb * p.G * 2 <= kStageMl;
   for (int idx = threadIdx.x; idx < GD; idx += kThreads) {
     const int hh = idx / D;
     const int d = idx - hh * D;
     float M = -INFINITY;
 #pragma unroll
-    for (int w = 0; w < kWaves; ++w) M = fmaxf(M, sm_m[w][hh]);
+    for (int w = 0; w < kWaves; ++w) M = fmaxf(M, sm.m[w][hh]);
     float wsum = 0.f, o = 0.f;
     if (M != -INFINITY) {
 #pragma unroll
       for (int w = 0; w < kWaves; ++w) {
-        const float f = fast_exp2(sm_m[w][hh] - M);
-        wsum += f * sm_l[w][hh];
-        o += f * sm_acc[w][hh][d];
+        const float f = fast_exp2(sm.m[w][hh] - M);
+        wsum += f * sm.l[w][hh];
+        o += f * sm.acc[w][hh][d];
       }
     }
-    if (ns == 1) {
+    if (nb == 1) {
       store_out<D>(p, out_row0 + hh, d, wsum > 0.f ? o / wsum : 0.f);
-    } else {
+    } else if (fuse) {
       store_device(&p.part_acc[slot * GD + idx], o);
       if (d == 0) {
         store_device(&p.part_ml[(slot * p.G + hh) * 2 + 0], M);
         store_device(&p.part_ml[(slot * p.G + hh) * 2 + 1], wsum);
       }
+    } else {
+      p.part_acc[slot * GD + idx] = o;
+      if (d == 0) {
+        p.part_ml[(slot * p.G + hh) * 2 + 0] = M;
+        p.part_ml[(slot * p.G + hh) * 2 + 1] = wsum;
+      }
     }
   }
-  if (ns == 1 || !p.fused_combine) return;
+  if (!fuse) return;
 
-  // ---- split-K combine by the last workgroup of this sequence to finish ----
+  // ---- the last run of the unit to finish merges its runs in place ----
   wait_stores_complete();  // this thread's partials are visible device-wide
-  __syncthreads();         // ... and so are those of every thread of the workgroup
+  __syncthreads();         // ... and those of every thread; LDS merge data is dead
   if (threadIdx.x == 0)
-    sm_last = __hip_atomic_fetch_add(&p.counters[unit], 1, __ATOMIC_RELAXED,
-                                     __HIP_MEMORY_SCOPE_AGENT) == ns - 1;
+    sm.last = __hip_atomic_fetch_add(&p.counters[unit], 1, __ATOMIC_RELAXED,
+                                     __HIP_MEMORY_SCOPE_AGENT) == nb - 1;
   __syncthreads();
-  if (!sm_last) return;
-  // Every other split bumped the counter after its partials completed, so the
-  // device-scope loads below see them.  The sequence's partials are one
-  // contiguous range [split][head][channel]: stage them in LDS with all loads
-  // in flight at once, then merge in ascending split order (deterministic).
-  const size_t base = static_cast<size_t>(unit) * p.n_split;
+  if (!sm.last) return;
+  // Every other run bumped the counter after its partials completed, so the
+  // device-scope loads below see them.  The unit's partials are contiguous
+  // ([run][head][channel]); stage them with all loads in flight, then merge
+  // in ascending run order (deterministic).
   {
-    const int n_acc = ns * GD;
-    const int n_ml = ns * p.G * 2;
-    float* src_acc = p.part_acc + base * GD;
-    float* src_ml = p.part_ml + base * p.G * 2;
-    for (int j0 = threadIdx.x; j0 < n_acc; j0 += kThreads * kStageBatch) {
-      float v[kStageBatch];
+    const int n_acc = nb * GD;
+    float* src = p.part_acc + unit * p.max_parts * GD;
+    for (int j0 = threadIdx.x; j0 < n_acc; j0 += kThreads * 8) {
+      float v[8];
 #pragma unroll
-      for (int u = 0; u < kStageBatch; ++u) {
-        const int j = j0 + u * kThreads;
-        v[u] = j < n_acc ? load_device(src_acc + j) : 0.f;
+      for (int u = 0; u < 8; ++u) {
+        const int jj = j0 + u * kThreads;
+        v[u] = jj < n_acc ? load_device(src + jj) : 0.f;
       }
 #pragma unroll
-      for (int u = 0; u < kStageBatch; ++u) {
-        const int j = j0 + u * kThreads;
-        if (j < n_acc) sm_buf[j] = v[u];
+      for (int u = 0; u < 8; ++u) {
+        const int jj = j0 + u * kThreads;
+        if (jj < n_acc) sm.stage[jj] = v[u];
       }
     }
-    for (int j = threadIdx.x; j < n_ml; j += kThreads) sm_ml[j] = load_device(src_ml + j);
+    float* src_ml = p.part_ml + unit * p.max_parts * p.G * 2;
+    for (int jj = threadIdx.x; jj < nb * p.G * 2; jj += kThreads) sm.stage_ml[jj] = load_device(src_ml + jj);
   }
   __syncthreads();
   for (int idx = threadIdx.x; idx < GD; idx += kThreads) {
     const int hh = idx / D;
     float M = -INFINITY;
-    for (int s = 0; s < ns; ++s) M = fmaxf(M, sm_ml[(s * p.G + hh) * 2]);
+    for (int s2 = 0; s2 < nb; ++s2) M = fmaxf(M, sm.stage_ml[(s2 * p.G + hh) * 2]);
     float den = 0.f, o = 0.f;
     if (M != -INFINITY) {
-      for (int s = 0; s < ns; ++s) {
-        const float f = fast_exp2(sm_ml[(s * p.G + hh) * 2] - M);
-        den += f * sm_ml[(s * p.G + hh) * 2 + 1];
-        o += f * sm_buf[s * GD + idx];
+      for (int s2 = 0; s2 < nb; ++s2) {
+        const float f = fast_exp2(sm.stage_ml[(s2 * p.G + hh) * 2] - M);
+        den += f * sm.stage_ml[(s2 * p.G + hh) * 2 + 1];
+        o += f * sm.stage[s2 * GD + idx];
       }
     }
     store_out<D>(p, out_row0 + hh, idx - hh * D, den > 0.f ? o / den : 0.f);
@@ -402,10 +550,61 @@ __global__ __launch_bounds__(kThreads) void attention_kernel(AttnParams p) {
 }
 
 // ---------------------------------------------------------------------------
-// Separate log-sum-exp combine for sequences with many splits: one workgroup
-// of four waves per (sequence, query head).  Wave w reads splits w, w+4, ...
-// eight at a time (max, denominator and channels in one round trip) and keeps
-// a running merge; the four waves then merge through LDS.  Fixed order.
+// The run schedule of a decode step, computed once for all its layers (they
+// share the lengths): one workgroup writes every workgroup's RunItem and the
+// runs per sequence.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kThreads) void plan_kernel(AttnParams p, RunItem* items) {
+  __shared__ SchedShared sm;
+  if (threadIdx.x < 64) schedule_wave0(p, sm, -1);
+  __syncthreads();
+  const int R = sm.sched[0];
+  const int n_runs = sm.sched[1];
+  for (int b = threadIdx.x; b < p.B; b += kThreads) p.runs[b] = div_up(tiles_of(sm.len[b]), R);
+  // Sequences with nothing to attend get zero outputs (one thread per sequence
+  // checks; only empty ones write).
+  for (int b = threadIdx.x; b < p.B; b += kThreads) {
+    if (sm.len[b] > 0) continue;
+    const size_t e0 = static_cast<size_t>(b) * p.h * p.D;
+    for (int i = 0; i < p.h * p.D; ++i) {
+      if (p.out_bf16)
+        static_cast<uint16_t*>(p.out)[e0 + i] = 0;
+      else
+        static_cast<float*>(p.out)[e0 + i] = 0.f;
+    }
+  }
+  for (int g = threadIdx.x; g < p.n_blocks; g += kThreads) {
+    RunItem it{-1, 0, 0, 0, 0, 0, 0, 0};
+    if (g < n_runs) {
+      int lo = 0, hi = p.B - 1;  // the last sequence whose first run is <= g
+      while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (sm.q[mid] <= g) lo = mid; else hi = mid - 1;
+      }
+      const int L = sm.len[lo];
+      const int tiles_b = tiles_of(L);
+      const int nb = div_up(tiles_b, R);
+      const int rem = g - sm.q[lo];
+      const int r = div_up(rem + 1, nb) - 1;
+      const int j = rem - r * nb;
+      it.b = lo;
+      it.r = r;
+      it.j = j;
+      it.nb = nb;
+      it.L = L;
+      it.k0 = j * R;
+      it.k1 = it.k0 + R < tiles_b ? it.k0 + R : tiles_b;
+    }
+    items[g] = it;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Log-sum-exp merge of the partials of units cut into several runs (and zero
+// output for empty sequences): one workgroup of four waves per (sequence,
+// query head).  Wave w reads
+// partials w, w+4, ... eight at a time (max, denominator and channels in one
+// round trip) with a running merge, then the waves merge through LDS.
 // ---------------------------------------------------------------------------
 template <int D>
 __global__ __launch_bounds__(kThreads) void combine_kernel(AttnParams p) {
@@ -417,12 +616,15 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(AttnParams p) {
   const int i = static_cast<int>(row - static_cast<size_t>(b) * p.h);
   const int r = i / p.G;
   const int hh = i - r * p.G;
-  const int unit = b * p.n_groups + r;
-  const int L = attended_len(p, b);
-  const int chunk = p.tiles_per_split * kTile;
-  const int ns = (L + chunk - 1) / chunk;
-  if (ns <= 1) return;  // one split: the attention kernel wrote the output itself
-  const size_t base = static_cast<size_t>(unit) * p.n_split;
+  const int ng = p.n_groups;
+  const int ns = p.runs[b];  // runs of each unit of sequence b
+  if (ns == 0) {             // nothing to attend: zero output
+    for (int d = threadIdx.x; d < D; d += kThreads) store_out<D>(p, row, d, 0.f);
+    return;
+  }
+  if (ns == 1) return;  // finished in place by its only run
+  if (p.fused && ns * p.G * D <= kStageFloats && ns * p.G * 2 <= kStageMl) return;  // merged in place
+  const size_t base = (static_cast<size_t>(b) * ng + r) * p.max_parts;
   const int GD = p.G * D;
 
   float run_m = -INFINITY, run_den = 0.f, run_o[C];
@@ -438,7 +640,8 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(AttnParams p) {
       m[u] = ok ? p.part_ml[(slot * p.G + hh) * 2] : -INFINITY;
       w[u] = ok ? p.part_ml[(slot * p.G + hh) * 2 + 1] : 0.f;
 #pragma unroll
-      for (int k = 0; k < C; ++k) a[u][k] = ok ? p.part_acc[slot * GD + hh * D + lane + 64 * k] : 0.f;
+      for (int k = 0; k < C; ++k)
+        a[u][k] = ok ? p.part_acc[slot * GD + hh * D + lane + 64 * k] : 0.f;
     }
     float bm = run_m;
 #pragma unroll
@@ -505,22 +708,58 @@ hipError_t launch_append(const AppendParams& p, int head_dim, int owned_count,
   return hipGetLastError();
 }
 
-int fused_partial_capacity() { return kFusedPartialFloats; }
-
-hipError_t launch_attention(const AttnParams& p, int head_dim, hipStream_t stream) {
-  const dim3 grid(p.B * p.n_groups, p.n_split);
-  if (head_dim == 64)
+hipError_t launch_attention_main(const AttnParams& p, int head_dim, hipStream_t stream,
+                                 hipEvent_t start, hipEvent_t stop) {
+  const dim3 grid(p.n_blocks);
+  if (start) {  // timed: events recorded with the dispatch itself
+    if (head_dim == 64)
+      hipExtLaunchKernelGGL(attention_kernel<64>, grid, dim3(kThreads), 0, stream, start, stop, 0, p);
+    else
+      hipExtLaunchKernelGGL(attention_kernel<128>, grid, dim3(kThreads), 0, stream, start, stop, 0, p);
+  } else if (head_dim == 64) {
     hipLaunchKernelGGL(attention_kernel<64>, grid, dim3(kThreads), 0, stream, p);
-  else
+  } else {
     hipLaunchKernelGGL(attention_kernel<128>, grid, dim3(kThreads), 0, stream, p);
-  hipError_t err = hipGetLastError();
-  if (err != hipSuccess || p.n_split == 1 || p.fused_combine) return err;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_attention_merge(const AttnParams& p, int head_dim, hipStream_t stream) {
+  if (p.n_blocks == 1) return hipSuccess;  // every unit is finished in place
   const dim3 cgrid(p.B * p.h);
   if (head_dim == 64)
     hipLaunchKernelGGL(combine_kernel<64>, cgrid, dim3(kThreads), 0, stream, p);
   else
     hipLaunchKernelGGL(combine_kernel<128>, cgrid, dim3(kThreads), 0, stream, p);
   return hipGetLastError();
+}
+
+hipError_t launch_plan(const AttnParams& p, hipStream_t stream) {
+  hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(kThreads), 0, stream, p,
+                     reinterpret_cast<RunItem*>(p.plan));
+  return hipGetLastError();
+}
+
+int max_batch() { return kMaxBatch; }
+int stage_floats() { return kStageFloats; }
+
+int resident_workgroups(int head_dim) {
+  static std::atomic<int> cached[2] = {{-1}, {-1}};
+  std::atomic<int>& slot = cached[head_dim == 64 ? 0 : 1];
+  int v = slot.load(std::memory_order_relaxed);
+  if (v >= 0) return v;
+  int dev = 0, cus = 0, per_cu = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+    return 0;
+  const hipError_t err =
+      head_dim == 64
+          ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attention_kernel<64>, kThreads, 0)
+          : hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attention_kernel<128>, kThreads, 0);
+  if (err != hipSuccess) return 0;
+  v = cus * per_cu;
+  slot.store(v, std::memory_order_relaxed);
+  return v;
 }
 
 hipError_t launch_fill(uint32_t* dst, size_t n_words, uint32_t value, hipStream_t stream) {

@@ -48,9 +48,6 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 bool aligned4(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
 
 constexpr int kTileTokens = 32;
-constexpr int kWaves = 4;
-constexpr int kMinTilesPerSplit = kWaves;  // every wave of a workgroup gets a tile
-constexpr int kTargetWorkgroups = 1024;    // ~4 per CU on a 256-CU MI355X
 
 // Derive the per-layer structure of a map; returns an error message or "".
 std::string analyse(mlkv_map& m) {
@@ -116,6 +113,8 @@ mlkv_status check_cache(const mlkv_cache* c, const mlkv_map* map) {
     return fail(MLKV_ERR_CAPACITY, "cache capacity %d is not a multiple of 32", c->capacity);
   if (c->head_dim != 64 && c->head_dim != 128)
     return fail(MLKV_ERR_UNSUPPORTED, "head_dim %d not supported (64 or 128)", c->head_dim);
+  if (c->batch > mlkv::max_batch())
+    return fail(MLKV_ERR_UNSUPPORTED, "batch %d above the supported %d", c->batch, mlkv::max_batch());
   if (c->n_kv != map->n_kv)
     return fail(MLKV_ERR_INVALID_ARG, "cache has %d KV heads, map has %d", c->n_kv, map->n_kv);
   const double elems = 2.0 * c->n_kv * c->batch * static_cast<double>(c->capacity) * c->head_dim;
@@ -125,59 +124,99 @@ mlkv_status check_cache(const mlkv_cache* c, const mlkv_map* map) {
 
 int tiles_of(int len) { return (len + kTileTokens - 1) / kTileTokens; }
 
-// Split-K plan for one layer.  Each workgroup (four waves) streams one split
-// of tiles_per_split 32-token tiles of one (sequence, KV head).  Short
-// sequences (<= 16 tiles) take one split: no partials, no merge.  Otherwise
-// the split is the longest of 64/32/16/8/4 tiles that still gives at least
-// kTargetWorkgroups workgroups, lengthened again while a sequence would have
-// more than kPreferredMaxSplits splits (merge cost grows with the count).
-constexpr int kPreferredMaxSplits = 64;
-constexpr int kMaxSplits = 256;  // the attention kernel's per-sequence limit
+// Split-K plan for one layer.  The kernel cuts every (sequence, KV head)
+// unit into runs of R tiles, R chosen on the device from the actual lengths
+// so that all runs fit the launched workgroups.  The host picks that count:
+// the device's resident capacity, capped at 32 per unit (more would only
+// multiply partials to merge) and at what runs of kMinTiles tiles need, but
+// at least one per unit; a single unit of at most 16 tiles takes one
+// workgroup (no partials at all).
+struct Plan {
+  int n_blocks;
+  int max_parts;  // bound on the runs of one unit
+  int max_tiles;  // tiles of the longest sequence allowed by max_len
+  int min_tiles;  // least tiles per run
+  int fused;      // 1: every unit's runs are merged in place (no merge kernel)
+};
+constexpr int kMinTiles = 4;
+constexpr int kMaxRunsPerUnit = 32;
+constexpr int kFallbackResident = 768;  // 256 CUs x 3 when no device can be queried
 
-void plan(const mlkv_map* map, int layer, int batch, int max_len, int* tps_out, int* ns_out) {
-  const int max_tiles = tiles_of(max_len < 1 ? 1 : max_len);
+long workgroups_for(long resident, long units, long t_max, int min_tiles) {
+  long g = resident < kMaxRunsPerUnit * units ? resident : kMaxRunsPerUnit * units;
+  // Runs of min_tiles tiles always fit this many workgroups: no more needed.
+  const long enough = (t_max + min_tiles - 1) / min_tiles + units;
+  g = g < enough ? g : enough;
+  return g > units ? g : units;
+}
+
+// With MLKV_COMBINE=fused, runs are merged inside the attention kernel (by
+// the last run of each unit to finish) when every unit's partials fit the
+// kernel's staging area; the run length floor that guarantees it is accepted
+// if it still leaves at least half the resident workgroups busy.  Otherwise
+// (and by default: on MI355X the merge kernel measured as fast or faster) a
+// separate merge kernel runs.
+Plan plan(const mlkv_map* map, int layer, int batch, int max_len, int head_dim) {
+  Plan pl{};
+  pl.max_tiles = tiles_of(max_len < 1 ? 1 : max_len);
   const long units = static_cast<long>(batch) * map->kv_count[layer];
-  int tps;
-  const char* env = std::getenv("MLKV_SPLIT_TOKENS");
-  if (env && *env) {
-    tps = std::atoi(env) / kTileTokens;
-    tps = (tps / kMinTilesPerSplit) * kMinTilesPerSplit;
-    if (tps < kMinTilesPerSplit) tps = kMinTilesPerSplit;
-  } else if (max_tiles <= 4 * kMinTilesPerSplit) {
-    tps = max_tiles;
-  } else {
-    tps = kMinTilesPerSplit;
-    for (int cand = 64; cand >= kMinTilesPerSplit; cand /= 2) {
-      if (units * ((max_tiles + cand - 1) / cand) >= kTargetWorkgroups) {
-        tps = cand;
-        break;
-      }
-    }
-    while ((max_tiles + tps - 1) / tps > kPreferredMaxSplits) tps *= 2;
+  const long t_max = units * pl.max_tiles;
+  long resident = mlkv::resident_workgroups(head_dim);
+  if (resident <= 0) resident = kFallbackResident;
+  if (const char* env = std::getenv("MLKV_WORKGROUPS")) {
+    const long w = std::atol(env);
+    if (w > 0) resident = w;
   }
-  while ((max_tiles + tps - 1) / tps > kMaxSplits) tps *= 2;
-  int ns = (max_tiles + tps - 1) / tps;
-  if (ns < 1) ns = 1;
-  if (ns == 1) tps = max_tiles < 1 ? 1 : max_tiles;  // one split: exactly the needed tiles
-  *tps_out = tps;
-  *ns_out = ns;
+  pl.min_tiles = kMinTiles;
+  pl.fused = 0;
+  const long cap_parts = mlkv::stage_floats() / (static_cast<long>(map->group[layer]) * head_dim);
+  const char* comb = std::getenv("MLKV_COMBINE");  // "fused": merge in place where it fits
+  const bool allow_fused = comb && std::strcmp(comb, "fused") == 0;
+  if (allow_fused && cap_parts >= 2) {
+    long mt = (pl.max_tiles + cap_parts - 1) / cap_parts;
+    mt = mt > kMinTiles ? mt : kMinTiles;
+    const long g = workgroups_for(resident, units, t_max, static_cast<int>(mt));
+    if (2 * g >= resident || g >= units * ((pl.max_tiles + mt - 1) / mt)) {
+      pl.min_tiles = static_cast<int>(mt);
+      pl.fused = 1;
+    }
+  }
+  long g = workgroups_for(resident, units, t_max, pl.min_tiles);
+  if (units == 1 && t_max <= 4 * kMinTiles) g = 1;
+  pl.n_blocks = static_cast<int>(g);
+  pl.max_parts = (pl.max_tiles + pl.min_tiles - 1) / pl.min_tiles + 1;
+  return pl;
 }
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
-// Workspace layout of one call (nothing when every sequence fits one split):
-//   counters  int32 [batch * h]                 (256-byte aligned blocks)
-//   part_acc  fp32  [batch * h * n_split][head_dim]
-//   part_ml   fp32  [batch * h * n_split][2]
-size_t counters_bytes(int batch, int h) {
-  return align_up(static_cast<size_t>(batch) * h * sizeof(int32_t), 256);
+// Workspace layout of one call (nothing when one workgroup does all):
+//   counters  int32 [batch * h]  finished runs per unit, zero between calls
+//   runs      int32 [batch]                          (256-byte aligned blocks)
+//   plan      32-byte run items [n_blocks]            (used by mlkv_decode_step)
+//   part_acc  fp32  [batch * h * max_parts][head_dim]
+//   part_ml   fp32  [batch * h * max_parts][2]
+constexpr size_t kRunItemBytes = 32;
+
+struct WsLayout {
+  size_t counters, runs, plan, acc, ml, total;
+};
+
+WsLayout ws_layout(int batch, int h, int head_dim, const Plan& pl) {
+  WsLayout w{};
+  if (pl.n_blocks <= 1) return w;
+  const size_t rows = static_cast<size_t>(batch) * h * pl.max_parts;
+  w.counters = 0;
+  w.runs = align_up(static_cast<size_t>(batch) * h * sizeof(int32_t), 256);
+  w.plan = w.runs + align_up(static_cast<size_t>(batch) * sizeof(int32_t), 256);
+  w.acc = w.plan + align_up(static_cast<size_t>(pl.n_blocks) * kRunItemBytes, 256);
+  w.ml = w.acc + align_up(rows * head_dim * sizeof(float), 256);
+  w.total = w.ml + rows * 2 * sizeof(float);
+  return w;
 }
 
-size_t workspace_need(int batch, int h, int head_dim, int n_split) {
-  if (n_split <= 1) return 0;
-  const size_t rows = static_cast<size_t>(batch) * h * n_split;
-  return counters_bytes(batch, h) + align_up(rows * head_dim * sizeof(float), 256) +
-         rows * 2 * sizeof(float);
+size_t workspace_need(int batch, int h, int head_dim, const Plan& pl) {
+  return ws_layout(batch, h, head_dim, pl).total;
 }
 
 mlkv_status check_lengths_if_requested(const int32_t* lens, int batch, int offset, int limit,
@@ -197,14 +236,24 @@ mlkv_status check_lengths_if_requested(const int32_t* lens, int batch, int offse
   return MLKV_OK;
 }
 
+// Event pairs around attention launches (mlkv_profile_*).
+struct Profile {
+  std::vector<hipEvent_t> start, stop;
+  int used = 0;
+  bool on = false;
+};
+thread_local Profile g_profile;
+
+// plan_mode: 0 = schedule inside the attention kernel; 1 = compute the plan
+// into the workspace first (plan_kernel); 2 = reuse the plan already there.
 mlkv_status attention_impl(int layer, const void* q, const mlkv_cache* cache, const mlkv_map* map,
                            const int32_t* lens, int len_offset, void* out, mlkv_out_dtype dt,
-                           int max_len_hint, void* ws, size_t ws_bytes, hipStream_t stream) {
+                           int max_len_hint, void* ws, size_t ws_bytes, hipStream_t stream,
+                           int plan_mode = 0) {
   const int B = cache->batch, S = cache->capacity, D = cache->head_dim;
   const int max_len = max_len_hint <= 0 ? S : max_len_hint;
-  int tps = 0, ns = 0;
-  plan(map, layer, B, max_len, &tps, &ns);
-  const size_t need = workspace_need(B, map->h, D, ns);
+  const Plan pl = plan(map, layer, B, max_len, D);
+  const size_t need = workspace_need(B, map->h, D, pl);
   if (need > 0 && (!ws || ws_bytes < need))
     return fail(MLKV_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need,
                 ws ? ws_bytes : 0);
@@ -215,30 +264,37 @@ mlkv_status attention_impl(int layer, const void* q, const mlkv_cache* cache, co
   p.v = static_cast<const uint16_t*>(cache->v);
   p.lens = lens;
   p.out = out;
-  const size_t rows = static_cast<size_t>(B) * map->h * ns;
+  const WsLayout wl = ws_layout(B, map->h, D, pl);
   char* base = static_cast<char*>(ws);
-  const size_t cnt = counters_bytes(B, map->h);
-  p.counters = need ? reinterpret_cast<int*>(base) : nullptr;
-  p.part_acc = need ? reinterpret_cast<float*>(base + cnt) : nullptr;
-  p.part_ml = need ? reinterpret_cast<float*>(base + cnt + align_up(rows * D * sizeof(float), 256))
-                   : nullptr;
+  p.counters = need ? reinterpret_cast<int*>(base + wl.counters) : nullptr;
+  p.runs = need ? reinterpret_cast<int*>(base + wl.runs) : nullptr;
+  p.plan = need && plan_mode != 0 ? base + wl.plan : nullptr;
+  p.part_acc = need ? reinterpret_cast<float*>(base + wl.acc) : nullptr;
+  p.part_ml = need ? reinterpret_cast<float*>(base + wl.ml) : nullptr;
   p.B = B;
   p.h = map->h;
   p.S = S;
   p.kv_begin = map->kv_begin[layer];
   p.G = map->group[layer];
   p.n_groups = map->kv_count[layer];
-  p.n_split = ns;
-  p.tiles_per_split = tps;
+  p.max_len = max_len;
+  p.n_blocks = pl.n_blocks;
+  p.min_tiles = pl.min_tiles;
+  p.max_parts = pl.max_parts;
+  p.fused = pl.fused;
+  p.D = D;
   p.len_offset = len_offset;
   p.out_bf16 = dt == MLKV_OUT_BF16 ? 1 : 0;
   p.scale_log2 = static_cast<float>(1.4426950408889634 / std::sqrt(static_cast<double>(D)));
-  // Split merge: a separate combine kernel by default; MLKV_COMBINE=fused lets
-  // the last workgroup of each sequence merge in place where the partials fit.
-  const bool fits = static_cast<long>(ns) * map->group[layer] * D <= mlkv::fused_partial_capacity();
-  const char* comb = std::getenv("MLKV_COMBINE");
-  p.fused_combine = fits && comb && std::strcmp(comb, "fused") == 0 ? 1 : 0;
-  const hipError_t err = mlkv::launch_attention(p, D, stream);
+  hipError_t err = hipSuccess;
+  if (p.plan && plan_mode == 1) err = mlkv::launch_plan(p, stream);
+  if (err != hipSuccess) return fail(MLKV_ERR_HIP, "plan launch: %s", hipGetErrorString(err));
+  Profile& prof = g_profile;
+  const bool timed = prof.on && prof.used < static_cast<int>(prof.start.size());
+  err = mlkv::launch_attention_main(p, D, stream, timed ? prof.start[prof.used] : nullptr,
+                                               timed ? prof.stop[prof.used] : nullptr);
+  if (err == hipSuccess && timed) ++prof.used;
+  if (err == hipSuccess && !pl.fused) err = mlkv::launch_attention_merge(p, D, stream);
   if (err != hipSuccess) return fail(MLKV_ERR_HIP, "attention launch: %s", hipGetErrorString(err));
   return MLKV_OK;
 }
@@ -384,10 +440,16 @@ size_t mlkv_cache_bytes(const mlkv_map* map, int batch, int capacity, int head_d
 
 size_t mlkv_workspace_bytes(const mlkv_map* map, int batch, int capacity, int head_dim) {
   if (!map || batch <= 0 || capacity <= 0 || (head_dim != 64 && head_dim != 128)) return 0;
-  // The most splits any plan can produce.
-  int ns_max = (tiles_of(capacity) + kMinTilesPerSplit - 1) / kMinTilesPerSplit;
-  ns_max = ns_max > kMaxSplits ? kMaxSplits : ns_max;
-  return workspace_need(batch, map->h, head_dim, ns_max);
+  size_t best = 0;
+  for (int n = 0; n < map->l; ++n) {
+    Plan pl = plan(map, n, batch, capacity, head_dim);
+    // Size for the most workgroups any device could get (32 per unit).
+    pl.n_blocks = kMaxRunsPerUnit * batch * map->kv_count[n];
+    pl.n_blocks = pl.n_blocks > 2 ? pl.n_blocks : 2;
+    const size_t need = workspace_need(batch, map->h, head_dim, pl);
+    best = need > best ? need : best;
+  }
+  return best;
 }
 
 mlkv_status mlkv_workspace_init(void* workspace, size_t workspace_bytes, hipStream_t stream) {
@@ -400,19 +462,18 @@ mlkv_status mlkv_workspace_init(void* workspace, size_t workspace_bytes, hipStre
   return ok();
 }
 
-mlkv_status mlkv_plan_splits(const mlkv_map* map, int layer, int batch, int capacity, int head_dim,
-                             int max_len, int* tokens_per_split, int* n_splits) {
+mlkv_status mlkv_plan(const mlkv_map* map, int layer, int batch, int capacity, int head_dim,
+                      int max_len, int* workgroups, int* max_parts) {
   if (check_map(map) != MLKV_OK) return MLKV_ERR_INVALID_ARG;
   if (layer < 0 || layer >= map->l) return fail(MLKV_ERR_INVALID_ARG, "layer out of range");
-  if (batch <= 0 || capacity <= 0 || !tokens_per_split || !n_splits)
+  if (batch <= 0 || capacity <= 0 || !workgroups || !max_parts)
     return fail(MLKV_ERR_INVALID_ARG, "bad arguments");
   if (head_dim != 64 && head_dim != 128) return fail(MLKV_ERR_UNSUPPORTED, "head_dim");
   if (max_len <= 0) max_len = capacity;
   if (max_len > capacity) return fail(MLKV_ERR_CAPACITY, "max_len above capacity");
-  int tps = 0, ns = 0;
-  plan(map, layer, batch, max_len, &tps, &ns);
-  *tokens_per_split = tps * kTileTokens;
-  *n_splits = ns;
+  const Plan pl = plan(map, layer, batch, max_len, head_dim);
+  *workgroups = pl.n_blocks;
+  *max_parts = pl.max_parts;
   return ok();
 }
 
@@ -488,9 +549,7 @@ mlkv_status mlkv_decode_step(const void* q_all, const void* k_new_all, const voi
   {
     const int max_len = max_len_hint <= 0 ? cache->capacity : max_len_hint;
     for (int n = 0; n < map->l; ++n) {
-      int tps = 0, ns = 0;
-      plan(map, n, B, max_len, &tps, &ns);
-      const size_t need = workspace_need(B, h, D, ns);
+      const size_t need = workspace_need(B, h, D, plan(map, n, B, max_len, D));
       if (need > 0 && (!workspace || workspace_bytes < need))
         return fail(MLKV_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need,
                     workspace ? workspace_bytes : 0);
@@ -504,6 +563,7 @@ mlkv_status mlkv_decode_step(const void* q_all, const void* k_new_all, const voi
   const size_t out_elem_bytes = out_dtype == MLKV_OUT_BF16 ? 2 : 4;
   const uint16_t* k_new = static_cast<const uint16_t*>(k_new_all);
   const uint16_t* v_new = static_cast<const uint16_t*>(v_new_all);
+  int planned_key = -1;
   for (int n = 0; n < map->l; ++n) {
     if (map->own_count[n] > 0) {
       const size_t col = static_cast<size_t>(map->own_begin[n]) * D;
@@ -513,11 +573,66 @@ mlkv_status mlkv_decode_step(const void* q_all, const void* k_new_all, const voi
     }
     const void* q = static_cast<const uint16_t*>(q_all) + layer_elems * n;
     void* out = static_cast<char*>(out_all) + layer_elems * out_elem_bytes * n;
+    // All layers share the lengths, so one plan serves every layer with the
+    // same number of KV heads (and hence the same workgroup count).
+    const int key = map->kv_count[n];
+    const int mode = key == planned_key ? 2 : 1;
     if ((s = attention_impl(n, q, cache, map, ctx_lens, 1, out, out_dtype, max_len_hint, workspace,
-                            workspace_bytes, stream)) != MLKV_OK)
+                            workspace_bytes, stream, mode)) != MLKV_OK)
       return s;
+    planned_key = key;
   }
   return ok();
+}
+
+mlkv_status mlkv_profile_enable(int max_launches) {
+  if (max_launches <= 0) return fail(MLKV_ERR_INVALID_ARG, "max_launches must be positive");
+  mlkv_profile_disable();
+  Profile& prof = g_profile;
+  prof.start.assign(max_launches, nullptr);
+  prof.stop.assign(max_launches, nullptr);
+  for (int i = 0; i < max_launches; ++i) {
+    if (hipEventCreate(&prof.start[i]) != hipSuccess || hipEventCreate(&prof.stop[i]) != hipSuccess) {
+      mlkv_profile_disable();
+      return fail(MLKV_ERR_HIP, "hipEventCreate failed");
+    }
+  }
+  prof.used = 0;
+  prof.on = true;
+  return ok();
+}
+
+mlkv_status mlkv_profile_read(int* launches, double* total_ms, double* min_ms, double* max_ms) {
+  if (!launches || !total_ms || !min_ms || !max_ms)
+    return fail(MLKV_ERR_INVALID_ARG, "output pointers must be non-NULL");
+  Profile& prof = g_profile;
+  double tot = 0.0, lo = 0.0, hi = 0.0;
+  for (int i = 0; i < prof.used; ++i) {
+    float ms = 0.f;
+    if (hipEventSynchronize(prof.stop[i]) != hipSuccess ||
+        hipEventElapsedTime(&ms, prof.start[i], prof.stop[i]) != hipSuccess)
+      return fail(MLKV_ERR_HIP, "reading profile events failed");
+    tot += ms;
+    lo = i == 0 || ms < lo ? ms : lo;
+    hi = i == 0 || ms > hi ? ms : hi;
+  }
+  *launches = prof.used;
+  *total_ms = tot;
+  *min_ms = lo;
+  *max_ms = hi;
+  return ok();
+}
+
+void mlkv_profile_disable(void) {
+  Profile& prof = g_profile;
+  for (hipEvent_t e : prof.start)
+    if (e) (void)hipEventDestroy(e);
+  for (hipEvent_t e : prof.stop)
+    if (e) (void)hipEventDestroy(e);
+  prof.start.clear();
+  prof.stop.clear();
+  prof.used = 0;
+  prof.on = false;
 }
 
 }  // extern "C"

@@ -117,7 +117,7 @@ def test_entry_points_reject_bad_arguments():
     assert names[L.mlkv_decode_attention(0, 0x30000, ref, mp.handle, 0x40002, 0x50000, 0, 0, 0x60000, 1 << 30, None)] == "MLKV_ERR_ALIGNMENT"
     assert names[L.mlkv_decode_attention(0, 0x30000, ref, mp.handle, 0x40000, 0x50000, 7, 0, 0x60000, 1 << 30, None)] == "MLKV_ERR_INVALID_ARG"
     assert names[L.mlkv_decode_attention(0, 0x30000, ref, mp.handle, 0x40000, 0x50000, 0, 65, 0x60000, 1 << 30, None)] == "MLKV_ERR_CAPACITY"
-    # a workspace that is too small is refused (B=2, 64 tokens plans 1 split: no workspace)
+    # a workspace that is too small is refused (B=2, 64 tokens plans 1 workgroup: no workspace)
     big = mlkv._Cache(0x10000, 0x20000, 4, 2, 4096, 64)
     assert names[L.mlkv_decode_attention(0, 0x30000, ctypes.byref(big), mp.handle, 0x40000, 0x50000, 0, 0, 0x60000, 16, None)] == "MLKV_ERR_WORKSPACE"
     assert names[L.mlkv_decode_step(0x30000, 0x30000, 0x30000, ctypes.byref(big), mp.handle, 0x40000, 0x50000, 0, 0, None, 0, None)] == "MLKV_ERR_WORKSPACE"
@@ -133,14 +133,22 @@ def test_entry_points_reject_bad_arguments():
 
 
 def test_workspace_covers_every_plan():
+    """mlkv_workspace_bytes covers the documented layout of every plan:
+    counters [B*h], runs [B], run items [workgroups], partials."""
     mp = mlkv.Map.uniform(12, 12, 4, 1)
+    al = lambda x: (x + 255) // 256 * 256  # noqa: E731
     for B, S in [(1, 160), (8, 32832), (128, 2112), (32, 2112)]:
         ws = mp.workspace_bytes(B, S, 64)
         for max_len in [x for x in (1, 31, 33, 129, 511, 513, S // 2, S) if x <= S]:
-            tps, ns = mp.plan_splits(0, B, S, 64, max_len)
-            assert tps % 32 == 0 and ns >= 1 and tps * ns >= max_len
-            al = lambda x: (x + 255) // 256 * 256  # noqa: E731
-            need = 0 if ns == 1 else al(B * 12 * 4) + al(B * 12 * ns * 64 * 4) + B * 12 * ns * 8
+            wg, parts = mp.plan(0, B, S, 64, max_len)
+            tiles = -(-max_len // 32)
+            assert 2 <= parts <= -(-tiles // 4) + 1
+            assert B <= wg <= -(-(B * tiles) // 4) + B or (B == 1 and wg == 1)
+            if B == 1 and tiles <= 16:
+                assert wg == 1
+            rows = B * 12 * parts
+            need = 0 if wg == 1 else (al(B * 12 * 4) + al(B * 4) + al(wg * 32)
+                                      + al(rows * 64 * 4) + rows * 8)
             assert need <= ws
 
 

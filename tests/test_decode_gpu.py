@@ -100,46 +100,51 @@ def test_length_sweep_across_tile_boundaries(D, m, g):
     dw = DeviceWorkload(w)
     lens = np.array(LEN_SWEEP, dtype=np.int32)
     lens_d = torch.from_numpy(lens).cuda()
-    for split_tokens in ("", "128", "256"):
-        os.environ["MLKV_SPLIT_TOKENS"] = split_tokens
+    for wg, comb in (("", ""), ("3", ""), ("40", ""), ("", "fused"), ("40", "fused")):
+        os.environ["MLKV_WORKGROUPS"] = wg
+        os.environ["MLKV_COMBINE"] = comb
         try:
             for n in (0, w.l - 1):
-                say(f"length sweep D={D} m={m} g={g} layer={n} split={split_tokens or 'auto'}")
+                say(f"length sweep D={D} m={m} g={g} layer={n} workgroups={wg or 'auto'} "
+                    f"merge={comb or 'kernel'}")
                 out = torch.empty((w.B, w.h, w.D), dtype=torch.float32, device="cuda")
                 mlkv.decode_attention(n, dw.q[n], dw.cache, dw.map, lens_d, out, ws=dw.ws)
                 torch.cuda.synchronize()
                 ref = oracle.decode_attention(n, dw.host["q"][n], dw.host["k_cache"],
                                               dw.host["v_cache"], dw.kv_of, lens)
-                check_close(out.cpu().numpy(), ref, f"sweep D{D} g{g} L{n} s{split_tokens}")
+                check_close(out.cpu().numpy(), ref, f"sweep D{D} g{g} L{n} wg{wg} {comb}")
         finally:
-            os.environ.pop("MLKV_SPLIT_TOKENS", None)
+            os.environ.pop("MLKV_WORKGROUPS", None)
+            os.environ.pop("MLKV_COMBINE", None)
 
 
 def test_split_count_invariance_and_determinism():
+    """Results do not depend on how many workgroups share the tiles (up to
+    rounding), and a repeated call is bitwise identical."""
     w = small("mlkv4_b8_long", B=2, ctx=5000)
     dw = DeviceWorkload(w)
     lens_d = torch.from_numpy(dw.host["ctx"]).cuda()
     outs = {}
-    for split_tokens in ("128", "512", "2048", "8192", ""):
-        os.environ["MLKV_SPLIT_TOKENS"] = split_tokens
+    for wg, comb in (("1", ""), ("7", ""), ("64", ""), ("300", ""), ("", ""), ("", "fused"),
+                     ("300", "fused")):
+        os.environ["MLKV_WORKGROUPS"] = wg
+        os.environ["MLKV_COMBINE"] = comb
         try:
-            say(f"split invariance split={split_tokens or 'auto'}")
+            say(f"workgroup invariance workgroups={wg or 'auto'} merge={comb or 'kernel'}")
             o = torch.empty((w.B, w.h, w.D), dtype=torch.float32, device="cuda")
             mlkv.decode_attention(2, dw.q[2], dw.cache, dw.map, lens_d, o, ws=dw.ws)
             o2 = torch.empty_like(o)
             mlkv.decode_attention(2, dw.q[2], dw.cache, dw.map, lens_d, o2, ws=dw.ws)
             torch.cuda.synchronize()
             assert torch.equal(o, o2), "run-to-run results differ"
-            outs[split_tokens] = o.cpu().numpy().astype(np.float64)
+            outs[wg + comb] = o.cpu().numpy().astype(np.float64)
         finally:
-            os.environ.pop("MLKV_SPLIT_TOKENS", None)
-    # every call hands the split counters (head of the workspace) back at zero
-    counters = dw.ws[: w.B * w.h * 4].view(torch.int32).cpu().numpy()
-    assert np.all(counters == 0)
+            os.environ.pop("MLKV_WORKGROUPS", None)
+            os.environ.pop("MLKV_COMBINE", None)
     ref = oracle.decode_attention(2, dw.host["q"][2], dw.host["k_cache"], dw.host["v_cache"],
                                   dw.kv_of, dw.host["ctx"])
     for k, o in outs.items():
-        check_close(o, ref, f"split {k or 'auto'}")
+        check_close(o, ref, f"workgroups {k or 'auto'}")
 
 
 def test_single_position_and_empty():
@@ -175,7 +180,7 @@ def test_needle_token(pos_kind):
     kc = dw.host["k_cache"]
     kc[0, b, pos] = synth.f32_to_bf16(synth.bf16_to_f32(q) * 4.0)
     dw.cache.load_rows(kc, dw.host["v_cache"])
-    os.environ["MLKV_SPLIT_TOKENS"] = "512"
+    os.environ["MLKV_WORKGROUPS"] = "5"
     try:
         say(f"needle at {pos} ({pos_kind})")
         out = torch.empty((w.B, w.h, w.D), dtype=torch.float32, device="cuda")
@@ -184,7 +189,7 @@ def test_needle_token(pos_kind):
                               ws=dw.ws)
         torch.cuda.synchronize()
     finally:
-        os.environ.pop("MLKV_SPLIT_TOKENS", None)
+        os.environ.pop("MLKV_WORKGROUPS", None)
     ref = oracle.decode_attention(0, dw.host["q"][0], kc, dw.host["v_cache"], dw.kv_of, lens)
     _, alpha = oracle.attend_one(q, kc[0, b, :L], dw.host["v_cache"][0, b, :L])
     assert alpha[pos] > 0.99
@@ -270,3 +275,24 @@ def test_map_sweep_full_size(mg):
     ref, k_ref, v_ref = _oracle_step(dw)
     assert np.array_equal(k_gpu, k_ref) and np.array_equal(v_gpu, v_ref), "cache differs"
     check_close(out, ref, f"step {w.name}")
+
+
+def test_full_size_step_with_in_place_merge():
+    """The ragged 128-sequence step with runs merged inside the attention kernel
+    (MLKV_COMBINE=fused) gives the same cache and outputs as the oracle."""
+    w = synth.get_workload("mlkv4_b128_ragged")
+    os.environ["MLKV_COMBINE"] = "fused"
+    try:
+        say("full step in-place merge: uploading")
+        dw = DeviceWorkload(w)
+        say("full step in-place merge: running (twice: counters must reset)")
+        _run_step(dw)
+        dw2 = DeviceWorkload(w)  # fresh cache, same workspace contract
+        dw2.ws = dw.ws
+        out = _run_step(dw2).cpu().numpy()
+    finally:
+        os.environ.pop("MLKV_COMBINE", None)
+    k_gpu, v_gpu = dw2.read_cache()
+    ref, k_ref, v_ref = _oracle_step(dw2)
+    assert np.array_equal(k_gpu, k_ref) and np.array_equal(v_gpu, v_ref), "cache differs"
+    check_close(out, ref, "step in-place merge")
