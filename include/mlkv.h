@@ -164,7 +164,7 @@ mlkv_status mlkv_cache_append(int layer, const mlkv_map* map, const mlkv_cache* 
  *   out: device [batch][h][head_dim], fp32 or bf16 per out_dtype.
  *   max_len_hint: an upper bound of every L_b (<= 0 means capacity); it sizes
  *        the work plan.  Lengths above it are truncated to it.
- *   batch: at most 4096 sequences (else MLKV_ERR_UNSUPPORTED).
+ *   batch: at most 2048 sequences (else MLKV_ERR_UNSUPPORTED).
  *   workspace: device memory of at least mlkv_workspace_bytes(...) bytes,
  *        16-byte aligned, zeroed once by mlkv_workspace_init (the split
  *        counters must start at zero; each call returns them to zero).
@@ -203,10 +203,16 @@ mlkv_status mlkv_decode_step(const void* q_all, const void* k_new_all, const voi
 /* Work plan mlkv_decode_attention uses for `layer` at this max length: the
  * 32-token tiles of all (sequence, KV head) pairs form one flat list shared
  * equally by `workgroups` workgroups (the device's resident capacity, capped
- * at 32 per (sequence, KV head) and at one per 4 tiles; one workgroup for at
+ * at 128 per (sequence, KV head) and at one per 4 tiles; one workgroup for at
  * most 16 tiles); `max_parts` bounds the workgroups covering one sequence.
- * Env MLKV_WORKGROUPS overrides the resident capacity used.  Returns
- * MLKV_ERR_* on invalid arguments. */
+ * Environment overrides, read on every call (tests and tuning):
+ *   MLKV_WORKGROUPS=n   resident capacity assumed instead of the device's;
+ *   MLKV_COMBINE=fused  the last run of each unit merges its runs in place
+ *                       when they fit the kernel's staging area;
+ *   MLKV_WIDE=1         one run per unit on a wider workgroup (no partials,
+ *                       no merge kernel).
+ * The workspace size from mlkv_workspace_bytes covers every choice.
+ * Returns MLKV_ERR_* on invalid arguments. */
 mlkv_status mlkv_plan(const mlkv_map* map, int layer, int batch, int capacity, int head_dim,
                       int max_len, int* workgroups, int* max_parts);
 

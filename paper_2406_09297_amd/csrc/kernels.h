@@ -34,6 +34,8 @@ struct AttnParams {
   int max_parts;             // partial slots per unit (bound on its runs)
   int len_offset, out_bf16;
   int fused;                 // 1: the last run of a unit merges its partials when they fit LDS
+  int merge_waves;           // waves merging one (sequence, head) row: 1 or 4
+  int waves;                 // waves per attention workgroup: 4, or wide_waves() for single runs
   float scale_log2;          // log2(e) / sqrt(D)
 };
 
@@ -48,8 +50,10 @@ hipError_t launch_attention_merge(const AttnParams& p, int head_dim, hipStream_t
 // One workgroup computing the run schedule into p.plan (and p.runs).
 hipError_t launch_plan(const AttnParams& p, hipStream_t stream);
 int max_batch();
-int stage_floats();  // partial-output floats one workgroup can merge in place                     // sequences one call may hold
+int stage_floats();  // partial-output floats one workgroup can merge in place
 int resident_workgroups(int head_dim); // attention workgroups the device holds at once (0: none)
+int wide_waves();                      // waves per workgroup of the one-run-per-unit layout
+int default_waves();                   // waves per workgroup otherwise
 hipError_t launch_fill(uint32_t* dst, size_t n_words, uint32_t value, hipStream_t stream);
 
 }  // namespace mlkv

@@ -48,10 +48,10 @@ typedef uint16_t u16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kTile = 32;     // tokens per wave iteration
-constexpr int kWaves = 4;     // waves per workgroup
+constexpr int kWaves = 4;      // waves per workgroup (split runs, merge kernel)
 constexpr int kThreads = kWaves * 64;
+constexpr int kWideWaves = 8;  // waves per workgroup when each unit is one run
 constexpr int kMaxBatch = 2048;  // sequences one call may hold (schedule tables in LDS)
-// A sequence has at most 256 splits (the host planner keeps within that).
 
 __device__ __forceinline__ u16x8 load16(const uint16_t* p) {
   return *reinterpret_cast<const u16x8*>(p);
@@ -221,6 +221,19 @@ __device__ __forceinline__ void store_out(const AttnParams& p, size_t row, int d
     static_cast<float*>(p.out)[row * D + d] = val;
 }
 
+// Four consecutive channels d..d+3 of output row `row` (d a multiple of 4).
+template <int D>
+__device__ __forceinline__ void store_out4(const AttnParams& p, size_t row, int d, f32x4 v) {
+  if (p.out_bf16) {
+    typedef uint16_t u16x4 __attribute__((ext_vector_type(4)));
+    const u16x4 bits = {f32_to_bf16_bits(v[0]), f32_to_bf16_bits(v[1]), f32_to_bf16_bits(v[2]),
+                        f32_to_bf16_bits(v[3])};
+    *reinterpret_cast<u16x4*>(static_cast<uint16_t*>(p.out) + row * D + d) = bits;
+  } else {
+    *reinterpret_cast<f32x4*>(static_cast<float*>(p.out) + row * D + d) = v;
+  }
+}
+
 __device__ __forceinline__ float wave_max(float v) {
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) v = fmaxf(v, __shfl_xor(v, off));
@@ -249,14 +262,14 @@ struct SchedShared {
 constexpr int kStageFloats = 8192;
 constexpr int kStageMl = 512;
 
-template <int D>
-struct AttnShared {
+template <int D, int W>
+struct alignas(16) AttnShared {
   union {  // phases: schedule, then the waves' merge, then (last run only) staging
     SchedShared sc;
     struct {
-      float acc[kWaves][16][D + 4];
-      float m[kWaves][16];
-      float l[kWaves][16];
+      float acc[W][16][D + 4];
+      float m[W][16];
+      float l[W][16];
     };
     float stage[kStageFloats];
   };
@@ -359,10 +372,11 @@ __device__ void schedule_wave0(const AttnParams& p, SchedShared& sm, int g) {
   }
 }
 
-template <int D>
-__global__ __launch_bounds__(kThreads) void attention_kernel(AttnParams p) {
+template <int D, int W>
+__global__ __launch_bounds__(W * 64) void attention_kernel(AttnParams p) {
   constexpr int KK = Tile<D>::KK, DB = Tile<D>::DB;
-  __shared__ AttnShared<D> sm;
+  constexpr int NT = W * 64;  // threads
+  __shared__ AttnShared<D, W> sm;
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int col = lane & 15;  // query head inside the group / MFMA row
@@ -386,11 +400,11 @@ __global__ __launch_bounds__(kThreads) void attention_kernel(AttnParams p) {
     const int R = sm.sc.sched[0];
     const int n_runs = sm.sc.sched[1];
     if (g == 0 && p.runs)  // runs per sequence, for the merge kernel
-      for (int bb = threadIdx.x; bb < p.B; bb += kThreads)
+      for (int bb = threadIdx.x; bb < p.B; bb += NT)
         p.runs[bb] = div_up(tiles_of(sm.sc.len[bb]), R);
     for (int bb = g; bb < p.B; bb += p.n_blocks) {  // sequences with nothing to attend
       if (sm.sc.len[bb] > 0) continue;
-      for (int i = threadIdx.x; i < p.h * D; i += kThreads)
+      for (int i = threadIdx.x; i < p.h * D; i += NT)
         store_out<D>(p, static_cast<size_t>(bb) * p.h, i, 0.f);
     }
     if (g >= n_runs) return;
@@ -431,19 +445,19 @@ __global__ __launch_bounds__(kThreads) void attention_kernel(AttnParams p) {
 #pragma unroll
   for (int db = 0; db < DB; ++db) st.acc[db] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // The loads of tile it+kWaves are issued before tile it is consumed; the
+  // The loads of tile it+W are issued before tile it is consumed; the
   // prefetch is never skipped (past the last tile it re-reads the current,
   // cache-resident tile) so that the wait before each tile covers only that
   // tile's own loads.
   if (it < k1) {
     load_tile(ta, kbase, vbase, it * kTile, col, grp);
     for (;;) {
-      int nxt = it + kWaves;
+      int nxt = it + W;
       load_tile(tb, kbase, vbase, (nxt < k1 ? nxt : it) * kTile, col, grp);
       process_tile(st, ta, qf, it * kTile, L, grp, p.scale_log2);
       it = nxt;
       if (it >= k1) break;
-      nxt = it + kWaves;
+      nxt = it + W;
       load_tile(ta, kbase, vbase, (nxt < k1 ? nxt : it) * kTile, col, grp);
       process_tile(st, tb, qf, it * kTile, L, grp, p.scale_log2);
       it = nxt;
@@ -466,31 +480,39 @@ __global__ __launch_bounds__(kThreads) void attention_kernel(AttnParams p) {
   const size_t unit = static_cast<size_t>(b) * p.n_groups + r;
   const size_t slot = unit * p.max_parts + j;
   const bool fuse = nb > 1 && p.fused && nb * GD <= kStageFloats && nb * p.G * 2 <= kStageMl;
-  for (int idx = threadIdx.x; idx < GD; idx += kThreads) {
-    const int hh = idx / D;
-    const int d = idx - hh * D;
+  // Each thread merges four channels of one head over the waves.
+  constexpr int D4 = D / 4;
+  for (int idx = threadIdx.x; idx < p.G * D4; idx += NT) {
+    const int hh = idx / D4;
+    const int d = (idx - hh * D4) * 4;
+    float mw[W];
     float M = -INFINITY;
 #pragma unroll
-    for (int w = 0; w < kWaves; ++w) M = fmaxf(M, sm.m[w][hh]);
-    float wsum = 0.f, o = 0.f;
+    for (int w = 0; w < W; ++w) {
+      mw[w] = sm.m[w][hh];
+      M = fmaxf(M, mw[w]);
+    }
+    float wsum = 0.f;
+    f32x4 o = {0.f, 0.f, 0.f, 0.f};
     if (M != -INFINITY) {
 #pragma unroll
-      for (int w = 0; w < kWaves; ++w) {
-        const float f = fast_exp2(sm.m[w][hh] - M);
+      for (int w = 0; w < W; ++w) {
+        const float f = fast_exp2(mw[w] - M);
         wsum += f * sm.l[w][hh];
-        o += f * sm.acc[w][hh][d];
+        o += f * *reinterpret_cast<const f32x4*>(&sm.acc[w][hh][d]);
       }
     }
     if (nb == 1) {
-      store_out<D>(p, out_row0 + hh, d, wsum > 0.f ? o / wsum : 0.f);
+      store_out4<D>(p, out_row0 + hh, d, wsum > 0.f ? o / wsum : f32x4{0.f, 0.f, 0.f, 0.f});
     } else if (fuse) {
-      store_device(&p.part_acc[slot * GD + idx], o);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) store_device(&p.part_acc[slot * GD + hh * D + d + e], o[e]);
       if (d == 0) {
         store_device(&p.part_ml[(slot * p.G + hh) * 2 + 0], M);
         store_device(&p.part_ml[(slot * p.G + hh) * 2 + 1], wsum);
       }
     } else {
-      p.part_acc[slot * GD + idx] = o;
+      *reinterpret_cast<f32x4*>(&p.part_acc[slot * GD + hh * D + d]) = o;
       if (d == 0) {
         p.part_ml[(slot * p.G + hh) * 2 + 0] = M;
         p.part_ml[(slot * p.G + hh) * 2 + 1] = wsum;
@@ -514,24 +536,24 @@ __global__ __launch_bounds__(kThreads) void attention_kernel(AttnParams p) {
   {
     const int n_acc = nb * GD;
     float* src = p.part_acc + unit * p.max_parts * GD;
-    for (int j0 = threadIdx.x; j0 < n_acc; j0 += kThreads * 8) {
+    for (int j0 = threadIdx.x; j0 < n_acc; j0 += NT * 8) {
       float v[8];
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
-        const int jj = j0 + u * kThreads;
+        const int jj = j0 + u * NT;
         v[u] = jj < n_acc ? load_device(src + jj) : 0.f;
       }
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
-        const int jj = j0 + u * kThreads;
+        const int jj = j0 + u * NT;
         if (jj < n_acc) sm.stage[jj] = v[u];
       }
     }
     float* src_ml = p.part_ml + unit * p.max_parts * p.G * 2;
-    for (int jj = threadIdx.x; jj < nb * p.G * 2; jj += kThreads) sm.stage_ml[jj] = load_device(src_ml + jj);
+    for (int jj = threadIdx.x; jj < nb * p.G * 2; jj += NT) sm.stage_ml[jj] = load_device(src_ml + jj);
   }
   __syncthreads();
-  for (int idx = threadIdx.x; idx < GD; idx += kThreads) {
+  for (int idx = threadIdx.x; idx < GD; idx += NT) {
     const int hh = idx / D;
     float M = -INFINITY;
     for (int s2 = 0; s2 < nb; ++s2) M = fmaxf(M, sm.stage_ml[(s2 * p.G + hh) * 2]);
@@ -601,91 +623,134 @@ __global__ __launch_bounds__(kThreads) void plan_kernel(AttnParams p, RunItem* i
 
 // ---------------------------------------------------------------------------
 // Log-sum-exp merge of the partials of units cut into several runs (and zero
-// output for empty sequences): one workgroup of four waves per (sequence,
-// query head).  Wave w reads
-// partials w, w+4, ... eight at a time (max, denominator and channels in one
-// round trip) with a running merge, then the waves merge through LDS.
+// output for empty sequences).  A (sequence, query head) row is merged by
+// p.merge_waves waves (1 or 4).  Inside a wave, lane (sub, c) reads channels
+// 4c..4c+3 of partials sub, sub + SP, ... (SP = 256 / D partials side by side),
+// 16 partials per wave per round trip; the first round is issued before the
+// run count arrives (slots past it are ignored).  Sub-streams are merged with
+// shuffles, waves through LDS, always in the same order (deterministic).
 // ---------------------------------------------------------------------------
 template <int D>
 __global__ __launch_bounds__(kThreads) void combine_kernel(AttnParams p) {
-  constexpr int C = D / 64;  // channels per lane
+  constexpr int CL = D / 4;   // lanes covering one partial (a float4 each)
+  constexpr int SP = 64 / CL;  // partials a wave reads side by side
+  constexpr int U = 16 / SP;   // partials per lane per round trip
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
-  const size_t row = blockIdx.x;  // b * h + i
-  const int b = static_cast<int>(row / p.h);
-  const int i = static_cast<int>(row - static_cast<size_t>(b) * p.h);
+  const int wpr = p.merge_waves;  // waves per row: 1 or kWaves
+  const int rows_per_block = kWaves / wpr;
+  const int wr = wave % wpr;      // wave index inside its row
+  const size_t row = static_cast<size_t>(blockIdx.x) * rows_per_block + wave / wpr;
+  const bool row_ok = row < static_cast<size_t>(p.B) * p.h;
+  const size_t rrow = row_ok ? row : 0;
+  const int b = static_cast<int>(rrow / p.h);
+  const int i = static_cast<int>(rrow - static_cast<size_t>(b) * p.h);
   const int r = i / p.G;
   const int hh = i - r * p.G;
-  const int ng = p.n_groups;
-  const int ns = p.runs[b];  // runs of each unit of sequence b
-  if (ns == 0) {             // nothing to attend: zero output
-    for (int d = threadIdx.x; d < D; d += kThreads) store_out<D>(p, row, d, 0.f);
-    return;
-  }
-  if (ns == 1) return;  // finished in place by its only run
-  if (p.fused && ns * p.G * D <= kStageFloats && ns * p.G * 2 <= kStageMl) return;  // merged in place
-  const size_t base = (static_cast<size_t>(b) * ng + r) * p.max_parts;
+  const int sub = lane / CL;
+  const int c = (lane - sub * CL) * 4;
   const int GD = p.G * D;
+  const size_t base = (static_cast<size_t>(b) * p.n_groups + r) * p.max_parts;
+  const int stride = wpr * SP;  // partial index step between a lane's consecutive reads
+  const int first = wr * SP + sub;
 
-  float run_m = -INFINITY, run_den = 0.f, run_o[C];
+  float m[U], w[U];
+  f32x4 a[U];
+  auto load_round = [&](int s0, int ns) {
 #pragma unroll
-  for (int k = 0; k < C; ++k) run_o[k] = 0.f;
-  for (int s0 = wave; s0 < ns; s0 += kWaves * 8) {
-    float m[8], w[8], a[8][C];
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const int s = s0 + u * kWaves;
+    for (int u = 0; u < U; ++u) {
+      const int s = s0 + first + u * stride;
       const bool ok = s < ns;
       const size_t slot = base + (ok ? s : 0);
-      m[u] = ok ? p.part_ml[(slot * p.G + hh) * 2] : -INFINITY;
-      w[u] = ok ? p.part_ml[(slot * p.G + hh) * 2 + 1] : 0.f;
+      const float mm = p.part_ml[(slot * p.G + hh) * 2];
+      const float ww = p.part_ml[(slot * p.G + hh) * 2 + 1];
+      const f32x4 aa = *reinterpret_cast<const f32x4*>(&p.part_acc[slot * GD + hh * D + c]);
+      m[u] = ok ? mm : -INFINITY;
+      w[u] = ok ? ww : 0.f;
+      a[u] = ok ? aa : f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+  };
+  // First round before the run count is known: every slot below max_parts
+  // is inside the workspace.
+  load_round(0, p.max_parts);
+  const int ns = row_ok ? p.runs[b] : 0;  // runs of each unit of sequence b
+  const bool merged_in_place =
+      ns == 1 || (p.fused && ns * p.G * D <= kStageFloats && ns * p.G * 2 <= kStageMl);
+  if (!row_ok || merged_in_place) return;  // uniform per row: all its waves leave
+  if (ns == 0) {                           // nothing to attend: zero output
+    if (wr == 0 && sub == 0) store_out4<D>(p, rrow, c, f32x4{0.f, 0.f, 0.f, 0.f});
+    return;
+  }
+
+  float run_m = -INFINITY, run_den = 0.f;
+  f32x4 run_o = {0.f, 0.f, 0.f, 0.f};
+  for (int s0 = 0;;) {
 #pragma unroll
-      for (int k = 0; k < C; ++k)
-        a[u][k] = ok ? p.part_acc[slot * GD + hh * D + lane + 64 * k] : 0.f;
+    for (int u = 0; u < U; ++u) {  // drop speculative slots at or past ns
+      const bool ok = s0 + first + u * stride < ns;
+      m[u] = ok ? m[u] : -INFINITY;
+      w[u] = ok ? w[u] : 0.f;
+      a[u] = ok ? a[u] : f32x4{0.f, 0.f, 0.f, 0.f};
     }
     float bm = run_m;
 #pragma unroll
-    for (int u = 0; u < 8; ++u) bm = fmaxf(bm, m[u]);
-    if (bm == -INFINITY) continue;
-    const float sc = fast_exp2(run_m - bm);
-    run_den *= sc;
+    for (int u = 0; u < U; ++u) bm = fmaxf(bm, m[u]);
+    if (bm != -INFINITY) {
+      const float sc = fast_exp2(run_m - bm);  // 0 while nothing is accumulated
+      run_den *= sc;
+      run_o *= sc;
 #pragma unroll
-    for (int k = 0; k < C; ++k) run_o[k] *= sc;
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const float f = fast_exp2(m[u] - bm);
-      run_den += f * w[u];
-#pragma unroll
-      for (int k = 0; k < C; ++k) run_o[k] += f * a[u][k];
+      for (int u = 0; u < U; ++u) {
+        const float f = fast_exp2(m[u] - bm);
+        run_den += f * w[u];
+        run_o += f * a[u];
+      }
+      run_m = bm;
     }
-    run_m = bm;
+    s0 += U * stride;
+    if (s0 >= ns) break;
+    load_round(s0, ns);
   }
-  __shared__ float sm_m[kWaves], sm_den[kWaves], sm_o[kWaves][D];
+
+  // Merge the SP sub-streams of the wave (lanes CL apart).
+  float M = run_m;
+#pragma unroll
+  for (int off = CL; off < 64; off <<= 1) M = fmaxf(M, __shfl_xor(M, off));
+  const float f = run_m == -INFINITY ? 0.f : fast_exp2(run_m - M);
+  float den = f * run_den;
+  f32x4 o = f * run_o;
+#pragma unroll
+  for (int off = CL; off < 64; off <<= 1) {
+    den += __shfl_xor(den, off);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) o[e] += __shfl_xor(o[e], off);
+  }
+  if (wpr == 1) {
+    if (sub == 0) store_out4<D>(p, rrow, c, den > 0.f ? o / den : f32x4{0.f, 0.f, 0.f, 0.f});
+    return;
+  }
+  // Several waves per row (one row per workgroup): merge through LDS.
+  __shared__ float sm_m[kWaves], sm_den[kWaves];
+  __shared__ f32x4 sm_o[kWaves][CL];
   if (lane == 0) {
-    sm_m[wave] = run_m;
-    sm_den[wave] = run_den;
+    sm_m[wave] = M;
+    sm_den[wave] = den;
   }
-#pragma unroll
-  for (int k = 0; k < C; ++k) sm_o[wave][lane + 64 * k] = run_o[k];
+  if (sub == 0) sm_o[wave][lane] = o;
   __syncthreads();
-  if (wave == 0) {
-    float M = -INFINITY;
+  if (wave == 0 && sub == 0) {
+    float MM = -INFINITY;
 #pragma unroll
-    for (int w = 0; w < kWaves; ++w) M = fmaxf(M, sm_m[w]);
-    float f[kWaves], den = 0.f;
+    for (int v = 0; v < kWaves; ++v) MM = fmaxf(MM, sm_m[v]);
+    float dd = 0.f;
+    f32x4 oo = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int w = 0; w < kWaves; ++w) {
-      f[w] = M == -INFINITY ? 0.f : fast_exp2(sm_m[w] - M);
-      den += f[w] * sm_den[w];
+    for (int v = 0; v < kWaves; ++v) {
+      const float fv = sm_m[v] == -INFINITY ? 0.f : fast_exp2(sm_m[v] - MM);
+      dd += fv * sm_den[v];
+      oo += fv * sm_o[v][lane];
     }
-#pragma unroll
-    for (int k = 0; k < C; ++k) {
-      const int d = lane + 64 * k;
-      float v = 0.f;
-#pragma unroll
-      for (int w = 0; w < kWaves; ++w) v += f[w] * sm_o[w][d];
-      store_out<D>(p, row, d, den > 0.f ? v / den : 0.f);
-    }
+    store_out4<D>(p, rrow, c, dd > 0.f ? oo / dd : f32x4{0.f, 0.f, 0.f, 0.f});
   }
 }
 
@@ -708,25 +773,38 @@ hipError_t launch_append(const AppendParams& p, int head_dim, int owned_count,
   return hipGetLastError();
 }
 
+template <int D, int W>
+static void launch_attention_t(const AttnParams& p, hipStream_t stream, hipEvent_t start,
+                               hipEvent_t stop) {
+  const dim3 grid(p.n_blocks), block(W * 64);
+  auto kernel = attention_kernel<D, W>;
+  if (start)  // timed: events recorded with the dispatch itself
+    hipExtLaunchKernelGGL(kernel, grid, block, 0, stream, start, stop, 0, p);
+  else
+    hipLaunchKernelGGL(kernel, grid, block, 0, stream, p);
+}
+
 hipError_t launch_attention_main(const AttnParams& p, int head_dim, hipStream_t stream,
                                  hipEvent_t start, hipEvent_t stop) {
-  const dim3 grid(p.n_blocks);
-  if (start) {  // timed: events recorded with the dispatch itself
-    if (head_dim == 64)
-      hipExtLaunchKernelGGL(attention_kernel<64>, grid, dim3(kThreads), 0, stream, start, stop, 0, p);
+  const bool wide = p.waves == kWideWaves;
+  if (head_dim == 64) {
+    if (wide)
+      launch_attention_t<64, kWideWaves>(p, stream, start, stop);
     else
-      hipExtLaunchKernelGGL(attention_kernel<128>, grid, dim3(kThreads), 0, stream, start, stop, 0, p);
-  } else if (head_dim == 64) {
-    hipLaunchKernelGGL(attention_kernel<64>, grid, dim3(kThreads), 0, stream, p);
+      launch_attention_t<64, kWaves>(p, stream, start, stop);
   } else {
-    hipLaunchKernelGGL(attention_kernel<128>, grid, dim3(kThreads), 0, stream, p);
+    if (wide)
+      launch_attention_t<128, kWideWaves>(p, stream, start, stop);
+    else
+      launch_attention_t<128, kWaves>(p, stream, start, stop);
   }
   return hipGetLastError();
 }
 
 hipError_t launch_attention_merge(const AttnParams& p, int head_dim, hipStream_t stream) {
   if (p.n_blocks == 1) return hipSuccess;  // every unit is finished in place
-  const dim3 cgrid(p.B * p.h);
+  const int rows_per_block = kWaves / p.merge_waves;
+  const dim3 cgrid((p.B * p.h + rows_per_block - 1) / rows_per_block);
   if (head_dim == 64)
     hipLaunchKernelGGL(combine_kernel<64>, cgrid, dim3(kThreads), 0, stream, p);
   else
@@ -743,6 +821,9 @@ hipError_t launch_plan(const AttnParams& p, hipStream_t stream) {
 int max_batch() { return kMaxBatch; }
 int stage_floats() { return kStageFloats; }
 
+int wide_waves() { return kWideWaves; }
+int default_waves() { return kWaves; }
+
 int resident_workgroups(int head_dim) {
   static std::atomic<int> cached[2] = {{-1}, {-1}};
   std::atomic<int>& slot = cached[head_dim == 64 ? 0 : 1];
@@ -754,8 +835,8 @@ int resident_workgroups(int head_dim) {
     return 0;
   const hipError_t err =
       head_dim == 64
-          ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attention_kernel<64>, kThreads, 0)
-          : hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attention_kernel<128>, kThreads, 0);
+          ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attention_kernel<64, kWaves>, kThreads, 0)
+          : hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attention_kernel<128, kWaves>, kThreads, 0);
   if (err != hipSuccess) return 0;
   v = cus * per_cu;
   slot.store(v, std::memory_order_relaxed);

@@ -127,7 +127,7 @@ int tiles_of(int len) { return (len + kTileTokens - 1) / kTileTokens; }
 // Split-K plan for one layer.  The kernel cuts every (sequence, KV head)
 // unit into runs of R tiles, R chosen on the device from the actual lengths
 // so that all runs fit the launched workgroups.  The host picks that count:
-// the device's resident capacity, capped at 32 per unit (more would only
+// the device's resident capacity, capped at 128 per unit (more would only
 // multiply partials to merge) and at what runs of kMinTiles tiles need, but
 // at least one per unit; a single unit of at most 16 tiles takes one
 // workgroup (no partials at all).
@@ -137,9 +137,10 @@ struct Plan {
   int max_tiles;  // tiles of the longest sequence allowed by max_len
   int min_tiles;  // least tiles per run
   int fused;      // 1: every unit's runs are merged in place (no merge kernel)
+  int waves;      // waves per attention workgroup
 };
 constexpr int kMinTiles = 4;
-constexpr int kMaxRunsPerUnit = 32;
+constexpr int kMaxRunsPerUnit = 128;
 constexpr int kFallbackResident = 768;  // 256 CUs x 3 when no device can be queried
 
 long workgroups_for(long resident, long units, long t_max, int min_tiles) {
@@ -183,7 +184,22 @@ Plan plan(const mlkv_map* map, int layer, int batch, int max_len, int head_dim) 
   }
   long g = workgroups_for(resident, units, t_max, pl.min_tiles);
   if (units == 1 && t_max <= 4 * kMinTiles) g = 1;
+  pl.waves = mlkv::default_waves();
+  // MLKV_WIDE=1: each unit becomes one run on a wider workgroup, so there
+  // are no partials and no merge kernel.  On MI355X this measured no faster
+  // than balanced runs plus the merge for a 128-sequence ragged batch (the
+  // longest sequence bounds it), so it is not the default.
+  bool wide = false;
+  if (const char* env = std::getenv("MLKV_WIDE")) wide = std::atoi(env) != 0;
+  if (wide) {
+    g = units;
+    pl.waves = mlkv::wide_waves();
+  }
   pl.n_blocks = static_cast<int>(g);
+  if (g == units) {  // one workgroup per unit: runs cover whole units, nothing to merge
+    pl.min_tiles = pl.max_tiles;
+    pl.fused = 0;
+  }
   pl.max_parts = (pl.max_tiles + pl.min_tiles - 1) / pl.min_tiles + 1;
   return pl;
 }
@@ -282,6 +298,9 @@ mlkv_status attention_impl(int layer, const void* q, const mlkv_cache* cache, co
   p.min_tiles = pl.min_tiles;
   p.max_parts = pl.max_parts;
   p.fused = pl.fused;
+  p.waves = pl.waves;
+  // One wave merges a row when units average at most 16 runs, else four.
+  p.merge_waves = pl.n_blocks <= 16L * B * map->kv_count[layer] ? 1 : 4;
   p.D = D;
   p.len_offset = len_offset;
   p.out_bf16 = dt == MLKV_OUT_BF16 ? 1 : 0;
@@ -294,7 +313,8 @@ mlkv_status attention_impl(int layer, const void* q, const mlkv_cache* cache, co
   err = mlkv::launch_attention_main(p, D, stream, timed ? prof.start[prof.used] : nullptr,
                                                timed ? prof.stop[prof.used] : nullptr);
   if (err == hipSuccess && timed) ++prof.used;
-  if (err == hipSuccess && !pl.fused) err = mlkv::launch_attention_merge(p, D, stream);
+  const bool single_runs = pl.n_blocks == B * map->kv_count[layer];
+  if (err == hipSuccess && !pl.fused && !single_runs) err = mlkv::launch_attention_merge(p, D, stream);
   if (err != hipSuccess) return fail(MLKV_ERR_HIP, "attention launch: %s", hipGetErrorString(err));
   return MLKV_OK;
 }
@@ -442,8 +462,12 @@ size_t mlkv_workspace_bytes(const mlkv_map* map, int batch, int capacity, int he
   if (!map || batch <= 0 || capacity <= 0 || (head_dim != 64 && head_dim != 128)) return 0;
   size_t best = 0;
   for (int n = 0; n < map->l; ++n) {
-    Plan pl = plan(map, n, batch, capacity, head_dim);
-    // Size for the most workgroups any device could get (32 per unit).
+    // The largest plan any device or launch layout can pick: the most
+    // workgroups (kMaxRunsPerUnit per unit) and the shortest runs (kMinTiles).
+    Plan pl{};
+    pl.max_tiles = tiles_of(capacity);
+    pl.min_tiles = kMinTiles;
+    pl.max_parts = (pl.max_tiles + kMinTiles - 1) / kMinTiles + 1;
     pl.n_blocks = kMaxRunsPerUnit * batch * map->kv_count[n];
     pl.n_blocks = pl.n_blocks > 2 ? pl.n_blocks : 2;
     const size_t need = workspace_need(batch, map->h, head_dim, pl);
@@ -592,7 +616,10 @@ mlkv_status mlkv_profile_enable(int max_launches) {
   prof.start.assign(max_launches, nullptr);
   prof.stop.assign(max_launches, nullptr);
   for (int i = 0; i < max_launches; ++i) {
-    if (hipEventCreate(&prof.start[i]) != hipSuccess || hipEventCreate(&prof.stop[i]) != hipSuccess) {
+    // Timing-only events: no system-scope fence (no cache writeback or
+    // invalidate around the timed kernel, which would slow it and the next).
+    if (hipEventCreateWithFlags(&prof.start[i], hipEventDisableSystemFence) != hipSuccess ||
+        hipEventCreateWithFlags(&prof.stop[i], hipEventDisableSystemFence) != hipSuccess) {
       mlkv_profile_disable();
       return fail(MLKV_ERR_HIP, "hipEventCreate failed");
     }

@@ -132,12 +132,18 @@ def test_entry_points_reject_bad_arguments():
     assert names[L.mlkv_decode_attention(0, 0x30000, ctypes.byref(c2), mq.handle, 0x40000, 0x50000, 0, 0, 0x60000, 1 << 30, None)] == "MLKV_ERR_UNSUPPORTED"
 
 
-def test_workspace_covers_every_plan():
-    """mlkv_workspace_bytes covers the documented layout of every plan:
-    counters [B*h], runs [B], run items [workgroups], partials."""
+@pytest.mark.parametrize("env", [{}, {"MLKV_WIDE": "1"}, {"MLKV_WIDE": "0"},
+                                 {"MLKV_COMBINE": "fused"}, {"MLKV_WORKGROUPS": "5"},
+                                 {"MLKV_WORKGROUPS": "100000", "MLKV_WIDE": "0"}])
+def test_workspace_covers_every_plan(env, monkeypatch):
+    """mlkv_workspace_bytes covers the documented layout of every plan, under
+    every launch-layout override: counters [B*h], runs [B], run items
+    [workgroups], partials."""
+    for k, v in env.items():
+        monkeypatch.setenv(k, v)
     mp = mlkv.Map.uniform(12, 12, 4, 1)
     al = lambda x: (x + 255) // 256 * 256  # noqa: E731
-    for B, S in [(1, 160), (8, 32832), (128, 2112), (32, 2112)]:
+    for B, S in [(1, 160), (8, 32832), (128, 2112), (32, 2112), (300, 2112)]:
         ws = mp.workspace_bytes(B, S, 64)
         for max_len in [x for x in (1, 31, 33, 129, 511, 513, S // 2, S) if x <= S]:
             wg, parts = mp.plan(0, B, S, 64, max_len)

@@ -4,6 +4,7 @@ Cache writes are compared bit for bit; attention outputs within the
 tolerances stated in gpu_util.  Every case prints its name before touching the
 GPU so that a failure names it.
 """
+import contextlib
 import os
 
 import numpy as np
@@ -30,6 +31,25 @@ def _gpu():
 
 def small(name, **kw):
     return synth.get_workload(name).scaled(**kw)
+
+
+@contextlib.contextmanager
+def plan_env(workgroups="", merge="", wide=""):
+    """Launch-plan overrides read by the library on every call:
+    MLKV_WORKGROUPS (resident workgroups assumed), MLKV_COMBINE=fused (merge
+    runs inside the attention kernel), MLKV_WIDE=0/1 (one run per unit on a
+    wide workgroup: off / forced)."""
+    names = {"MLKV_WORKGROUPS": workgroups, "MLKV_COMBINE": merge, "MLKV_WIDE": wide}
+    for k, v in names.items():
+        if v:
+            os.environ[k] = v
+        else:
+            os.environ.pop(k, None)
+    try:
+        yield
+    finally:
+        for k in names:
+            os.environ.pop(k, None)
 
 
 # ------------------------------------------------------------------ append --
@@ -100,22 +120,18 @@ def test_length_sweep_across_tile_boundaries(D, m, g):
     dw = DeviceWorkload(w)
     lens = np.array(LEN_SWEEP, dtype=np.int32)
     lens_d = torch.from_numpy(lens).cuda()
-    for wg, comb in (("", ""), ("3", ""), ("40", ""), ("", "fused"), ("40", "fused")):
-        os.environ["MLKV_WORKGROUPS"] = wg
-        os.environ["MLKV_COMBINE"] = comb
-        try:
+    for wg, comb, wide in (("", "", ""), ("3", "", ""), ("40", "", ""), ("", "fused", ""),
+                           ("40", "fused", ""), ("", "", "1"), ("", "", "0")):
+        with plan_env(wg, comb, wide):
             for n in (0, w.l - 1):
                 say(f"length sweep D={D} m={m} g={g} layer={n} workgroups={wg or 'auto'} "
-                    f"merge={comb or 'kernel'}")
+                    f"merge={comb or 'kernel'} wide={wide or 'auto'}")
                 out = torch.empty((w.B, w.h, w.D), dtype=torch.float32, device="cuda")
                 mlkv.decode_attention(n, dw.q[n], dw.cache, dw.map, lens_d, out, ws=dw.ws)
                 torch.cuda.synchronize()
                 ref = oracle.decode_attention(n, dw.host["q"][n], dw.host["k_cache"],
                                               dw.host["v_cache"], dw.kv_of, lens)
-                check_close(out.cpu().numpy(), ref, f"sweep D{D} g{g} L{n} wg{wg} {comb}")
-        finally:
-            os.environ.pop("MLKV_WORKGROUPS", None)
-            os.environ.pop("MLKV_COMBINE", None)
+                check_close(out.cpu().numpy(), ref, f"sweep D{D} g{g} L{n} wg{wg} {comb} {wide}")
 
 
 def test_split_count_invariance_and_determinism():
@@ -125,22 +141,18 @@ def test_split_count_invariance_and_determinism():
     dw = DeviceWorkload(w)
     lens_d = torch.from_numpy(dw.host["ctx"]).cuda()
     outs = {}
-    for wg, comb in (("1", ""), ("7", ""), ("64", ""), ("300", ""), ("", ""), ("", "fused"),
-                     ("300", "fused")):
-        os.environ["MLKV_WORKGROUPS"] = wg
-        os.environ["MLKV_COMBINE"] = comb
-        try:
-            say(f"workgroup invariance workgroups={wg or 'auto'} merge={comb or 'kernel'}")
+    for wg, comb, wide in (("1", "", ""), ("7", "", ""), ("64", "", ""), ("300", "", ""),
+                           ("", "", ""), ("", "fused", ""), ("300", "fused", ""), ("", "", "1")):
+        with plan_env(wg, comb, wide):
+            say(f"workgroup invariance workgroups={wg or 'auto'} merge={comb or 'kernel'} "
+                f"wide={wide or 'auto'}")
             o = torch.empty((w.B, w.h, w.D), dtype=torch.float32, device="cuda")
             mlkv.decode_attention(2, dw.q[2], dw.cache, dw.map, lens_d, o, ws=dw.ws)
             o2 = torch.empty_like(o)
             mlkv.decode_attention(2, dw.q[2], dw.cache, dw.map, lens_d, o2, ws=dw.ws)
             torch.cuda.synchronize()
             assert torch.equal(o, o2), "run-to-run results differ"
-            outs[wg + comb] = o.cpu().numpy().astype(np.float64)
-        finally:
-            os.environ.pop("MLKV_WORKGROUPS", None)
-            os.environ.pop("MLKV_COMBINE", None)
+            outs[wg + comb + wide] = o.cpu().numpy().astype(np.float64)
     ref = oracle.decode_attention(2, dw.host["q"][2], dw.host["k_cache"], dw.host["v_cache"],
                                   dw.kv_of, dw.host["ctx"])
     for k, o in outs.items():
@@ -180,16 +192,13 @@ def test_needle_token(pos_kind):
     kc = dw.host["k_cache"]
     kc[0, b, pos] = synth.f32_to_bf16(synth.bf16_to_f32(q) * 4.0)
     dw.cache.load_rows(kc, dw.host["v_cache"])
-    os.environ["MLKV_WORKGROUPS"] = "5"
-    try:
+    with plan_env(workgroups="5"):
         say(f"needle at {pos} ({pos_kind})")
         out = torch.empty((w.B, w.h, w.D), dtype=torch.float32, device="cuda")
         lens = np.array([L, L], np.int32)
         mlkv.decode_attention(0, dw.q[0], dw.cache, dw.map, torch.from_numpy(lens).cuda(), out,
                               ws=dw.ws)
         torch.cuda.synchronize()
-    finally:
-        os.environ.pop("MLKV_WORKGROUPS", None)
     ref = oracle.decode_attention(0, dw.host["q"][0], kc, dw.host["v_cache"], dw.kv_of, lens)
     _, alpha = oracle.attend_one(q, kc[0, b, :L], dw.host["v_cache"][0, b, :L])
     assert alpha[pos] > 0.99
@@ -248,14 +257,17 @@ def test_step_mlkv2_empty_context_outputs_new_value_exactly():
                                       f64(dw.host["v_new"][b, n // 6]).astype(np.float32))
 
 
-@pytest.mark.parametrize("wname", ["mlkv2_b1", "mlkv4_b128_ragged", "mlkv4_b8_long"])
-def test_full_size_step_matches_oracle(wname):
-    """Full-size workloads in the launch configuration the benchmark times."""
+@pytest.mark.parametrize("wname,wide", [("mlkv2_b1", ""), ("mlkv4_b128_ragged", ""),
+                                        ("mlkv4_b128_ragged", "1"), ("mlkv4_b8_long", "")])
+def test_full_size_step_matches_oracle(wname, wide):
+    """Full-size workloads in the launch configuration the benchmark times
+    (and the ragged batch also with one wide workgroup per sequence)."""
     w = synth.get_workload(wname)
-    say(f"full step {wname}: uploading")
+    say(f"full step {wname} wide={wide or 'auto'}: uploading")
     dw = DeviceWorkload(w)
     say(f"full step {wname}: running")
-    out = _run_step(dw).cpu().numpy()
+    with plan_env(wide=wide):
+        out = _run_step(dw).cpu().numpy()
     k_gpu, v_gpu = dw.read_cache()
     say(f"full step {wname}: oracle")
     ref, k_ref, v_ref = _oracle_step(dw)
@@ -281,8 +293,7 @@ def test_full_size_step_with_in_place_merge():
     """The ragged 128-sequence step with runs merged inside the attention kernel
     (MLKV_COMBINE=fused) gives the same cache and outputs as the oracle."""
     w = synth.get_workload("mlkv4_b128_ragged")
-    os.environ["MLKV_COMBINE"] = "fused"
-    try:
+    with plan_env(merge="fused"):
         say("full step in-place merge: uploading")
         dw = DeviceWorkload(w)
         say("full step in-place merge: running (twice: counters must reset)")
@@ -290,8 +301,6 @@ def test_full_size_step_with_in_place_merge():
         dw2 = DeviceWorkload(w)  # fresh cache, same workspace contract
         dw2.ws = dw.ws
         out = _run_step(dw2).cpu().numpy()
-    finally:
-        os.environ.pop("MLKV_COMBINE", None)
     k_gpu, v_gpu = dw2.read_cache()
     ref, k_ref, v_ref = _oracle_step(dw2)
     assert np.array_equal(k_gpu, k_ref) and np.array_equal(v_gpu, v_ref), "cache differs"
