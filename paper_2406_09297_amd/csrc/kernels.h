@@ -22,7 +22,8 @@ struct AttnParams {
   const int32_t* lens;       // [B]; attended length = lens[b] + len_offset
   void* out;                 // [B][h][D] fp32 or bf16
   int* runs;                 // [B] runs per unit of sequence b (written by workgroup 0)
-  void* plan;                // [n_blocks] run items from plan_kernel, or null: schedule in-kernel
+  void* plan;                // [n_blocks] run items to follow, or null: schedule in-kernel
+  void* plan_out;            // with plan null: where each workgroup records its run item (or null)
   int* counters;             // [B*n_groups] finished runs per unit (zero between calls)
   float* part_acc;           // [B*n_groups][max_parts][G][D]  unnormalised partial outputs
   float* part_ml;            // [B*n_groups][max_parts][G][2]  (max in log2 units, denominator)
@@ -37,6 +38,12 @@ struct AttnParams {
   int merge_waves;           // waves merging one (sequence, head) row: 1 or 4
   int waves;                 // waves per attention workgroup: 4, or wide_waves() for single runs
   float scale_log2;          // log2(e) / sqrt(D)
+  // Fused append (owning layer of a decode step), k_new null when none: row
+  // of KV head kv for sequence b at k_new + b*new_stride + kv*D; heads
+  // [own_begin, own_begin + own_count) are appended at slot lens[b] + len_offset - 1.
+  const uint16_t* k_new;
+  const uint16_t* v_new;
+  int new_stride, own_begin, own_count;
 };
 
 hipError_t launch_append(const AppendParams& p, int head_dim, int owned_count,
@@ -47,8 +54,6 @@ hipError_t launch_append(const AppendParams& p, int head_dim, int owned_count,
 hipError_t launch_attention_main(const AttnParams& p, int head_dim, hipStream_t stream,
                                  hipEvent_t start, hipEvent_t stop);
 hipError_t launch_attention_merge(const AttnParams& p, int head_dim, hipStream_t stream);
-// One workgroup computing the run schedule into p.plan (and p.runs).
-hipError_t launch_plan(const AttnParams& p, hipStream_t stream);
 int max_batch();
 int stage_floats();  // partial-output floats one workgroup can merge in place
 int resident_workgroups(int head_dim); // attention workgroups the device holds at once (0: none)

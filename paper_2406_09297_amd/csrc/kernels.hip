@@ -156,10 +156,33 @@ struct WaveState {
 // skip rescaling the accumulators.  Any reference gives the same softmax.
 constexpr float kLazyRescale = 8.f;
 
-template <int D>
+// LAST: the wave's last tile of its run, the only one that can hold the
+// ragged end of a sequence or the newest token.  pos_new >= 0: position of
+// the newest token, whose key and value are taken from new_row (LDS: key
+// then value, D each) instead of the loaded tile.
+template <int D, bool LAST>
 __device__ __forceinline__ void process_tile(WaveState<D>& st, Tile<D>& t, const bf16x8* qf,
-                                             int t0, int L, int grp, float scale_log2) {
+                                             int t0, int L, int col, int grp, float scale_log2,
+                                             int pos_new, const uint16_t* new_row) {
   constexpr int KK = Tile<D>::KK, DB = Tile<D>::DB;
+  if (LAST && pos_new >= t0 && pos_new < t0 + kTile) {
+#pragma unroll
+    for (int sb = 0; sb < 2; ++sb) {
+      if (t0 + (col >> 2) * 8 + sb * 4 + (col & 3) == pos_new) {
+#pragma unroll
+        for (int kk = 0; kk < KK; ++kk)
+          t.k[sb][kk] = *reinterpret_cast<const u16x8*>(new_row + grp * 8 + kk * 32);
+      }
+    }
+    const int e_new = pos_new - t0 - grp * 8;  // in [0, 8) for the lanes holding it
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      const uint16_t vn = new_row[D + db * 16 + col];
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        if (e == e_new) t.v[db][e] = vn;
+    }
+  }
   f32x4 s[2];
 #pragma unroll
   for (int sb = 0; sb < 2; ++sb) {
@@ -173,7 +196,7 @@ __device__ __forceinline__ void process_tile(WaveState<D>& st, Tile<D>& t, const
 #pragma unroll
     for (int i = 0; i < 4; ++i) x[sb * 4 + i] = s[sb][i];
 
-  if (t0 + kTile > L) {  // ragged tail: positions >= L take no weight and no value
+  if (LAST && t0 + kTile > L) {  // ragged tail: positions >= L take no weight and no value
     const int first = t0 + grp * 8;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
@@ -274,14 +297,17 @@ struct alignas(16) AttnShared {
     float stage[kStageFloats];
   };
   float stage_ml[kStageMl];
+  alignas(16) uint16_t new_row[2 * D];  // newest token's key and value (fused append)
   int last;
 };
 
 // A run of the plan: sequence b, KV group r, run j of nb of that unit,
 // attended length L, tiles [k0, k1).  b < 0 marks a workgroup with no run.
+// z >= 0: sequence z attends to nothing and this workgroup writes its zero
+// output (a launch has at least as many workgroups as sequences).
 struct RunItem {
   int b, r, j, nb;
-  int L, k0, k1, pad;
+  int L, k0, k1, z;
 };
 
 // ceil(x / y) for 0 <= x < 2^21, 1 <= y < 2^21 without the integer-division
@@ -372,10 +398,14 @@ __device__ void schedule_wave0(const AttnParams& p, SchedShared& sm, int g) {
   }
 }
 
+// Register budget: at least 3 waves per SIMD for D = 64 and 2 for D = 128
+// with four-wave workgroups (12 / 8 waves per compute unit in flight).
 template <int D, int W>
-__global__ __launch_bounds__(W * 64) void attention_kernel(AttnParams p) {
+__global__ __launch_bounds__(W * 64) __attribute__((amdgpu_waves_per_eu(D == 64 ? 3 : 2)))
+void attention_kernel(AttnParams p) {
   constexpr int KK = Tile<D>::KK, DB = Tile<D>::DB;
   constexpr int NT = W * 64;  // threads
+  constexpr int D4 = D / 4;    // four-channel groups of a head
   __shared__ AttnShared<D, W> sm;
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
@@ -384,8 +414,11 @@ __global__ __launch_bounds__(W * 64) void attention_kernel(AttnParams p) {
   const int g = blockIdx.x;
 
   int b, r, j, nb, L, k0, k1;
-  if (p.plan) {  // the step's plan was computed once by plan_kernel
+  if (p.plan) {  // the step's plan, written by the step's first attention launch
     const RunItem item = reinterpret_cast<const RunItem*>(p.plan)[g];
+    if (item.z >= 0)
+      for (int i = threadIdx.x; i < p.h * D4; i += NT)
+        store_out4<D>(p, static_cast<size_t>(item.z) * p.h, i * 4, f32x4{0.f, 0.f, 0.f, 0.f});
     if (item.b < 0) return;
     b = item.b;
     r = item.r;
@@ -404,10 +437,15 @@ __global__ __launch_bounds__(W * 64) void attention_kernel(AttnParams p) {
         p.runs[bb] = div_up(tiles_of(sm.sc.len[bb]), R);
     for (int bb = g; bb < p.B; bb += p.n_blocks) {  // sequences with nothing to attend
       if (sm.sc.len[bb] > 0) continue;
-      for (int i = threadIdx.x; i < p.h * D; i += NT)
-        store_out<D>(p, static_cast<size_t>(bb) * p.h, i, 0.f);
+      for (int i = threadIdx.x; i < p.h * D4; i += NT)
+        store_out4<D>(p, static_cast<size_t>(bb) * p.h, i * 4, f32x4{0.f, 0.f, 0.f, 0.f});
     }
-    if (g >= n_runs) return;
+    RunItem* const plan_out = reinterpret_cast<RunItem*>(p.plan_out);
+    const int z = g < p.B && sm.sc.len[g] == 0 ? g : -1;
+    if (g >= n_runs) {
+      if (plan_out && threadIdx.x == 0) plan_out[g] = RunItem{-1, 0, 0, 0, 0, 0, 0, z};
+      return;
+    }
     // Run g: sequence b, KV group r, run j of that unit.
     b = sm.sc.sched[2];
     L = sm.sc.len[b];
@@ -418,6 +456,7 @@ __global__ __launch_bounds__(W * 64) void attention_kernel(AttnParams p) {
     j = rem - r * nb;
     k0 = j * R;
     k1 = k0 + R < tiles_b ? k0 + R : tiles_b;
+    if (plan_out && threadIdx.x == 0) plan_out[g] = RunItem{b, r, j, nb, L, k0, k1, z};
   }
 
   const int kv = p.kv_begin + r;
@@ -445,24 +484,58 @@ __global__ __launch_bounds__(W * 64) void attention_kernel(AttnParams p) {
 #pragma unroll
   for (int db = 0; db < DB; ++db) st.acc[db] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // The loads of tile it+W are issued before tile it is consumed; the
-  // prefetch is never skipped (past the last tile it re-reads the current,
-  // cache-resident tile) so that the wait before each tile covers only that
-  // tile's own loads.
-  if (it < k1) {
-    load_tile(ta, kbase, vbase, it * kTile, col, grp);
-    for (;;) {
-      int nxt = it + W;
-      load_tile(tb, kbase, vbase, (nxt < k1 ? nxt : it) * kTile, col, grp);
-      process_tile(st, ta, qf, it * kTile, L, grp, p.scale_log2);
-      it = nxt;
-      if (it >= k1) break;
-      nxt = it + W;
-      load_tile(ta, kbase, vbase, (nxt < k1 ? nxt : it) * kTile, col, grp);
-      process_tile(st, tb, qf, it * kTile, L, grp, p.scale_log2);
-      it = nxt;
-      if (it >= k1) break;
+  const bool has_tiles = it < k1;
+  if (has_tiles) load_tile(ta, kbase, vbase, it * kTile, col, grp);
+
+  // Fused append of the owning layer (Section 2.4): the last run of each
+  // owned unit writes the newest token's K/V row into slot lens[b] +
+  // len_offset - 1 and, when that slot is the last attended position, takes
+  // the row from LDS (this kernel's tile loads may not see the write).
+  int pos_new = -1;
+  if (p.k_new && j == nb - 1 && kv >= p.own_begin && kv < p.own_begin + p.own_count) {
+    const int pos = p.lens[b] + p.len_offset - 1;
+    if (pos >= 0 && pos < p.S) {
+      if (threadIdx.x < D / 8) {
+        const int d0 = threadIdx.x * 8;
+        const size_t src = static_cast<size_t>(b) * p.new_stride + static_cast<size_t>(kv) * D + d0;
+        const u16x8 nk = load16(p.k_new + src);
+        const u16x8 nv = load16(p.v_new + src);
+        uint16_t* kc = const_cast<uint16_t*>(kbase);  // the caller's cache, written here only
+        uint16_t* vc = const_cast<uint16_t*>(vbase);
+        *reinterpret_cast<u16x8*>(kc + static_cast<size_t>(pos) * D + d0) = nk;
+        uint16_t* vdst = vc + static_cast<size_t>(pos & ~(kTile - 1)) * D + (pos & (kTile - 1));
+#pragma unroll
+        for (int e = 0; e < 8; ++e) vdst[(d0 + e) * kTile] = nv[e];
+        *reinterpret_cast<u16x8*>(&sm.new_row[d0]) = nk;
+        *reinterpret_cast<u16x8*>(&sm.new_row[D + d0]) = nv;
+      }
+      if (pos == L - 1) {
+        pos_new = pos;
+        __syncthreads();  // the staged row is visible to every wave
+      }
     }
+  }
+
+  // The loads of tile it+W are issued before tile it is consumed (two
+  // register buffers); the wave's last tile is processed after the loop,
+  // with the ragged-end mask and the newest token.
+  if (has_tiles) {
+    for (;;) {
+      const int nxt = it + W;
+      if (nxt >= k1) break;  // ta holds the last tile
+      load_tile(tb, kbase, vbase, nxt * kTile, col, grp);
+      process_tile<D, false>(st, ta, qf, it * kTile, L, col, grp, p.scale_log2, -1, nullptr);
+      it = nxt;
+      const int nx2 = it + W;
+      if (nx2 >= k1) {  // tb holds the last tile
+        ta = tb;
+        break;
+      }
+      load_tile(ta, kbase, vbase, nx2 * kTile, col, grp);
+      process_tile<D, false>(st, tb, qf, it * kTile, L, col, grp, p.scale_log2, -1, nullptr);
+      it = nx2;
+    }
+    process_tile<D, true>(st, ta, qf, it * kTile, L, col, grp, p.scale_log2, pos_new, sm.new_row);
   }
 
   // Merge the four waves through LDS.
@@ -481,7 +554,6 @@ __global__ __launch_bounds__(W * 64) void attention_kernel(AttnParams p) {
   const size_t slot = unit * p.max_parts + j;
   const bool fuse = nb > 1 && p.fused && nb * GD <= kStageFloats && nb * p.G * 2 <= kStageMl;
   // Each thread merges four channels of one head over the waves.
-  constexpr int D4 = D / 4;
   for (int idx = threadIdx.x; idx < p.G * D4; idx += NT) {
     const int hh = idx / D4;
     const int d = (idx - hh * D4) * 4;
@@ -569,56 +641,6 @@ __global__ __launch_bounds__(W * 64) void attention_kernel(AttnParams p) {
   }
   if (threadIdx.x == 0)  // ready for the next call on this workspace
     __hip_atomic_store(&p.counters[unit], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-
-// ---------------------------------------------------------------------------
-// The run schedule of a decode step, computed once for all its layers (they
-// share the lengths): one workgroup writes every workgroup's RunItem and the
-// runs per sequence.
-// ---------------------------------------------------------------------------
-__global__ __launch_bounds__(kThreads) void plan_kernel(AttnParams p, RunItem* items) {
-  __shared__ SchedShared sm;
-  if (threadIdx.x < 64) schedule_wave0(p, sm, -1);
-  __syncthreads();
-  const int R = sm.sched[0];
-  const int n_runs = sm.sched[1];
-  for (int b = threadIdx.x; b < p.B; b += kThreads) p.runs[b] = div_up(tiles_of(sm.len[b]), R);
-  // Sequences with nothing to attend get zero outputs (one thread per sequence
-  // checks; only empty ones write).
-  for (int b = threadIdx.x; b < p.B; b += kThreads) {
-    if (sm.len[b] > 0) continue;
-    const size_t e0 = static_cast<size_t>(b) * p.h * p.D;
-    for (int i = 0; i < p.h * p.D; ++i) {
-      if (p.out_bf16)
-        static_cast<uint16_t*>(p.out)[e0 + i] = 0;
-      else
-        static_cast<float*>(p.out)[e0 + i] = 0.f;
-    }
-  }
-  for (int g = threadIdx.x; g < p.n_blocks; g += kThreads) {
-    RunItem it{-1, 0, 0, 0, 0, 0, 0, 0};
-    if (g < n_runs) {
-      int lo = 0, hi = p.B - 1;  // the last sequence whose first run is <= g
-      while (lo < hi) {
-        const int mid = (lo + hi + 1) >> 1;
-        if (sm.q[mid] <= g) lo = mid; else hi = mid - 1;
-      }
-      const int L = sm.len[lo];
-      const int tiles_b = tiles_of(L);
-      const int nb = div_up(tiles_b, R);
-      const int rem = g - sm.q[lo];
-      const int r = div_up(rem + 1, nb) - 1;
-      const int j = rem - r * nb;
-      it.b = lo;
-      it.r = r;
-      it.j = j;
-      it.nb = nb;
-      it.L = L;
-      it.k0 = j * R;
-      it.k1 = it.k0 + R < tiles_b ? it.k0 + R : tiles_b;
-    }
-    items[g] = it;
-  }
 }
 
 // ---------------------------------------------------------------------------
@@ -809,12 +831,6 @@ hipError_t launch_attention_merge(const AttnParams& p, int head_dim, hipStream_t
     hipLaunchKernelGGL(combine_kernel<64>, cgrid, dim3(kThreads), 0, stream, p);
   else
     hipLaunchKernelGGL(combine_kernel<128>, cgrid, dim3(kThreads), 0, stream, p);
-  return hipGetLastError();
-}
-
-hipError_t launch_plan(const AttnParams& p, hipStream_t stream) {
-  hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(kThreads), 0, stream, p,
-                     reinterpret_cast<RunItem*>(p.plan));
   return hipGetLastError();
 }
 

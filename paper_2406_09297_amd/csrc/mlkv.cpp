@@ -260,12 +260,16 @@ struct Profile {
 };
 thread_local Profile g_profile;
 
-// plan_mode: 0 = schedule inside the attention kernel; 1 = compute the plan
-// into the workspace first (plan_kernel); 2 = reuse the plan already there.
+// plan_mode: 0 = every workgroup schedules inside the attention kernel;
+// 1 = the same, and each workgroup also records its run in the workspace's
+// plan; 2 = follow the plan already recorded there (same lengths and launch).
+// k_new/v_new (may be null): the step's new rows [B][n_kv][D]; when given,
+// the kernel also appends the heads `layer` owns (all inside its read range).
 mlkv_status attention_impl(int layer, const void* q, const mlkv_cache* cache, const mlkv_map* map,
                            const int32_t* lens, int len_offset, void* out, mlkv_out_dtype dt,
                            int max_len_hint, void* ws, size_t ws_bytes, hipStream_t stream,
-                           int plan_mode = 0) {
+                           int plan_mode = 0, const uint16_t* k_new = nullptr,
+                           const uint16_t* v_new = nullptr) {
   const int B = cache->batch, S = cache->capacity, D = cache->head_dim;
   const int max_len = max_len_hint <= 0 ? S : max_len_hint;
   const Plan pl = plan(map, layer, B, max_len, D);
@@ -284,7 +288,8 @@ mlkv_status attention_impl(int layer, const void* q, const mlkv_cache* cache, co
   char* base = static_cast<char*>(ws);
   p.counters = need ? reinterpret_cast<int*>(base + wl.counters) : nullptr;
   p.runs = need ? reinterpret_cast<int*>(base + wl.runs) : nullptr;
-  p.plan = need && plan_mode != 0 ? base + wl.plan : nullptr;
+  p.plan = need && plan_mode == 2 ? base + wl.plan : nullptr;
+  p.plan_out = need && plan_mode == 1 ? base + wl.plan : nullptr;
   p.part_acc = need ? reinterpret_cast<float*>(base + wl.acc) : nullptr;
   p.part_ml = need ? reinterpret_cast<float*>(base + wl.ml) : nullptr;
   p.B = B;
@@ -305,9 +310,14 @@ mlkv_status attention_impl(int layer, const void* q, const mlkv_cache* cache, co
   p.len_offset = len_offset;
   p.out_bf16 = dt == MLKV_OUT_BF16 ? 1 : 0;
   p.scale_log2 = static_cast<float>(1.4426950408889634 / std::sqrt(static_cast<double>(D)));
+  if (k_new && map->own_count[layer] > 0) {
+    p.k_new = k_new;
+    p.v_new = v_new;
+    p.new_stride = map->n_kv * D;
+    p.own_begin = map->own_begin[layer];
+    p.own_count = map->own_count[layer];
+  }
   hipError_t err = hipSuccess;
-  if (p.plan && plan_mode == 1) err = mlkv::launch_plan(p, stream);
-  if (err != hipSuccess) return fail(MLKV_ERR_HIP, "plan launch: %s", hipGetErrorString(err));
   Profile& prof = g_profile;
   const bool timed = prof.on && prof.used < static_cast<int>(prof.start.size());
   err = mlkv::launch_attention_main(p, D, stream, timed ? prof.start[prof.used] : nullptr,
@@ -589,7 +599,12 @@ mlkv_status mlkv_decode_step(const void* q_all, const void* k_new_all, const voi
   const uint16_t* v_new = static_cast<const uint16_t*>(v_new_all);
   int planned_key = -1;
   for (int n = 0; n < map->l; ++n) {
-    if (map->own_count[n] > 0) {
+    // The attention launch appends the heads the layer owns when it reads
+    // them all; otherwise a separate append runs first.
+    const bool fused_append = map->own_count[n] > 0 && map->own_begin[n] >= map->kv_begin[n] &&
+                              map->own_begin[n] + map->own_count[n] <=
+                                  map->kv_begin[n] + map->kv_count[n];
+    if (map->own_count[n] > 0 && !fused_append) {
       const size_t col = static_cast<size_t>(map->own_begin[n]) * D;
       if ((s = append_impl(n, map, cache, k_new + col, v_new + col, n_kv * D, ctx_lens, stream)) !=
           MLKV_OK)
@@ -602,7 +617,8 @@ mlkv_status mlkv_decode_step(const void* q_all, const void* k_new_all, const voi
     const int key = map->kv_count[n];
     const int mode = key == planned_key ? 2 : 1;
     if ((s = attention_impl(n, q, cache, map, ctx_lens, 1, out, out_dtype, max_len_hint, workspace,
-                            workspace_bytes, stream, mode)) != MLKV_OK)
+                            workspace_bytes, stream, mode, fused_append ? k_new : nullptr,
+                            fused_append ? v_new : nullptr)) != MLKV_OK)
       return s;
     planned_key = key;
   }

@@ -305,3 +305,62 @@ def test_full_size_step_with_in_place_merge():
     ref, k_ref, v_ref = _oracle_step(dw2)
     assert np.array_equal(k_gpu, k_ref) and np.array_equal(v_gpu, v_ref), "cache differs"
     check_close(out, ref, "step in-place merge")
+
+
+# ---------------------------------------------------- fused append in step --
+
+def _with_contexts(dw, ctx):
+    """Give a device workload explicit per-sequence contexts: slots at or past
+    each context are NaN-poisoned again on host and device."""
+    ctx = np.asarray(ctx, dtype=np.int32)
+    assert ctx.size == dw.w.B and ctx.max() < dw.S
+    for arr in (dw.host["k_cache"], dw.host["v_cache"]):
+        for b, c in enumerate(ctx):
+            arr[:, b, max(c, 0):] = synth.BF16_NAN
+    dw.host["ctx"] = ctx
+    dw.ctx = torch.from_numpy(ctx).cuda()
+    dw.cache.load_rows(dw.host["k_cache"], dw.host["v_cache"])
+    return dw
+
+
+APPEND_CTX = [0, 1, 30, 31, 32, 33, 63, 64, 95, 96, 127, 128, 200, 254, 255]
+
+
+@pytest.mark.parametrize("D,m,g,workgroups,wide", [
+    (64, 4, 1, "", ""), (64, 4, 1, "7", ""), (64, 4, 1, "", "1"), (64, 4, 3, "40", ""),
+    (128, 2, 4, "", ""), (128, 2, 4, "", "1")])
+def test_step_fused_append_across_tile_boundaries(D, m, g, workgroups, wide):
+    """The owning layers append inside their attention launch: the new token
+    lands at every offset of a 32-token tile (and in the last slot of the
+    cache), is attended by the owner in the same launch and by the later
+    layers of its group; the whole cache matches the oracle bit for bit."""
+    w = synth.Workload("append_sweep", l=4, h=12, m=m, g=g, D=D, B=len(APPEND_CTX),
+                       ctx=max(APPEND_CTX), seed=77)
+    dw = _with_contexts(DeviceWorkload(w), APPEND_CTX)
+    assert dw.S == 256  # the last context appends into the last slot
+    say(f"fused append D={D} m={m} g={g} workgroups={workgroups or 'auto'} wide={wide or 'auto'}")
+    with plan_env(workgroups=workgroups, wide=wide):
+        out = _run_step(dw).cpu().numpy()
+    k_gpu, v_gpu = dw.read_cache()
+    ref, k_ref, v_ref = _oracle_step(dw)
+    assert np.array_equal(k_gpu, k_ref) and np.array_equal(v_gpu, v_ref), "cache differs"
+    check_close(out, ref, f"fused append D{D} m{m} g{g} wg{workgroups} {wide}")
+
+
+def test_step_owner_that_does_not_read_its_head():
+    """A general map where layer 0 owns KV heads 0 and 1 but reads only head 0:
+    head 1 is appended by a separate launch before layer 0 attends, and layer
+    1 reads it."""
+    w = synth.Workload("general", l=4, h=4, m=2, g=1, D=64, B=3, ctx=100, seed=11)
+    dw = DeviceWorkload(w)
+    kv_of = np.array([[0] * 4, [1] * 4, [0] * 4, [1] * 4], np.int32)
+    owner_of = np.array([0, 0], np.int32)
+    dw.map = mlkv.Map.from_tables(kv_of, owner_of)
+    dw.kv_of, dw.owner_of = kv_of, owner_of
+    _with_contexts(dw, [0, 37, 100])
+    say("general map: owner not reading its head")
+    out = _run_step(dw).cpu().numpy()
+    k_gpu, v_gpu = dw.read_cache()
+    ref, k_ref, v_ref = _oracle_step(dw)
+    assert np.array_equal(k_gpu, k_ref) and np.array_equal(v_gpu, v_ref), "cache differs"
+    check_close(out, ref, "general map")
