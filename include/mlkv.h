@@ -202,11 +202,12 @@ mlkv_status mlkv_decode_step(const void* q_all, const void* k_new_all, const voi
 
 /* Work plan mlkv_decode_attention uses for `layer` at this max length: the
  * 32-token tiles of all (sequence, KV head) pairs form one flat list shared
- * equally by `workgroups` workgroups (the device's resident capacity, capped
- * at 128 per (sequence, KV head) and at one per 4 tiles; one workgroup for at
+ * equally by `workgroups` workgroups (two per compute unit, or the device's
+ * resident capacity if lower; capped at 128 per (sequence, KV head) and at
+ * one per 4 tiles, at least one per (sequence, KV head); one workgroup for at
  * most 16 tiles); `max_parts` bounds the workgroups covering one sequence.
  * Environment overrides, read on every call (tests and tuning):
- *   MLKV_WORKGROUPS=n   resident capacity assumed instead of the device's;
+ *   MLKV_WORKGROUPS=n   workgroup budget n instead of the device's;
  *   MLKV_COMBINE=fused  the last run of each unit merges its runs in place
  *                       when they fit the kernel's staging area;
  *   MLKV_WIDE=1         one run per unit on a wider workgroup (no partials,

@@ -58,6 +58,7 @@ int max_batch();
 int stage_floats();  // partial-output floats one workgroup can merge in place
 int resident_workgroups(int head_dim); // attention workgroups the device holds at once (0: none)
 int wide_waves();                      // waves per workgroup of the one-run-per-unit layout
+int compute_units();                   // compute units of the current device (0: unknown)
 int default_waves();                   // waves per workgroup otherwise
 hipError_t launch_fill(uint32_t* dst, size_t n_words, uint32_t value, hipStream_t stream);
 

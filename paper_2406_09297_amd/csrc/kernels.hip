@@ -837,6 +837,18 @@ hipError_t launch_attention_merge(const AttnParams& p, int head_dim, hipStream_t
 int max_batch() { return kMaxBatch; }
 int stage_floats() { return kStageFloats; }
 
+int compute_units() {
+  static std::atomic<int> cached{-1};
+  int v = cached.load(std::memory_order_relaxed);
+  if (v >= 0) return v;
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+    return 0;
+  cached.store(cus, std::memory_order_relaxed);
+  return cus;
+}
+
 int wide_waves() { return kWideWaves; }
 int default_waves() { return kWaves; }
 

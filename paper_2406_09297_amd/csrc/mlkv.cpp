@@ -142,6 +142,7 @@ struct Plan {
 constexpr int kMinTiles = 4;
 constexpr int kMaxRunsPerUnit = 128;
 constexpr int kFallbackResident = 768;  // 256 CUs x 3 when no device can be queried
+constexpr int kWorkgroupsPerCu = 2;
 
 long workgroups_for(long resident, long units, long t_max, int min_tiles) {
   long g = resident < kMaxRunsPerUnit * units ? resident : kMaxRunsPerUnit * units;
@@ -164,6 +165,12 @@ Plan plan(const mlkv_map* map, int layer, int batch, int max_len, int head_dim) 
   const long t_max = units * pl.max_tiles;
   long resident = mlkv::resident_workgroups(head_dim);
   if (resident <= 0) resident = kFallbackResident;
+  // Two workgroups per compute unit: on MI355X fewer, longer runs beat
+  // filling every resident slot (fewer partials, longer pipelines), and a
+  // whole multiple of the compute units keeps their bandwidth shares equal.
+  long cus = mlkv::compute_units();
+  if (cus <= 0) cus = kFallbackResident / 3;
+  if (resident > kWorkgroupsPerCu * cus) resident = kWorkgroupsPerCu * cus;
   if (const char* env = std::getenv("MLKV_WORKGROUPS")) {
     const long w = std::atol(env);
     if (w > 0) resident = w;
