@@ -36,6 +36,7 @@ struct AttnParams {
   int len_offset, out_bf16;
   int fused;                 // 1: the last run of a unit merges its partials when they fit LDS
   int merge_waves;           // waves merging one (sequence, head) row: 1 or 4
+  int merge_first;           // partial slots the merge reads before it knows the run count
   int waves;                 // waves per attention workgroup: 4, or wide_waves() for single runs
   float scale_log2;          // log2(e) / sqrt(D)
   // Fused append (owning layer of a decode step), k_new null when none: row

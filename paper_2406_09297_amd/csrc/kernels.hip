@@ -678,23 +678,24 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(AttnParams p) {
 
   float m[U], w[U];
   f32x4 a[U];
-  auto load_round = [&](int s0, int ns) {
+  auto load_round = [&](int s0, int ns) {  // lanes past ns load nothing
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int s = s0 + first + u * stride;
-      const bool ok = s < ns;
-      const size_t slot = base + (ok ? s : 0);
-      const float mm = p.part_ml[(slot * p.G + hh) * 2];
-      const float ww = p.part_ml[(slot * p.G + hh) * 2 + 1];
-      const f32x4 aa = *reinterpret_cast<const f32x4*>(&p.part_acc[slot * GD + hh * D + c]);
-      m[u] = ok ? mm : -INFINITY;
-      w[u] = ok ? ww : 0.f;
-      a[u] = ok ? aa : f32x4{0.f, 0.f, 0.f, 0.f};
+      m[u] = -INFINITY;
+      w[u] = 0.f;
+      a[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+      if (s < ns) {
+        const size_t slot = base + s;
+        m[u] = p.part_ml[(slot * p.G + hh) * 2];
+        w[u] = p.part_ml[(slot * p.G + hh) * 2 + 1];
+        a[u] = *reinterpret_cast<const f32x4*>(&p.part_acc[slot * GD + hh * D + c]);
+      }
     }
   };
-  // First round before the run count is known: every slot below max_parts
-  // is inside the workspace.
-  load_round(0, p.max_parts);
+  // First round before the run count is known, over the slots the launch
+  // expects to be used (p.merge_first <= max_parts: inside the workspace).
+  load_round(0, p.merge_first);
   const int ns = row_ok ? p.runs[b] : 0;  // runs of each unit of sequence b
   const bool merged_in_place =
       ns == 1 || (p.fused && ns * p.G * D <= kStageFloats && ns * p.G * 2 <= kStageMl);

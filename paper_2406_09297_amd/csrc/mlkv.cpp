@@ -311,8 +311,12 @@ mlkv_status attention_impl(int layer, const void* q, const mlkv_cache* cache, co
   p.max_parts = pl.max_parts;
   p.fused = pl.fused;
   p.waves = pl.waves;
-  // One wave merges a row when units average at most 16 runs, else four.
-  p.merge_waves = pl.n_blocks <= 16L * B * map->kv_count[layer] ? 1 : 4;
+  // One wave merges a row when units average at most 16 runs, else four;
+  // the merge's first reads cover twice the average runs per unit.
+  const long units = static_cast<long>(B) * map->kv_count[layer];
+  p.merge_waves = pl.n_blocks <= 16L * units ? 1 : 4;
+  const long avg_runs = (pl.n_blocks + units - 1) / units;
+  p.merge_first = static_cast<int>(2 * avg_runs < pl.max_parts ? 2 * avg_runs : pl.max_parts);
   p.D = D;
   p.len_offset = len_offset;
   p.out_bf16 = dt == MLKV_OUT_BF16 ? 1 : 0;
