@@ -108,6 +108,8 @@ def main():
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--map", default=None,
+                    help="m,g of a map-sweep workload (default: its last point)")
     ap.add_argument("--no-cold", action="store_true",
                     help="skip timing attention launches after a 1 GiB read evicts the caches")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -129,7 +131,10 @@ def main():
     dev = "cuda:0"
     torch.cuda.set_device(0)
     w = synth.get_workload(args.workload)
-    if w.sweep:
+    if args.map:
+        m, g = (int(x) for x in args.map.split(","))
+        w = w.with_map(m, g)
+    elif w.sweep:
         m, g = w.sweep[-1]
         w = w.with_map(m, g)
     log(f"[bench] workload {w.name}: generating inputs")
