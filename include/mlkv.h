@@ -211,7 +211,9 @@ mlkv_status mlkv_decode_step(const void* q_all, const void* k_new_all, const voi
  *   MLKV_COMBINE=fused  the last run of each unit merges its runs in place
  *                       when they fit the kernel's staging area;
  *   MLKV_WIDE=1         one run per unit on a wider workgroup (no partials,
- *                       no merge kernel).
+ *                       no merge kernel);
+ *   MLKV_QK=valu        q.K as bf16 dot products on the vector ALUs instead
+ *                       of matrix-core (MFMA) instructions.
  * The workspace size from mlkv_workspace_bytes covers every choice.
  * Returns MLKV_ERR_* on invalid arguments. */
 mlkv_status mlkv_plan(const mlkv_map* map, int layer, int batch, int capacity, int head_dim,

@@ -65,6 +65,37 @@ __device__ __forceinline__ f32x4 mfma_bf16(bf16x8 a, bf16x8 b, f32x4 c) {
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+// Dot product of 8 bf16 pairs' worth of channels in fp32 (exact products).
+__device__ __forceinline__ float dot8_bf16(u16x8 a, u16x8 b) {
+  const bf16x8 x = as_bf16(a), y = as_bf16(b);
+  float c = 0.f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+    c = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{x[2 * i], x[2 * i + 1]}, bf16x2{y[2 * i], y[2 * i + 1]},
+                                        c, false);
+  return c;
+}
+
+// DPP move of a float within rows of 16 lanes.
+template <int CTRL>
+__device__ __forceinline__ float dpp(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), CTRL, 0xF,
+                                                            0xF, false));
+}
+
+// Sum over aligned groups of N (8 or 16) consecutive lanes, left in every
+// lane of the group: swaps inside quads, then half-row and row mirrors.
+template <int N>
+__device__ __forceinline__ float row_group_sum(float v) {
+  v += dpp<0xB1>(v);   // quad_perm [1,0,3,2]
+  v += dpp<0x4E>(v);   // quad_perm [2,3,0,1]
+  v += dpp<0x141>(v);  // row_half_mirror: lane i <-> 7-i within 8
+  if (N == 16) v += dpp<0x140>(v);  // row_mirror: lane i <-> 15-i within 16
+  return v;
+}
+
 // Device-scope (all XCDs) stores and loads for partials merged inside the
 // attention kernel: on CDNA3/4 the scope travels with each access (SC bits),
 // so no L2 writeback or invalidate is needed, only completion of the stores
@@ -129,15 +160,25 @@ struct Tile {
 
 // Score block sb, MFMA row rr holds token 8*(rr/4) + 4*sb + rr%4, so the result
 // lane (col, grp) ends up with tokens 8*grp + 4*sb + i: the P^T k-slots it owns.
-template <int D>
+//
+// QK_VALU (the VALU dot-product variant of q.K): the tile's key rows are read
+// as contiguous 1 KB pieces instead; lane l of piece j holds channels
+// 8*(l % (D/8)) .. +7 of row j*(512/D) + l/(D/8).
+template <int D, bool QK_VALU>
 __device__ __forceinline__ void load_tile(Tile<D>& t, const uint16_t* kbase,
                                           const uint16_t* vbase, int t0, int col, int grp) {
+  if (QK_VALU) {
+    const uint16_t* kt = kbase + static_cast<size_t>(t0) * D + (grp * 16 + col) * 8;
 #pragma unroll
-  for (int sb = 0; sb < 2; ++sb) {
-    const int tok = t0 + (col >> 2) * 8 + sb * 4 + (col & 3);
-    const uint16_t* krow = kbase + static_cast<size_t>(tok) * D + grp * 8;
+    for (int j = 0; j < 2 * Tile<D>::KK; ++j) t.k[j / Tile<D>::KK][j % Tile<D>::KK] = load16(kt + j * 512);
+  } else {
 #pragma unroll
-    for (int kk = 0; kk < Tile<D>::KK; ++kk) t.k[sb][kk] = load16(krow + kk * 32);
+    for (int sb = 0; sb < 2; ++sb) {
+      const int tok = t0 + (col >> 2) * 8 + sb * 4 + (col & 3);
+      const uint16_t* krow = kbase + static_cast<size_t>(tok) * D + grp * 8;
+#pragma unroll
+      for (int kk = 0; kk < Tile<D>::KK; ++kk) t.k[sb][kk] = load16(krow + kk * 32);
+    }
   }
   const uint16_t* vblk = vbase + static_cast<size_t>(t0) * D + grp * 8;
 #pragma unroll
@@ -160,18 +201,29 @@ constexpr float kLazyRescale = 8.f;
 // ragged end of a sequence or the newest token.  pos_new >= 0: position of
 // the newest token, whose key and value are taken from new_row (LDS: key
 // then value, D each) instead of the loaded tile.
-template <int D, bool LAST>
+template <int D, bool LAST, bool QK_VALU>
 __device__ __forceinline__ void process_tile(WaveState<D>& st, Tile<D>& t, const bf16x8* qf,
                                              int t0, int L, int col, int grp, float scale_log2,
-                                             int pos_new, const uint16_t* new_row) {
+                                             int pos_new, const uint16_t* new_row,
+                                             const uint16_t* q_lds, float* s_lds, int G) {
   constexpr int KK = Tile<D>::KK, DB = Tile<D>::DB;
+  constexpr int LPR = D / 8;         // QK_VALU: lanes holding one key row
+  constexpr int RPP = 512 / D;       // QK_VALU: rows per 1 KB piece
+  const int lane = grp * 16 + col;
   if (LAST && pos_new >= t0 && pos_new < t0 + kTile) {
+    if (QK_VALU) {
 #pragma unroll
-    for (int sb = 0; sb < 2; ++sb) {
-      if (t0 + (col >> 2) * 8 + sb * 4 + (col & 3) == pos_new) {
+      for (int j = 0; j < 2 * KK; ++j)
+        if (t0 + j * RPP + lane / LPR == pos_new)
+          t.k[j / KK][j % KK] = *reinterpret_cast<const u16x8*>(new_row + (lane % LPR) * 8);
+    } else {
 #pragma unroll
-        for (int kk = 0; kk < KK; ++kk)
-          t.k[sb][kk] = *reinterpret_cast<const u16x8*>(new_row + grp * 8 + kk * 32);
+      for (int sb = 0; sb < 2; ++sb) {
+        if (t0 + (col >> 2) * 8 + sb * 4 + (col & 3) == pos_new) {
+#pragma unroll
+          for (int kk = 0; kk < KK; ++kk)
+            t.k[sb][kk] = *reinterpret_cast<const u16x8*>(new_row + grp * 8 + kk * 32);
+        }
       }
     }
     const int e_new = pos_new - t0 - grp * 8;  // in [0, 8) for the lanes holding it
@@ -183,18 +235,49 @@ __device__ __forceinline__ void process_tile(WaveState<D>& st, Tile<D>& t, const
         if (e == e_new) t.v[db][e] = vn;
     }
   }
-  f32x4 s[2];
-#pragma unroll
-  for (int sb = 0; sb < 2; ++sb) {
-    s[sb] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int kk = 0; kk < KK; ++kk) s[sb] = mfma_bf16(as_bf16(t.k[sb][kk]), qf[kk], s[sb]);
-  }
   float x[8];  // raw scores q.k of tokens 8*grp + e
+  if (QK_VALU) {
+    // Per head: each lane dots its 8 channels of each held row with q
+    // (v_dot2 on bf16 pairs, fp32 sums), the LPR lanes of a row add up by
+    // DPP, and the row scores go through this wave's LDS block s_lds[16][32]
+    // to the lanes that use them as P^T k-slots.
+    const int c8 = lane % LPR;
+    for (int hh = 0; hh < G; ++hh) {
+      const u16x8 qq = *reinterpret_cast<const u16x8*>(q_lds + hh * D + c8 * 8);
+      float part[2 * KK];
 #pragma unroll
-  for (int sb = 0; sb < 2; ++sb)
+      for (int j = 0; j < 2 * KK; ++j) part[j] = dot8_bf16(t.k[j / KK][j % KK], qq);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) x[sb * 4 + i] = s[sb][i];
+      for (int j = 0; j < 2 * KK; ++j) part[j] = row_group_sum<LPR>(part[j]);
+      if (c8 == hh % LPR) {
+#pragma unroll
+        for (int j = 0; j < 2 * KK; ++j) s_lds[hh * kTile + j * RPP + lane / LPR] = part[j];
+      }
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    const f32x4 lo = *reinterpret_cast<const f32x4*>(s_lds + col * kTile + grp * 8);
+    const f32x4 hi = *reinterpret_cast<const f32x4*>(s_lds + col * kTile + grp * 8 + 4);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      x[i] = lo[i];
+      x[4 + i] = hi[i];
+    }
+    __builtin_amdgcn_wave_barrier();  // reads done before the next tile's writes
+  } else {
+    f32x4 s[2];
+#pragma unroll
+    for (int sb = 0; sb < 2; ++sb) {
+      s[sb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kk = 0; kk < KK; ++kk) s[sb] = mfma_bf16(as_bf16(t.k[sb][kk]), qf[kk], s[sb]);
+    }
+#pragma unroll
+    for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) x[sb * 4 + i] = s[sb][i];
+  }
 
   if (LAST && t0 + kTile > L) {  // ragged tail: positions >= L take no weight and no value
     const int first = t0 + grp * 8;
@@ -285,7 +368,7 @@ struct SchedShared {
 constexpr int kStageFloats = 8192;
 constexpr int kStageMl = 512;
 
-template <int D, int W>
+template <int D, int W, bool QK_VALU>
 struct alignas(16) AttnShared {
   union {  // phases: schedule, then the waves' merge, then (last run only) staging
     SchedShared sc;
@@ -298,6 +381,10 @@ struct alignas(16) AttnShared {
   };
   float stage_ml[kStageMl];
   alignas(16) uint16_t new_row[2 * D];  // newest token's key and value (fused append)
+  // QK_VALU: the group's queries (16 heads, zero-padded) and each wave's
+  // score block [16 heads][32 tokens].
+  alignas(16) uint16_t q_lds[QK_VALU ? 16 * D : 8];
+  alignas(16) float s_lds[QK_VALU ? W * 16 * kTile : 4];
   int last;
 };
 
@@ -400,13 +487,13 @@ __device__ void schedule_wave0(const AttnParams& p, SchedShared& sm, int g) {
 
 // Register budget: at least 3 waves per SIMD for D = 64 and 2 for D = 128
 // with four-wave workgroups (12 / 8 waves per compute unit in flight).
-template <int D, int W>
+template <int D, int W, bool QK_VALU>
 __global__ __launch_bounds__(W * 64) __attribute__((amdgpu_waves_per_eu(D == 64 ? 3 : 2)))
 void attention_kernel(AttnParams p) {
   constexpr int KK = Tile<D>::KK, DB = Tile<D>::DB;
   constexpr int NT = W * 64;  // threads
   constexpr int D4 = D / 4;    // four-channel groups of a head
-  __shared__ AttnShared<D, W> sm;
+  __shared__ AttnShared<D, W, QK_VALU> sm;
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int col = lane & 15;  // query head inside the group / MFMA row
@@ -465,6 +552,18 @@ void attention_kernel(AttnParams p) {
   const uint16_t* kbase = p.k + seq * p.S * D;
   const uint16_t* vbase = p.v + seq * p.S * D;
 
+  if (QK_VALU) {  // stage the group's queries (padded heads zero) and zero padded score rows
+    for (int idx = threadIdx.x; idx < 16 * D / 8; idx += NT) {
+      const int hh = idx / (D / 8);
+      const int c = (idx - hh * (D / 8)) * 8;
+      u16x8 v = {0, 0, 0, 0, 0, 0, 0, 0};
+      if (hh < p.G) v = load16(p.q + (static_cast<size_t>(b) * p.h + head0 + hh) * D + c);
+      *reinterpret_cast<u16x8*>(&sm.q_lds[hh * D + c]) = v;
+    }
+    for (int idx = threadIdx.x; idx < W * 16 * kTile; idx += NT)
+      if ((idx / kTile) % 16 >= p.G) sm.s_lds[idx] = 0.f;
+    __syncthreads();
+  }
   bf16x8 qf[KK];
   {
     const bool valid = col < p.G;
@@ -485,7 +584,8 @@ void attention_kernel(AttnParams p) {
   for (int db = 0; db < DB; ++db) st.acc[db] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   const bool has_tiles = it < k1;
-  if (has_tiles) load_tile(ta, kbase, vbase, it * kTile, col, grp);
+  if (has_tiles) load_tile<D, QK_VALU>(ta, kbase, vbase, it * kTile, col, grp);
+  float* const s_wave = sm.s_lds + (QK_VALU ? wave * 16 * kTile : 0);
 
   // Fused append of the owning layer (Section 2.4): the last run of each
   // owned unit writes the newest token's K/V row into slot lens[b] +
@@ -523,19 +623,22 @@ void attention_kernel(AttnParams p) {
     for (;;) {
       const int nxt = it + W;
       if (nxt >= k1) break;  // ta holds the last tile
-      load_tile(tb, kbase, vbase, nxt * kTile, col, grp);
-      process_tile<D, false>(st, ta, qf, it * kTile, L, col, grp, p.scale_log2, -1, nullptr);
+      load_tile<D, QK_VALU>(tb, kbase, vbase, nxt * kTile, col, grp);
+      process_tile<D, false, QK_VALU>(st, ta, qf, it * kTile, L, col, grp, p.scale_log2, -1,
+                                      nullptr, sm.q_lds, s_wave, p.G);
       it = nxt;
       const int nx2 = it + W;
       if (nx2 >= k1) {  // tb holds the last tile
         ta = tb;
         break;
       }
-      load_tile(ta, kbase, vbase, nx2 * kTile, col, grp);
-      process_tile<D, false>(st, tb, qf, it * kTile, L, col, grp, p.scale_log2, -1, nullptr);
+      load_tile<D, QK_VALU>(ta, kbase, vbase, nx2 * kTile, col, grp);
+      process_tile<D, false, QK_VALU>(st, tb, qf, it * kTile, L, col, grp, p.scale_log2, -1,
+                                      nullptr, sm.q_lds, s_wave, p.G);
       it = nx2;
     }
-    process_tile<D, true>(st, ta, qf, it * kTile, L, col, grp, p.scale_log2, pos_new, sm.new_row);
+    process_tile<D, true, QK_VALU>(st, ta, qf, it * kTile, L, col, grp, p.scale_log2, pos_new,
+                                   sm.new_row, sm.q_lds, s_wave, p.G);
   }
 
   // Merge the four waves through LDS.
@@ -796,11 +899,11 @@ hipError_t launch_append(const AppendParams& p, int head_dim, int owned_count,
   return hipGetLastError();
 }
 
-template <int D, int W>
+template <int D, int W, bool QK_VALU = false>
 static void launch_attention_t(const AttnParams& p, hipStream_t stream, hipEvent_t start,
                                hipEvent_t stop) {
   const dim3 grid(p.n_blocks), block(W * 64);
-  auto kernel = attention_kernel<D, W>;
+  auto kernel = attention_kernel<D, W, QK_VALU>;
   if (start)  // timed: events recorded with the dispatch itself
     hipExtLaunchKernelGGL(kernel, grid, block, 0, stream, start, stop, 0, p);
   else
@@ -813,11 +916,15 @@ hipError_t launch_attention_main(const AttnParams& p, int head_dim, hipStream_t 
   if (head_dim == 64) {
     if (wide)
       launch_attention_t<64, kWideWaves>(p, stream, start, stop);
+    else if (p.qk_valu)
+      launch_attention_t<64, kWaves, true>(p, stream, start, stop);
     else
       launch_attention_t<64, kWaves>(p, stream, start, stop);
   } else {
     if (wide)
       launch_attention_t<128, kWideWaves>(p, stream, start, stop);
+    else if (p.qk_valu)
+      launch_attention_t<128, kWaves, true>(p, stream, start, stop);
     else
       launch_attention_t<128, kWaves>(p, stream, start, stop);
   }
@@ -864,8 +971,8 @@ int resident_workgroups(int head_dim) {
     return 0;
   const hipError_t err =
       head_dim == 64
-          ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attention_kernel<64, kWaves>, kThreads, 0)
-          : hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attention_kernel<128, kWaves>, kThreads, 0);
+          ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attention_kernel<64, kWaves, false>, kThreads, 0)
+          : hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attention_kernel<128, kWaves, false>, kThreads, 0);
   if (err != hipSuccess) return 0;
   v = cus * per_cu;
   slot.store(v, std::memory_order_relaxed);

@@ -311,6 +311,7 @@ mlkv_status attention_impl(int layer, const void* q, const mlkv_cache* cache, co
   p.max_parts = pl.max_parts;
   p.fused = pl.fused;
   p.waves = pl.waves;
+  if (const char* env = std::getenv("MLKV_QK")) p.qk_valu = std::strcmp(env, "valu") == 0 ? 1 : 0;
   // One wave merges a row when units average at most 16 runs, else four;
   // the merge's first reads cover twice the average runs per unit.
   const long units = static_cast<long>(B) * map->kv_count[layer];

@@ -34,12 +34,13 @@ def small(name, **kw):
 
 
 @contextlib.contextmanager
-def plan_env(workgroups="", merge="", wide=""):
+def plan_env(workgroups="", merge="", wide="", qk=""):
     """Launch-plan overrides read by the library on every call:
-    MLKV_WORKGROUPS (resident workgroups assumed), MLKV_COMBINE=fused (merge
-    runs inside the attention kernel), MLKV_WIDE=0/1 (one run per unit on a
-    wide workgroup: off / forced)."""
-    names = {"MLKV_WORKGROUPS": workgroups, "MLKV_COMBINE": merge, "MLKV_WIDE": wide}
+    MLKV_WORKGROUPS (workgroup budget), MLKV_COMBINE=fused (merge runs inside
+    the attention kernel), MLKV_WIDE=0/1 (one run per unit on a wide
+    workgroup: off / forced), MLKV_QK=valu (q.K on the vector ALUs)."""
+    names = {"MLKV_WORKGROUPS": workgroups, "MLKV_COMBINE": merge, "MLKV_WIDE": wide,
+             "MLKV_QK": qk}
     for k, v in names.items():
         if v:
             os.environ[k] = v
@@ -120,18 +121,19 @@ def test_length_sweep_across_tile_boundaries(D, m, g):
     dw = DeviceWorkload(w)
     lens = np.array(LEN_SWEEP, dtype=np.int32)
     lens_d = torch.from_numpy(lens).cuda()
-    for wg, comb, wide in (("", "", ""), ("3", "", ""), ("40", "", ""), ("", "fused", ""),
-                           ("40", "fused", ""), ("", "", "1"), ("", "", "0")):
-        with plan_env(wg, comb, wide):
+    for wg, comb, wide, qk in (("", "", "", ""), ("3", "", "", ""), ("40", "", "", ""),
+                               ("", "fused", "", ""), ("40", "fused", "", ""), ("", "", "1", ""),
+                               ("", "", "0", ""), ("", "", "", "valu"), ("40", "", "", "valu")):
+        with plan_env(wg, comb, wide, qk):
             for n in (0, w.l - 1):
                 say(f"length sweep D={D} m={m} g={g} layer={n} workgroups={wg or 'auto'} "
-                    f"merge={comb or 'kernel'} wide={wide or 'auto'}")
+                    f"merge={comb or 'kernel'} wide={wide or 'auto'} qk={qk or 'mfma'}")
                 out = torch.empty((w.B, w.h, w.D), dtype=torch.float32, device="cuda")
                 mlkv.decode_attention(n, dw.q[n], dw.cache, dw.map, lens_d, out, ws=dw.ws)
                 torch.cuda.synchronize()
                 ref = oracle.decode_attention(n, dw.host["q"][n], dw.host["k_cache"],
                                               dw.host["v_cache"], dw.kv_of, lens)
-                check_close(out.cpu().numpy(), ref, f"sweep D{D} g{g} L{n} wg{wg} {comb} {wide}")
+                check_close(out.cpu().numpy(), ref, f"sweep D{D} g{g} L{n} wg{wg} {comb} {wide} {qk}")
 
 
 def test_split_count_invariance_and_determinism():
@@ -257,16 +259,19 @@ def test_step_mlkv2_empty_context_outputs_new_value_exactly():
                                       f64(dw.host["v_new"][b, n // 6]).astype(np.float32))
 
 
-@pytest.mark.parametrize("wname,wide", [("mlkv2_b1", ""), ("mlkv4_b128_ragged", ""),
-                                        ("mlkv4_b128_ragged", "1"), ("mlkv4_b8_long", "")])
-def test_full_size_step_matches_oracle(wname, wide):
+@pytest.mark.parametrize("wname,wide,qk", [("mlkv2_b1", "", ""), ("mlkv4_b128_ragged", "", ""),
+                                           ("mlkv4_b128_ragged", "1", ""),
+                                           ("mlkv4_b128_ragged", "", "valu"),
+                                           ("mlkv4_b8_long", "", "")])
+def test_full_size_step_matches_oracle(wname, wide, qk):
     """Full-size workloads in the launch configuration the benchmark times
-    (and the ragged batch also with one wide workgroup per sequence)."""
+    (and the ragged batch also with one wide workgroup per sequence, and with
+    q.K on the vector ALUs)."""
     w = synth.get_workload(wname)
-    say(f"full step {wname} wide={wide or 'auto'}: uploading")
+    say(f"full step {wname} wide={wide or 'auto'} qk={qk or 'mfma'}: uploading")
     dw = DeviceWorkload(w)
     say(f"full step {wname}: running")
-    with plan_env(wide=wide):
+    with plan_env(wide=wide, qk=qk):
         out = _run_step(dw).cpu().numpy()
     k_gpu, v_gpu = dw.read_cache()
     say(f"full step {wname}: oracle")
@@ -326,10 +331,11 @@ def _with_contexts(dw, ctx):
 APPEND_CTX = [0, 1, 30, 31, 32, 33, 63, 64, 95, 96, 127, 128, 200, 254, 255]
 
 
-@pytest.mark.parametrize("D,m,g,workgroups,wide", [
-    (64, 4, 1, "", ""), (64, 4, 1, "7", ""), (64, 4, 1, "", "1"), (64, 4, 3, "40", ""),
-    (128, 2, 4, "", ""), (128, 2, 4, "", "1")])
-def test_step_fused_append_across_tile_boundaries(D, m, g, workgroups, wide):
+@pytest.mark.parametrize("D,m,g,workgroups,wide,qk", [
+    (64, 4, 1, "", "", ""), (64, 4, 1, "7", "", ""), (64, 4, 1, "", "1", ""),
+    (64, 4, 3, "40", "", ""), (128, 2, 4, "", "", ""), (128, 2, 4, "", "1", ""),
+    (64, 4, 1, "", "", "valu"), (128, 2, 4, "7", "", "valu")])
+def test_step_fused_append_across_tile_boundaries(D, m, g, workgroups, wide, qk):
     """The owning layers append inside their attention launch: the new token
     lands at every offset of a 32-token tile (and in the last slot of the
     cache), is attended by the owner in the same launch and by the later
@@ -338,13 +344,14 @@ def test_step_fused_append_across_tile_boundaries(D, m, g, workgroups, wide):
                        ctx=max(APPEND_CTX), seed=77)
     dw = _with_contexts(DeviceWorkload(w), APPEND_CTX)
     assert dw.S == 256  # the last context appends into the last slot
-    say(f"fused append D={D} m={m} g={g} workgroups={workgroups or 'auto'} wide={wide or 'auto'}")
-    with plan_env(workgroups=workgroups, wide=wide):
+    say(f"fused append D={D} m={m} g={g} workgroups={workgroups or 'auto'} wide={wide or 'auto'} "
+        f"qk={qk or 'mfma'}")
+    with plan_env(workgroups=workgroups, wide=wide, qk=qk):
         out = _run_step(dw).cpu().numpy()
     k_gpu, v_gpu = dw.read_cache()
     ref, k_ref, v_ref = _oracle_step(dw)
     assert np.array_equal(k_gpu, k_ref) and np.array_equal(v_gpu, v_ref), "cache differs"
-    check_close(out, ref, f"fused append D{D} m{m} g{g} wg{workgroups} {wide}")
+    check_close(out, ref, f"fused append D{D} m{m} g{g} wg{workgroups} {wide} {qk}")
 
 
 def test_step_owner_that_does_not_read_its_head():
