@@ -501,6 +501,7 @@ void attention_kernel(AttnParams p) {
   const int g = blockIdx.x;
 
   int b, r, j, nb, L, k0, k1;
+  const bool single = !p.plan && p.n_blocks == 1 && p.B == 1 && p.n_groups == 1;
   if (p.plan) {  // the step's plan, written by the step's first attention launch
     const RunItem item = reinterpret_cast<const RunItem*>(p.plan)[g];
     if (item.z >= 0)
@@ -514,6 +515,14 @@ void attention_kernel(AttnParams p) {
     L = item.L;
     k0 = item.k0;
     k1 = item.k1;
+  } else if (single) {
+    // One workgroup for one short unit: its run is the whole sequence.  The
+    // first tiles are requested for the longest allowed length before the
+    // length itself arrives; the length is read below.
+    b = r = j = k0 = 0;
+    nb = 1;
+    L = p.max_len;
+    k1 = tiles_of(L);
   } else {
     if (wave == 0) schedule_wave0(p, sm.sc, g);
     __syncthreads();
@@ -583,8 +592,17 @@ void attention_kernel(AttnParams p) {
 #pragma unroll
   for (int db = 0; db < DB; ++db) st.acc[db] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+  if (it < k1) load_tile<D, QK_VALU>(ta, kbase, vbase, it * kTile, col, grp);
+  if (single) {  // the actual length (the tile above may go unused)
+    L = attended_len(p, 0);
+    k1 = tiles_of(L);
+    if (L == 0) {
+      for (int i = threadIdx.x; i < p.h * D4; i += NT)
+        store_out4<D>(p, 0, i * 4, f32x4{0.f, 0.f, 0.f, 0.f});
+      return;
+    }
+  }
   const bool has_tiles = it < k1;
-  if (has_tiles) load_tile<D, QK_VALU>(ta, kbase, vbase, it * kTile, col, grp);
   float* const s_wave = sm.s_lds + (QK_VALU ? wave * 16 * kTile : 0);
 
   // Fused append of the owning layer (Section 2.4): the last run of each
