@@ -168,3 +168,15 @@ def test_layout_reference_matches_binding_packer():
     for _ in range(100):
         kv, b, t, d = rng.integers(n_kv), rng.integers(B), rng.integers(S), rng.integers(D)
         assert packed.reshape(-1)[layout_ref.v_index(kv, b, t, d, B, S, D)] == rows[kv, b, t, d]
+
+
+def test_binding_fails_loudly_without_the_library(tmp_path):
+    """No fallback: with the HIP library absent the binding raises on first use."""
+    import subprocess
+    import sys
+    code = ("import paper_2406_09297_amd as m\n"
+            "try:\n    m.lib()\nexcept ImportError as e:\n    print('raised', e)\n")
+    env = dict(os.environ, MLKV_LIBRARY=str(tmp_path / "absent.so"))
+    r = subprocess.run([sys.executable, "-c", code], env=env, capture_output=True, text=True,
+                       cwd=os.path.dirname(os.path.dirname(os.path.abspath(__file__))), timeout=120)
+    assert "raised" in r.stdout and "no fallback" in r.stdout, r.stdout + r.stderr

@@ -371,3 +371,68 @@ def test_step_owner_that_does_not_read_its_head():
     ref, k_ref, v_ref = _oracle_step(dw)
     assert np.array_equal(k_gpu, k_ref) and np.array_equal(v_gpu, v_ref), "cache differs"
     check_close(out, ref, "general map")
+
+
+# ------------------------------------------------------------ edge cases --
+
+def test_step_bf16_output_is_the_rounded_fp32_step():
+    """decode_step in bf16 output mode returns the RNE rounding of its fp32
+    output (the append is idempotent, so the step can run twice)."""
+    w = small("mlkv4_b128_ragged", B=6, ctx=700)
+    dw = DeviceWorkload(w)
+    say("step bf16 output")
+    out32 = _run_step(dw, torch.float32)
+    out16 = _run_step(dw, torch.bfloat16)
+    assert np.array_equal(mlkv.bf16_bits(out16), synth.f32_to_bf16(out32.cpu().numpy()))
+
+
+def test_step_sequence_with_nothing_cached_before_nothing_to_attend():
+    """A context of -1 (no token, nothing to append: L = 0) gives zero output
+    in every layer and leaves the cache untouched; the other sequences of the
+    batch are unaffected."""
+    w = synth.Workload("neg_ctx", l=4, h=12, m=2, g=1, D=64, B=3, ctx=80, seed=21)
+    dw = _with_contexts(DeviceWorkload(w), [-1, 5, 80])
+    say("step with a -1 context")
+    out = _run_step(dw).cpu().numpy()
+    k_gpu, v_gpu = dw.read_cache()
+    ref, k_ref, v_ref = _oracle_step(dw)
+    assert np.array_equal(k_gpu, k_ref) and np.array_equal(v_gpu, v_ref), "cache differs"
+    assert np.all(out[:, 0] == 0)
+    check_close(out, ref, "step with -1 context")
+
+
+def test_lengths_above_the_hint_are_truncated_to_it():
+    """max_len_hint bounds the attended positions: a sequence longer than the
+    hint attends to its first max_len_hint positions."""
+    w = _sweep_workload(64, 2, 1, [50, 300, 150], h=12, l=2)
+    dw = DeviceWorkload(w)
+    lens = np.array([50, 300, 150], np.int32)
+    hint = 100
+    say("lengths truncated by max_len_hint")
+    out = torch.empty((w.B, w.h, w.D), dtype=torch.float32, device="cuda")
+    mlkv.decode_attention(1, dw.q[1], dw.cache, dw.map, torch.from_numpy(lens).cuda(), out,
+                          max_len_hint=hint, ws=dw.ws)
+    torch.cuda.synchronize()
+    ref = oracle.decode_attention(1, dw.host["q"][1], dw.host["k_cache"], dw.host["v_cache"],
+                                  dw.kv_of, np.minimum(lens, hint))
+    check_close(out.cpu().numpy(), ref, "hint truncation")
+
+
+def test_length_check_rejects_out_of_range_lengths(monkeypatch):
+    """MLKV_CHECK=1 reads the device lengths back and rejects any above the
+    capacity before launching anything."""
+    w = _sweep_workload(64, 2, 1, [10, 20], h=12, l=2)
+    dw = DeviceWorkload(w)
+    monkeypatch.setenv("MLKV_CHECK", "1")
+    out = torch.zeros((w.B, w.h, w.D), dtype=torch.float32, device="cuda")
+    say("MLKV_CHECK rejects a length above capacity")
+    bad = torch.tensor([10, dw.S + 1], dtype=torch.int32, device="cuda")
+    with pytest.raises(mlkv.MLKVError, match="MLKV_ERR_CAPACITY"):
+        mlkv.decode_attention(0, dw.q[0], dw.cache, dw.map, bad, out, ws=dw.ws)
+    with pytest.raises(mlkv.MLKVError, match="MLKV_ERR_CAPACITY"):
+        mlkv.decode_step(dw.q, dw.k_new, dw.v_new, dw.cache, dw.map,
+                         torch.tensor([3, dw.S], dtype=torch.int32, device="cuda"),
+                         torch.empty((w.l, w.B, w.h, w.D), dtype=torch.float32, device="cuda"),
+                         ws=dw.ws)
+    torch.cuda.synchronize()
+    assert torch.count_nonzero(out) == 0  # nothing ran
