@@ -171,8 +171,9 @@ mlkv_status mlkv_cache_append(int layer, const mlkv_map* map, const mlkv_cache* 
  * Every query head mapped to one KV head is served from a single pass over
  * that head's cache rows.  The tiles of all sequences are shared equally by
  * the workgroups (ragged batches stay balanced); a sequence spread over
- * several workgroups is merged by a second kernel in a fixed order, so
- * results are bitwise reproducible.
+ * several workgroups is merged in a fixed order, by the last of those
+ * workgroups to finish when their partial results fit its staging area, else
+ * by a second kernel, so results are bitwise reproducible.
  */
 mlkv_status mlkv_decode_attention(int layer, const void* q, const mlkv_cache* cache,
                                   const mlkv_map* map, const int32_t* seq_lens, void* out,
@@ -208,8 +209,12 @@ mlkv_status mlkv_decode_step(const void* q_all, const void* k_new_all, const voi
  * most 16 tiles); `max_parts` bounds the workgroups covering one sequence.
  * Environment overrides, read on every call (tests and tuning):
  *   MLKV_WORKGROUPS=n   workgroup budget n instead of the device's;
- *   MLKV_COMBINE=fused  the last run of each unit merges its runs in place
- *                       when they fit the kernel's staging area;
+ *   MLKV_COMBINE=kernel always merge split runs with the separate merge
+ *                       kernel (by default the last run of each unit merges
+ *                       them in place when they fit the kernel's staging
+ *                       area without reducing the workgroup count);
+ *   MLKV_COMBINE=fused  merge in place also when that costs up to half of
+ *                       the workgroups;
  *   MLKV_WIDE=1         one run per unit on a wider workgroup (no partials,
  *                       no merge kernel);
  *   MLKV_QK=valu        q.K as bf16 dot products on the vector ALUs instead

@@ -108,6 +108,20 @@ __device__ __forceinline__ float load_device(float* p) {
 }
 __device__ __forceinline__ void wait_stores_complete() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
+// 16-byte device-scope (sc1) accesses through a buffer resource over `bytes`
+// bytes at `base` (offsets are 32-bit; out-of-range accesses are dropped).
+constexpr int kCpolDevice = 16;  // sc1: coherent across XCDs
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t device_rsrc(float* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(base, 0, bytes, 0x00020000);
+}
+__device__ __forceinline__ void store4_device(__amdgpu_buffer_rsrc_t r, uint32_t off, f32x4 v) {
+  typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r, off, 0, kCpolDevice);
+}
+__device__ __forceinline__ f32x4 load4_device(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kCpolDevice));
+}
+
 __device__ __forceinline__ uint16_t f32_to_bf16_bits(float f) {
   return __builtin_bit_cast(uint16_t, static_cast<__bf16>(f));
 }
@@ -317,14 +331,6 @@ __device__ __forceinline__ void process_tile(WaveState<D>& st, Tile<D>& t, const
   st.den = mfma_bf16(as_bf16(ones), pf, st.den);
 #pragma unroll
   for (int db = 0; db < DB; ++db) st.acc[db] = mfma_bf16(as_bf16(t.v[db]), pf, st.acc[db]);
-}
-
-template <int D>
-__device__ __forceinline__ void store_out(const AttnParams& p, size_t row, int d, float val) {
-  if (p.out_bf16)
-    static_cast<uint16_t*>(p.out)[row * D + d] = f32_to_bf16_bits(val);
-  else
-    static_cast<float*>(p.out)[row * D + d] = val;
 }
 
 // Four consecutive channels d..d+3 of output row `row` (d a multiple of 4).
@@ -674,6 +680,11 @@ void attention_kernel(AttnParams p) {
   const size_t unit = static_cast<size_t>(b) * p.n_groups + r;
   const size_t slot = unit * p.max_parts + j;
   const bool fuse = nb > 1 && p.fused && nb * GD <= kStageFloats && nb * p.G * 2 <= kStageMl;
+  // The unit's partial outputs ([run][head][channel], nb * GD floats), for
+  // the in-place merge.
+  float* const unit_acc = fuse ? p.part_acc + unit * p.max_parts * GD : p.part_acc;
+  const __amdgpu_buffer_rsrc_t rsrc_acc =
+      device_rsrc(unit_acc, fuse ? static_cast<uint32_t>(nb * GD * 4) : 0u);
   // Each thread merges four channels of one head over the waves.
   for (int idx = threadIdx.x; idx < p.G * D4; idx += NT) {
     const int hh = idx / D4;
@@ -698,8 +709,7 @@ void attention_kernel(AttnParams p) {
     if (nb == 1) {
       store_out4<D>(p, out_row0 + hh, d, wsum > 0.f ? o / wsum : f32x4{0.f, 0.f, 0.f, 0.f});
     } else if (fuse) {
-#pragma unroll
-      for (int e = 0; e < 4; ++e) store_device(&p.part_acc[slot * GD + hh * D + d + e], o[e]);
+      store4_device(rsrc_acc, (j * GD + hh * D + d) * 4, o);
       if (d == 0) {
         store_device(&p.part_ml[(slot * p.G + hh) * 2 + 0], M);
         store_device(&p.part_ml[(slot * p.G + hh) * 2 + 1], wsum);
@@ -727,38 +737,51 @@ void attention_kernel(AttnParams p) {
   // ([run][head][channel]); stage them with all loads in flight, then merge
   // in ascending run order (deterministic).
   {
-    const int n_acc = nb * GD;
-    float* src = p.part_acc + unit * p.max_parts * GD;
-    for (int j0 = threadIdx.x; j0 < n_acc; j0 += NT * 8) {
-      float v[8];
+    // One round trip: every 16-byte piece of the unit's partials is in
+    // flight at once (kStageFloats / 4 / NT pieces per thread at most).
+    constexpr int kPieces = (kStageFloats / 4 + NT - 1) / NT;
+    const int n4 = nb * GD / 4;
+    f32x4 v[kPieces];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int jj = j0 + u * NT;
-        v[u] = jj < n_acc ? load_device(src + jj) : 0.f;
-      }
-#pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int jj = j0 + u * NT;
-        if (jj < n_acc) sm.stage[jj] = v[u];
-      }
+    for (int u = 0; u < kPieces; ++u) {
+      const int i4 = threadIdx.x + u * NT;
+      v[u] = i4 < n4 ? load4_device(rsrc_acc, i4 * 16) : f32x4{0.f, 0.f, 0.f, 0.f};
     }
+    const int n_ml = nb * p.G * 2;
     float* src_ml = p.part_ml + unit * p.max_parts * p.G * 2;
-    for (int jj = threadIdx.x; jj < nb * p.G * 2; jj += NT) sm.stage_ml[jj] = load_device(src_ml + jj);
+    float ml[(kStageMl + NT - 1) / NT];
+#pragma unroll
+    for (int u = 0; u < (kStageMl + NT - 1) / NT; ++u) {
+      const int jj = threadIdx.x + u * NT;
+      ml[u] = jj < n_ml ? load_device(src_ml + jj) : 0.f;
+    }
+#pragma unroll
+    for (int u = 0; u < kPieces; ++u) {
+      const int i4 = threadIdx.x + u * NT;
+      if (i4 < n4) *reinterpret_cast<f32x4*>(&sm.stage[i4 * 4]) = v[u];
+    }
+#pragma unroll
+    for (int u = 0; u < (kStageMl + NT - 1) / NT; ++u) {
+      const int jj = threadIdx.x + u * NT;
+      if (jj < n_ml) sm.stage_ml[jj] = ml[u];
+    }
   }
   __syncthreads();
-  for (int idx = threadIdx.x; idx < GD; idx += NT) {
-    const int hh = idx / D;
+  for (int idx = threadIdx.x; idx < p.G * D4; idx += NT) {
+    const int hh = idx / D4;
+    const int d = (idx - hh * D4) * 4;
     float M = -INFINITY;
     for (int s2 = 0; s2 < nb; ++s2) M = fmaxf(M, sm.stage_ml[(s2 * p.G + hh) * 2]);
-    float den = 0.f, o = 0.f;
+    float den = 0.f;
+    f32x4 o = {0.f, 0.f, 0.f, 0.f};
     if (M != -INFINITY) {
       for (int s2 = 0; s2 < nb; ++s2) {
         const float f = fast_exp2(sm.stage_ml[(s2 * p.G + hh) * 2] - M);
         den += f * sm.stage_ml[(s2 * p.G + hh) * 2 + 1];
-        o += f * sm.stage[s2 * GD + idx];
+        o += f * *reinterpret_cast<const f32x4*>(&sm.stage[s2 * GD + hh * D + d]);
       }
     }
-    store_out<D>(p, out_row0 + hh, idx - hh * D, den > 0.f ? o / den : 0.f);
+    store_out4<D>(p, out_row0 + hh, d, den > 0.f ? o / den : f32x4{0.f, 0.f, 0.f, 0.f});
   }
   if (threadIdx.x == 0)  // ready for the next call on this workspace
     __hip_atomic_store(&p.counters[unit], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);

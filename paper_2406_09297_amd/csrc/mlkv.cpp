@@ -152,12 +152,14 @@ long workgroups_for(long resident, long units, long t_max, int min_tiles) {
   return g > units ? g : units;
 }
 
-// With MLKV_COMBINE=fused, runs are merged inside the attention kernel (by
-// the last run of each unit to finish) when every unit's partials fit the
-// kernel's staging area; the run length floor that guarantees it is accepted
-// if it still leaves at least half the resident workgroups busy.  Otherwise
-// (and by default: on MI355X the merge kernel measured as fast or faster) a
-// separate merge kernel runs.
+// Runs of a unit are merged inside the attention kernel (by the last run of
+// the unit to finish) when every unit's partials fit the kernel's staging
+// area: the run length floor that guarantees it must leave the workgroup
+// count of the plain plan unchanged (on MI355X the in-place merge then beats
+// the separate merge kernel by about a tenth of a ragged 128-sequence step).
+// Otherwise a separate merge kernel runs.  MLKV_COMBINE=kernel forces the
+// merge kernel; MLKV_COMBINE=fused also accepts a floor that keeps at least
+// half of the workgroups.
 Plan plan(const mlkv_map* map, int layer, int batch, int max_len, int head_dim) {
   Plan pl{};
   pl.max_tiles = tiles_of(max_len < 1 ? 1 : max_len);
@@ -178,13 +180,17 @@ Plan plan(const mlkv_map* map, int layer, int batch, int max_len, int head_dim) 
   pl.min_tiles = kMinTiles;
   pl.fused = 0;
   const long cap_parts = mlkv::stage_floats() / (static_cast<long>(map->group[layer]) * head_dim);
-  const char* comb = std::getenv("MLKV_COMBINE");  // "fused": merge in place where it fits
-  const bool allow_fused = comb && std::strcmp(comb, "fused") == 0;
-  if (allow_fused && cap_parts >= 2) {
+  const char* comb = std::getenv("MLKV_COMBINE");
+  const bool force_kernel = comb && std::strcmp(comb, "kernel") == 0;
+  const bool force_fused = comb && std::strcmp(comb, "fused") == 0;
+  if (!force_kernel && cap_parts >= 2) {
     long mt = (pl.max_tiles + cap_parts - 1) / cap_parts;
     mt = mt > kMinTiles ? mt : kMinTiles;
     const long g = workgroups_for(resident, units, t_max, static_cast<int>(mt));
-    if (2 * g >= resident || g >= units * ((pl.max_tiles + mt - 1) / mt)) {
+    const long g_plain = workgroups_for(resident, units, t_max, kMinTiles);
+    const bool accept = force_fused ? 2 * g >= resident || g >= units * ((pl.max_tiles + mt - 1) / mt)
+                                    : g >= g_plain;
+    if (accept) {
       pl.min_tiles = static_cast<int>(mt);
       pl.fused = 1;
     }

@@ -36,8 +36,9 @@ def small(name, **kw):
 @contextlib.contextmanager
 def plan_env(workgroups="", merge="", wide="", qk=""):
     """Launch-plan overrides read by the library on every call:
-    MLKV_WORKGROUPS (workgroup budget), MLKV_COMBINE=fused (merge runs inside
-    the attention kernel), MLKV_WIDE=0/1 (one run per unit on a wide
+    MLKV_WORKGROUPS (workgroup budget), MLKV_COMBINE=kernel/fused (merge
+    split runs in a separate kernel / in place even at a cost in
+    workgroups), MLKV_WIDE=0/1 (one run per unit on a wide
     workgroup: off / forced), MLKV_QK=valu (q.K on the vector ALUs)."""
     names = {"MLKV_WORKGROUPS": workgroups, "MLKV_COMBINE": merge, "MLKV_WIDE": wide,
              "MLKV_QK": qk}
@@ -122,7 +123,8 @@ def test_length_sweep_across_tile_boundaries(D, m, g):
     lens = np.array(LEN_SWEEP, dtype=np.int32)
     lens_d = torch.from_numpy(lens).cuda()
     for wg, comb, wide, qk in (("", "", "", ""), ("3", "", "", ""), ("40", "", "", ""),
-                               ("", "fused", "", ""), ("40", "fused", "", ""), ("", "", "1", ""),
+                               ("", "fused", "", ""), ("40", "fused", "", ""),
+                               ("", "kernel", "", ""), ("40", "kernel", "", ""), ("", "", "1", ""),
                                ("", "", "0", ""), ("", "", "", "valu"), ("40", "", "", "valu")):
         with plan_env(wg, comb, wide, qk):
             for n in (0, w.l - 1):
@@ -144,7 +146,8 @@ def test_split_count_invariance_and_determinism():
     lens_d = torch.from_numpy(dw.host["ctx"]).cuda()
     outs = {}
     for wg, comb, wide in (("1", "", ""), ("7", "", ""), ("64", "", ""), ("300", "", ""),
-                           ("", "", ""), ("", "fused", ""), ("300", "fused", ""), ("", "", "1")):
+                           ("", "", ""), ("", "fused", ""), ("300", "fused", ""),
+                           ("", "kernel", ""), ("300", "kernel", ""), ("", "", "1")):
         with plan_env(wg, comb, wide):
             say(f"workgroup invariance workgroups={wg or 'auto'} merge={comb or 'kernel'} "
                 f"wide={wide or 'auto'}")
@@ -294,22 +297,24 @@ def test_map_sweep_full_size(mg):
     check_close(out, ref, f"step {w.name}")
 
 
-def test_full_size_step_with_in_place_merge():
-    """The ragged 128-sequence step with runs merged inside the attention kernel
-    (MLKV_COMBINE=fused) gives the same cache and outputs as the oracle."""
+@pytest.mark.parametrize("merge", ["", "kernel"])
+def test_full_size_step_twice_on_one_workspace(merge):
+    """The ragged 128-sequence step, run twice on one workspace (the in-place
+    merge's arrival counters must return to zero), with the default merge
+    (in place where it fits) and with the separate merge kernel."""
     w = synth.get_workload("mlkv4_b128_ragged")
-    with plan_env(merge="fused"):
-        say("full step in-place merge: uploading")
+    with plan_env(merge=merge):
+        say(f"full step twice merge={merge or 'auto'}: uploading")
         dw = DeviceWorkload(w)
-        say("full step in-place merge: running (twice: counters must reset)")
+        say("full step twice: running")
         _run_step(dw)
-        dw2 = DeviceWorkload(w)  # fresh cache, same workspace contract
+        dw2 = DeviceWorkload(w)  # fresh cache, same workspace
         dw2.ws = dw.ws
         out = _run_step(dw2).cpu().numpy()
     k_gpu, v_gpu = dw2.read_cache()
     ref, k_ref, v_ref = _oracle_step(dw2)
     assert np.array_equal(k_gpu, k_ref) and np.array_equal(v_gpu, v_ref), "cache differs"
-    check_close(out, ref, "step in-place merge")
+    check_close(out, ref, f"step twice merge={merge or 'auto'}")
 
 
 # ---------------------------------------------------- fused append in step --
