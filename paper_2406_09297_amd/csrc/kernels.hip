@@ -9,9 +9,15 @@
 //                     a workgroup takes one run and serves every query head
 //                     mapped to the KV head from one pass over it.  A unit of
 //                     one run is finished in place; otherwise each run leaves
-//                     a partial (max, denominator, output)
+//                     a partial (max, denominator, output), merged by the
+//                     unit's last run to finish when the partials fit its
+//                     staging area.  In a decode step the owning layer's
+//                     launch also appends the newest token.
 //   combine_kernel    log-sum-exp merge of a unit's partials, fixed order
+//                     (when they were not merged in place)
 //   fill_kernel       zero fill of a workspace
+//   (QK_VALU: a variant computing q.K with bf16 dot2 on the vector ALUs,
+//   kept to compare with the matrix-core path.)
 //
 // Math (paper Section 2.1 Eqs. 1-3; MLKV head map Section 3 Eqs. 13-17):
 //   o = sum_t softmax_t(q.k_t / sqrt(D)) v_t.  Scores are kept in the log2
@@ -124,10 +130,6 @@ __device__ __forceinline__ f32x4 load4_device(__amdgpu_buffer_rsrc_t r, uint32_t
 
 __device__ __forceinline__ uint16_t f32_to_bf16_bits(float f) {
   return __builtin_bit_cast(uint16_t, static_cast<__bf16>(f));
-}
-
-__device__ __forceinline__ float bf16_bits_to_f32(uint16_t u) {
-  return __builtin_bit_cast(float, static_cast<uint32_t>(u) << 16);
 }
 
 // Attended length of sequence b: lens[b] + len_offset, clamped to [0, max_len]
@@ -344,18 +346,6 @@ __device__ __forceinline__ void store_out4(const AttnParams& p, size_t row, int 
   } else {
     *reinterpret_cast<f32x4*>(static_cast<float*>(p.out) + row * D + d) = v;
   }
-}
-
-__device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) v = fmaxf(v, __shfl_xor(v, off));
-  return v;
-}
-
-__device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
-  return v;
 }
 
 __device__ __forceinline__ int wave_sum_int(int v) {
