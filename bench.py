@@ -217,8 +217,10 @@ def main():
         prof_ms += e2.elapsed_time(e3)
         done += n
     n_launch, tot_ms, min_ms, max_ms = mlkv.profile_read()
+    durations = mlkv.profile_durations(n_launch)
     mlkv.profile_disable()
     ms_step_profiled = prof_ms / args.steps
+    p10, p50, p90 = (float(np.percentile(durations, q)) for q in (10, 50, 90))
     avg = tot_ms * 1e-3 / n_launch
     attn_bytes = float(np.mean([x["kv"] + x["q"] + x["out"] for x in per_layer]))
     achieved = attn_bytes / avg / 1e9
@@ -275,6 +277,9 @@ def main():
                      "avg_launch_us": round(avg * 1e6, 3),
                      "min_launch_us": round(min_ms * 1e3, 3),
                      "max_launch_us": round(max_ms * 1e3, 3),
+                     "p10_p50_p90_launch_us": [round(p10 * 1e3, 3), round(p50 * 1e3, 3),
+                                               round(p90 * 1e3, 3)],
+
                      "launches": n_launch,
                      "bytes_per_launch": int(attn_bytes),
                      "cache_state": "natural layer order, back-to-back steps",

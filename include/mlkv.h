@@ -239,6 +239,11 @@ mlkv_status mlkv_profile_enable(int max_launches);
 /* Synchronizes on the recorded events and reports the number of timed
  * launches and the sum, minimum and maximum of their durations (ms). */
 mlkv_status mlkv_profile_read(int* launches, double* total_ms, double* min_ms, double* max_ms);
+/* Synchronizes on the recorded events and writes the duration (ms) of each
+ * timed launch, in launch order, to ms[0 .. min(launches, capacity) - 1];
+ * *count receives that number.  Errors: MLKV_ERR_INVALID_ARG (count NULL, or
+ * ms NULL with capacity > 0), MLKV_ERR_HIP. */
+mlkv_status mlkv_profile_durations(double* ms, int capacity, int* count);
 /* Stops timing and destroys the events. */
 void mlkv_profile_disable(void);
 

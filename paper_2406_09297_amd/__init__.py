@@ -37,7 +37,7 @@ EXPORTS = [
     "mlkv_map_layer_owned_count", "mlkv_map_layer_owned_begin", "mlkv_cache_bytes",
     "mlkv_workspace_bytes", "mlkv_cache_append", "mlkv_decode_attention", "mlkv_decode_step",
     "mlkv_plan", "mlkv_workspace_init", "mlkv_profile_enable", "mlkv_profile_read",
-    "mlkv_profile_disable",
+    "mlkv_profile_durations", "mlkv_profile_disable",
 ]
 
 
@@ -89,6 +89,7 @@ def lib():
             "mlkv_workspace_init": ([P, Z, P], S),
             "mlkv_profile_enable": ([I], S),
             "mlkv_profile_read": ([ctypes.POINTER(I)] + [ctypes.POINTER(ctypes.c_double)] * 3, S),
+            "mlkv_profile_durations": ([ctypes.POINTER(ctypes.c_double), I, ctypes.POINTER(I)], S),
             "mlkv_profile_disable": ([], None),
         }
         for name, (args, res) in sig.items():
@@ -325,6 +326,14 @@ def profile_read():
     _check(lib().mlkv_profile_read(ctypes.byref(n), ctypes.byref(tot), ctypes.byref(lo),
                                    ctypes.byref(hi)))
     return n.value, tot.value, lo.value, hi.value
+
+
+def profile_durations(capacity: int) -> np.ndarray:
+    """Per-launch durations (ms) of the timed attention kernels, in order."""
+    buf = (ctypes.c_double * max(capacity, 1))()
+    n = ctypes.c_int()
+    _check(lib().mlkv_profile_durations(buf, capacity, ctypes.byref(n)))
+    return np.array(buf[:n.value], dtype=np.float64)
 
 
 def profile_disable():

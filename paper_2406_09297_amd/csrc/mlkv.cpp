@@ -684,6 +684,21 @@ mlkv_status mlkv_profile_read(int* launches, double* total_ms, double* min_ms, d
   return ok();
 }
 
+mlkv_status mlkv_profile_durations(double* ms, int capacity, int* count) {
+  if (!count || (capacity > 0 && !ms)) return fail(MLKV_ERR_INVALID_ARG, "bad output arguments");
+  Profile& prof = g_profile;
+  const int n = prof.used < capacity ? prof.used : (capacity > 0 ? capacity : 0);
+  for (int i = 0; i < n; ++i) {
+    float t = 0.f;
+    if (hipEventSynchronize(prof.stop[i]) != hipSuccess ||
+        hipEventElapsedTime(&t, prof.start[i], prof.stop[i]) != hipSuccess)
+      return fail(MLKV_ERR_HIP, "reading profile events failed");
+    ms[i] = t;
+  }
+  *count = n;
+  return ok();
+}
+
 void mlkv_profile_disable(void) {
   Profile& prof = g_profile;
   for (hipEvent_t e : prof.start)
