@@ -55,6 +55,16 @@ def _load():
         lib.oracle_append.restype = I
         lib.oracle_decode_step.argtypes = [I, I, I, I, I, I, P, P, P, P, P, P, P, P, P, P]
         lib.oracle_decode_step.restype = None
+        D_ = ctypes.c_double
+        lib.oracle_bf16_from_double.argtypes = [D_]
+        lib.oracle_bf16_from_double.restype = ctypes.c_uint16
+        lib.oracle_rope.argtypes = [P, I, I, D_, L, P]
+        lib.oracle_rope.restype = None
+        lib.oracle_rope_f64.argtypes = [P, I, I, D_, D_, P]
+        lib.oracle_rope_f64.restype = None
+        lib.oracle_decode_step_rope.argtypes = [I, I, I, I, I, I, I, D_, P, P, P, P, P, P, P, P,
+                                                P, P, P, P]
+        lib.oracle_decode_step_rope.restype = None
         _lib = lib
     return _lib
 
@@ -158,6 +168,52 @@ def decode_step(q_all, k_cache, v_cache, k_new, v_new, kv_of, owner_of, ctx):
                                _p(_bf16(q_all)), _p(k_cache), _p(v_cache),
                                _p(_bf16(k_new, (B, n_kv, D))), _p(_bf16(v_new, (B, n_kv, D))),
                                _p(_i32(ctx)), _p(scratch), _p(out))
+    return out
+
+
+def bf16_from_double(x: float) -> int:
+    """Nearest bf16 (ties to even) of a double, as its 16-bit pattern."""
+    return int(_load().oracle_bf16_from_double(float(x)))
+
+
+def rope(x, pos: int, rd: int, base: float = 10000.0) -> np.ndarray:
+    """GPT-NeoX rotary embedding of one head vector (bf16 bits in and out):
+    the first rd channels in rotate-half pairs (j, j + rd/2), angle
+    pos * base^(-2j/rd); computed in double, rounded to bf16 (the models of
+    Section 4.2 use the GPT-NeoX architecture)."""
+    x = _bf16(x)
+    D = x.shape[-1]
+    assert x.ndim == 1 and rd % 2 == 0 and 0 <= rd <= D
+    y = np.empty(D, dtype=np.uint16)
+    _load().oracle_rope(_p(x), D, rd, float(base), int(pos), _p(y))
+    return y
+
+
+def rope_f64(x, pos: float, rd: int, base: float = 10000.0) -> np.ndarray:
+    """The same rotation on a float64 vector, unrounded."""
+    x = np.ascontiguousarray(x, dtype=np.float64)
+    y = np.empty_like(x)
+    _load().oracle_rope_f64(_p(x), x.shape[-1], rd, float(base), float(pos), _p(y))
+    return y
+
+
+def decode_step_rope(q_all, k_cache, v_cache, k_new, v_new, kv_of, owner_of, ctx, rd: int,
+                     base: float = 10000.0):
+    """decode_step with the newest token's queries and keys rotated at
+    position ctx[b] (rotary embedding, rd channels)."""
+    l, B, h, D = q_all.shape
+    n_kv, B2, S, D2 = k_cache.shape
+    assert (B2, D2) == (B, D) and rd % 2 == 0 and 0 <= rd <= D
+    assert k_cache.flags.c_contiguous and v_cache.flags.c_contiguous
+    out = np.empty((l, B, h, D), dtype=np.float64)
+    q_rot = np.empty((l, B, h, D), dtype=np.uint16)
+    k_rot = np.empty((B, n_kv, D), dtype=np.uint16)
+    scratch = np.empty(B, dtype=np.int32)
+    _load().oracle_decode_step_rope(l, B, h, n_kv, S, D, rd, float(base), _p(_i32(kv_of)),
+                                    _p(_i32(owner_of)), _p(_bf16(q_all)), _p(k_cache),
+                                    _p(v_cache), _p(_bf16(k_new, (B, n_kv, D))),
+                                    _p(_bf16(v_new, (B, n_kv, D))), _p(_i32(ctx)), _p(q_rot),
+                                    _p(k_rot), _p(scratch), _p(out))
     return out
 
 

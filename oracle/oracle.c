@@ -20,6 +20,9 @@
  *   KV caching ............. Section 2.4
  *   MLKV sharing ........... Section 3, Eqs. (13)-(17); the shared head comes
  *                            from the bottom layer of its group (Figure 2)
+ *   rotary embedding ....... the GPT-NeoX architecture of the Pythia models
+ *                            (Section 4.2): rotate-half pairs of the first
+ *                            rd channels, angle pos * base^(-2j/rd)
  *
  * Readings where the paper is silent (each is listed in the design notes):
  *   - K/V of a shared head are produced once, by the lowest layer of its
@@ -33,7 +36,10 @@
  * independent brute-force loop and torch SDPA; one head per layer == MQA;
  * L = 1 gives v; identical keys give mean(V); weights sum to 1; shift and
  * permutation invariance; needle tokens; Table 2 head counts; Table 1
- * cache-size ratios.
+ * cache-size ratios.  Rotary (tests/test_oracle_rope.py): identity at
+ * position 0, a four-channel closed form, pair lengths kept, scores that
+ * depend only on the position difference, bf16 rounding against an
+ * enumeration of neighbouring bf16 values.
  */
 #include <math.h>
 #include <stdint.h>
@@ -192,4 +198,81 @@ void oracle_decode_step(int l, int B, int h, int n_kv, int S, int D, const int32
     oracle_decode_attention(n, B, h, n_kv, S, D, kv_of, q_all + (size_t)n * B * h * D, Kc, Vc,
                             lens_scratch, out_all + (size_t)n * B * h * D);
   }
+}
+
+/* ------------------------------------------------------------------------ */
+/* Rotary position embedding of the GPT-NeoX architecture that the paper's   */
+/* Pythia models use (Section 4.2).                                          */
+/* ------------------------------------------------------------------------ */
+
+/* Nearest bf16 (ties to even) of a double, as bits, by rounding the
+ * significand to 8 bits directly (no intermediate float rounding). */
+uint16_t oracle_bf16_from_double(double x) {
+  if (x == 0.0) return signbit(x) ? 0x8000u : 0u;
+  int e;
+  const double m = frexp(x, &e);          /* x = m * 2^e, 0.5 <= |m| < 1 */
+  const double r = nearbyint(m * 256.0);  /* 8 significant bits, ties to even */
+  const float f = (float)ldexp(r, e - 8);  /* exact: r has at most 9 bits */
+  uint32_t u;
+  memcpy(&u, &f, sizeof u);
+  return (uint16_t)(u >> 16);
+}
+
+/*
+ * One head vector x[0..D) at position pos.  The first rd channels (rd even)
+ * form rd/2 pairs (j, j + rd/2); pair j turns by the angle
+ *   theta_j = pos * base^(-2j/rd),
+ *   y_j        = x_j cos(theta_j) - x_{j+rd/2} sin(theta_j)
+ *   y_{j+rd/2} = x_{j+rd/2} cos(theta_j) + x_j sin(theta_j).
+ * Channels rd..D-1 are copied.  Arithmetic in double, stored as bf16.
+ */
+void oracle_rope(const uint16_t* x, int D, int rd, double base, long pos, uint16_t* y) {
+  const int half = rd / 2;
+  for (int d = rd; d < D; ++d) y[d] = x[d];
+  for (int j = 0; j < half; ++j) {
+    const double theta = (double)pos * pow(base, -2.0 * j / rd);
+    const double c = cos(theta), s = sin(theta);
+    const double a = bf16_value(x[j]), b = bf16_value(x[j + half]);
+    y[j] = oracle_bf16_from_double(a * c - b * s);
+    y[j + half] = oracle_bf16_from_double(b * c + a * s);
+  }
+}
+
+/* The double-precision rotation itself (for the invariance pins). */
+void oracle_rope_f64(const double* x, int D, int rd, double base, double pos, double* y) {
+  const int half = rd / 2;
+  for (int d = rd; d < D; ++d) y[d] = x[d];
+  for (int j = 0; j < half; ++j) {
+    const double theta = pos * pow(base, -2.0 * j / rd);
+    const double c = cos(theta), s = sin(theta);
+    y[j] = x[j] * c - x[j + half] * s;
+    y[j + half] = x[j + half] * c + x[j] * s;
+  }
+}
+
+/*
+ * A decode step with rotary embedding: the newest token sits at position
+ * ctx[b]; its keys (for every KV head) and its queries (every layer and head)
+ * are rotated at that position, then the step runs as above.  q_rot and
+ * k_rot are caller scratch of the sizes of q_all and k_new.
+ */
+void oracle_decode_step_rope(int l, int B, int h, int n_kv, int S, int D, int rd, double base,
+                             const int32_t* kv_of, const int32_t* owner_of,
+                             const uint16_t* q_all, uint16_t* Kc, uint16_t* Vc,
+                             const uint16_t* k_new, const uint16_t* v_new, const int32_t* ctx,
+                             uint16_t* q_rot, uint16_t* k_rot, int32_t* lens_scratch,
+                             double* out_all) {
+  for (int n = 0; n < l; ++n)
+    for (int b = 0; b < B; ++b)
+      for (int i = 0; i < h; ++i) {
+        const size_t off = (((size_t)n * B + b) * h + i) * D;
+        oracle_rope(q_all + off, D, rd, base, ctx[b], q_rot + off);
+      }
+  for (int b = 0; b < B; ++b)
+    for (int kv = 0; kv < n_kv; ++kv) {
+      const size_t off = ((size_t)b * n_kv + kv) * D;
+      oracle_rope(k_new + off, D, rd, base, ctx[b], k_rot + off);
+    }
+  oracle_decode_step(l, B, h, n_kv, S, D, kv_of, owner_of, q_rot, Kc, Vc, k_rot, v_new, ctx,
+                     lens_scratch, out_all);
 }

@@ -10,6 +10,7 @@ import pytest
 
 import oracle
 import test_oracle as pins
+import test_oracle_rope as rope_pins
 
 SRC = os.path.join(os.path.dirname(oracle.__file__), "oracle.c")
 
@@ -36,6 +37,14 @@ MUTANTS = [
      "    oracle_append(n, B, n_kv, S, D, owner_of, Kc, Vc, k_new, v_new, ctx);"),
     ("value_row_of_first_token", "o[d] += w[t] * bf16_value(V[t * ld + d]);",
      "o[d] += w[t] * bf16_value(V[d]);"),
+    # rotary embedding
+    ("rope_sign", "y[j] = x[j] * c - x[j + half] * s;", "y[j] = x[j] * c + x[j + half] * s;"),
+    ("rope_frequency", "const double theta = pos * pow(base, -2.0 * j / rd);",
+     "const double theta = pos * pow(base, -1.0 * j / rd);"),
+    ("rope_interleaved_pairs", "b = bf16_value(x[j + half]);", "b = bf16_value(x[j ^ 1]);"),
+    ("rope_rounding_truncates", "nearbyint(m * 256.0)", "trunc(m * 256.0)"),
+    ("rope_step_key_position", "oracle_rope(k_new + off, D, rd, base, ctx[b], k_rot + off);",
+     "oracle_rope(k_new + off, D, rd, base, ctx[b] + 1, k_rot + off);"),
 ]
 
 
@@ -58,6 +67,13 @@ def _pin_calls():
         ("append", pins.test_append_writes_only_owned_slots),
         ("mlkv2 ctx0", pins.test_step_mlkv2_empty_context_outputs_owner_values),
         ("non-owner sees new token", pins.test_step_non_owner_layer_sees_token_appended_this_step),
+        ("bf16 rounding", rope_pins.test_bf16_rounding_is_nearest_ties_to_even),
+        ("rope identity", rope_pins.test_position_zero_and_zero_channels_are_identity),
+        ("rope closed form", rope_pins.test_closed_form_of_a_four_channel_rotation),
+        ("rope lengths", rope_pins.test_pairs_keep_their_length),
+        ("rope relative position", rope_pins.test_scores_depend_only_on_the_position_difference),
+        ("rope bf16", rope_pins.test_bf16_rope_is_the_rounded_double_rotation),
+        ("rope step", rope_pins.test_step_with_rope_is_the_step_on_rotated_inputs),
     ]
     return calls
 
