@@ -78,7 +78,7 @@ def step_bytes(w, ctx, kv_count, owned_count, out_bytes=4):
     return per_layer
 
 
-def cpu_baseline(w, inp, kv_of, owner_of, bytes_per_step, budget_s=12.0):
+def cpu_baseline(w, inp, kv_of, owner_of, bytes_per_step, budget_s=12.0, rotary=(0, 1e4)):
     """The oracle, as it stands, on the host cores: whole decode steps on the
     same host inputs, repeated until the time budget is used (at least once)."""
     import oracle
@@ -88,7 +88,12 @@ def cpu_baseline(w, inp, kv_of, owner_of, bytes_per_step, budget_s=12.0):
     while True:
         k, v = inp["k_cache"].copy(), inp["v_cache"].copy()
         ts = time.perf_counter()
-        oracle.decode_step(inp["q"], k, v, inp["k_new"], inp["v_new"], kv_of, owner_of, inp["ctx"])
+        if rotary[0]:
+            oracle.decode_step_rope(inp["q"], k, v, inp["k_new"], inp["v_new"], kv_of, owner_of,
+                                    inp["ctx"], rotary[0], rotary[1])
+        else:
+            oracle.decode_step(inp["q"], k, v, inp["k_new"], inp["v_new"], kv_of, owner_of,
+                               inp["ctx"])
         runs += 1
         if runs == 1:
             spent = time.perf_counter() - ts
@@ -113,6 +118,10 @@ def main():
     ap.add_argument("--no-cold", action="store_true",
                     help="skip timing attention launches after a 1 GiB read evicts the caches")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--rotary-dims", type=int, default=0,
+                    help="rotate the newest token's queries and keys inside the step "
+                         "(GPT-NeoX rotary embedding; Pythia-160M: 16)")
+    ap.add_argument("--rotary-base", type=float, default=10000.0)
     ap.add_argument("--pmc-pass", action="store_true",
                     help="for rocprofv3 --pmc runs: a 256 MiB reference copy, then a few steps")
     args = ap.parse_args()
@@ -161,7 +170,8 @@ def main():
     kv_total = sum(x["kv"] for x in per_layer)
 
     def one_step():
-        mlkv.decode_step(q, kn, vn, cache, mp, ctx, out, max_len_hint=max_len, ws=ws)
+        mlkv.decode_step(q, kn, vn, cache, mp, ctx, out, max_len_hint=max_len, ws=ws,
+                         rotary_dims=args.rotary_dims, rotary_base=args.rotary_base)
 
     if args.pmc_pass:
         # Counter pass: two plain copies of 256 MiB (a device-to-device copy
@@ -269,10 +279,10 @@ def main():
                    "batch": w.B, "ctx": w.ctx if w.ctx is not None else list(w.ctx_range),
                    "ctx_sum": int(inp["ctx"].sum()), "capacity": S,
                    "bytes_per_step": int(step_total), "kv_bytes_per_step": int(kv_total),
-                   "workgroups_layer0": workgroups},
+                   "workgroups_layer0": workgroups, "rotary_dims": args.rotary_dims},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                     "traffic": measured_traffic(w.name),
+                     "traffic": measured_traffic(w.name) if not args.rotary_dims else None,
                      "kernel": "attention_kernel",
                      "avg_launch_us": round(avg * 1e6, 3),
                      "min_launch_us": round(min_ms * 1e3, 3),
@@ -291,7 +301,8 @@ def main():
         import oracle
 
         kv_of, owner_of = oracle.map_uniform(w.l, w.h, w.m, w.g)
-        result["cpu_baseline"] = cpu_baseline(w, inp, kv_of, owner_of, step_total)
+        result["cpu_baseline"] = cpu_baseline(w, inp, kv_of, owner_of, step_total,
+                                              rotary=(args.rotary_dims, args.rotary_base))
     print(json.dumps(result), flush=True)
 
 

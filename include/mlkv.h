@@ -197,6 +197,30 @@ mlkv_status mlkv_decode_step(const void* q_all, const void* k_new_all, const voi
                              int max_len_hint, void* workspace, size_t workspace_bytes,
                              hipStream_t stream);
 
+/*
+ * mlkv_decode_step with the rotary position embedding of the GPT-NeoX
+ * architecture that the paper's Pythia models use (Section 4.2) applied
+ * first to the newest token, IN PLACE: on return q_all (every layer and head)
+ * and k_new_all (every KV head) hold their vectors rotated at position
+ * ctx_lens[b], and the cache holds the rotated keys.  Calling it twice on
+ * the same buffers rotates twice.
+ * Rotation: channel pairs (j, j + rotary_dims/2), j < rotary_dims/2, of each
+ * head vector turn by ctx_lens[b] * rotary_base^(-2j/rotary_dims) radians
+ * (angle, sine, cosine and rotation in double, rounded once to bf16,
+ * nearest even); channels at or past rotary_dims and the values are
+ * unchanged.  Pythia-160M: rotary_dims 16, rotary_base 10000.
+ *   rotary_dims: a multiple of 16 in [0, head_dim] (else
+ *                MLKV_ERR_UNSUPPORTED); 0 is mlkv_decode_step.
+ *   rotary_base: positive and finite (else MLKV_ERR_INVALID_ARG).
+ * Other arguments and errors as mlkv_decode_step; every check is made before
+ * anything is rotated or launched.
+ */
+mlkv_status mlkv_decode_step_rope(void* q_all, void* k_new_all, const void* v_new_all,
+                                  const mlkv_cache* cache, const mlkv_map* map,
+                                  const int32_t* ctx_lens, int rotary_dims, double rotary_base,
+                                  void* out_all, mlkv_out_dtype out_dtype, int max_len_hint,
+                                  void* workspace, size_t workspace_bytes, hipStream_t stream);
+
 /* ----------------------------------------------------------------------- */
 /* Introspection (tests and benchmarks)                                      */
 /* ----------------------------------------------------------------------- */

@@ -198,9 +198,10 @@ def rope_f64(x, pos: float, rd: int, base: float = 10000.0) -> np.ndarray:
 
 
 def decode_step_rope(q_all, k_cache, v_cache, k_new, v_new, kv_of, owner_of, ctx, rd: int,
-                     base: float = 10000.0):
+                     base: float = 10000.0, return_rotated: bool = False):
     """decode_step with the newest token's queries and keys rotated at
-    position ctx[b] (rotary embedding, rd channels)."""
+    position ctx[b] (rotary embedding, rd channels).  return_rotated: also
+    return the rotated queries [l][B][h][D] and keys [B][n_kv][D] (bf16 bits)."""
     l, B, h, D = q_all.shape
     n_kv, B2, S, D2 = k_cache.shape
     assert (B2, D2) == (B, D) and rd % 2 == 0 and 0 <= rd <= D
@@ -214,6 +215,8 @@ def decode_step_rope(q_all, k_cache, v_cache, k_new, v_new, kv_of, owner_of, ctx
                                     _p(v_cache), _p(_bf16(k_new, (B, n_kv, D))),
                                     _p(_bf16(v_new, (B, n_kv, D))), _p(_i32(ctx)), _p(q_rot),
                                     _p(k_rot), _p(scratch), _p(out))
+    if return_rotated:
+        return out, q_rot, k_rot
     return out
 
 

@@ -37,7 +37,7 @@ EXPORTS = [
     "mlkv_map_layer_owned_count", "mlkv_map_layer_owned_begin", "mlkv_cache_bytes",
     "mlkv_workspace_bytes", "mlkv_cache_append", "mlkv_decode_attention", "mlkv_decode_step",
     "mlkv_plan", "mlkv_workspace_init", "mlkv_profile_enable", "mlkv_profile_read",
-    "mlkv_profile_durations", "mlkv_profile_disable",
+    "mlkv_profile_durations", "mlkv_profile_disable", "mlkv_decode_step_rope",
 ]
 
 
@@ -85,6 +85,7 @@ def lib():
             "mlkv_cache_append": ([I, P, P, P, P, I, P, P], S),
             "mlkv_decode_attention": ([I, P, P, P, P, P, I, I, P, Z, P], S),
             "mlkv_decode_step": ([P, P, P, P, P, P, P, I, I, P, Z, P], S),
+            "mlkv_decode_step_rope": ([P, P, P, P, P, P, I, ctypes.c_double, P, I, I, P, Z, P], S),
             "mlkv_plan": ([P, I, I, I, I, I, ctypes.POINTER(I), ctypes.POINTER(I)], S),
             "mlkv_workspace_init": ([P, Z, P], S),
             "mlkv_profile_enable": ([I], S),
@@ -298,18 +299,26 @@ def decode_attention(layer: int, q: torch.Tensor, cache: Cache, map_: Map, seq_l
 
 def decode_step(q_all: torch.Tensor, k_new_all: torch.Tensor, v_new_all: torch.Tensor,
                 cache: Cache, map_: Map, ctx_lens: torch.Tensor, out_all: torch.Tensor,
-                max_len_hint: int = 0, ws: torch.Tensor | None = None, stream=None):
-    """mlkv_decode_step over all layers: q_all [l][B][h][D], k/v_new_all [B][n_kv][D]."""
+                max_len_hint: int = 0, ws: torch.Tensor | None = None, stream=None,
+                rotary_dims: int = 0, rotary_base: float = 10000.0):
+    """mlkv_decode_step over all layers: q_all [l][B][h][D], k/v_new_all [B][n_kv][D].
+    rotary_dims > 0 calls mlkv_decode_step_rope: the newest token's queries
+    and keys are first rotated IN PLACE (q_all and k_new_all) at position
+    ctx_lens[b]."""
     out_dt = OUT_BF16 if out_all.dtype == torch.bfloat16 else OUT_F32
     if out_all.dtype not in (torch.float32, torch.bfloat16):
         raise ValueError("out_all must be float32 or bfloat16")
     ws_ptr, ws_n = (ws.data_ptr(), ws.numel() * ws.element_size()) if ws is not None else (None, 0)
-    _check(lib().mlkv_decode_step(_dev_ptr(q_all, torch.bfloat16, "q_all"),
-                                  _dev_ptr(k_new_all, torch.bfloat16, "k_new_all"),
-                                  _dev_ptr(v_new_all, torch.bfloat16, "v_new_all"), cache.struct,
-                                  map_.handle, _dev_ptr(ctx_lens, torch.int32, "ctx_lens"),
-                                  _dev_ptr(out_all, out_all.dtype, "out_all"), out_dt,
-                                  max_len_hint, ws_ptr, ws_n, _stream(stream)))
+    args = (_dev_ptr(q_all, torch.bfloat16, "q_all"),
+            _dev_ptr(k_new_all, torch.bfloat16, "k_new_all"),
+            _dev_ptr(v_new_all, torch.bfloat16, "v_new_all"), cache.struct, map_.handle,
+            _dev_ptr(ctx_lens, torch.int32, "ctx_lens"))
+    tail = (_dev_ptr(out_all, out_all.dtype, "out_all"), out_dt, max_len_hint, ws_ptr, ws_n,
+            _stream(stream))
+    if rotary_dims:
+        _check(lib().mlkv_decode_step_rope(*args, rotary_dims, float(rotary_base), *tail))
+    else:
+        _check(lib().mlkv_decode_step(*args, *tail))
 
 
 # ------------------------------------------------------------------ timing ---

@@ -6,6 +6,19 @@
 
 namespace mlkv {
 
+// Rotary position embedding of the newest token (GPT-NeoX: rotate-half pairs
+// (j, j + dims/2) of the first `dims` channels of every head vector), applied
+// in place to its queries of every layer and its keys of every KV head.
+// inv_freq[j] = base^(-2j/dims): radians pair j turns by per position.
+constexpr int kMaxRopePairs = 64;
+struct RopeParams {
+  uint16_t* q;               // [l][B][h][D]
+  uint16_t* k;               // [B][n_kv][D]
+  const int32_t* pos;        // [B] position of sequence b's newest token
+  int l, B, h, n_kv, D, dims;
+  double inv_freq[kMaxRopePairs];
+};
+
 struct AppendParams {
   const uint16_t* k_new;     // row b at k_new + b*row_stride: [owned][D]
   const uint16_t* v_new;
@@ -50,6 +63,7 @@ struct AttnParams {
 
 hipError_t launch_append(const AppendParams& p, int head_dim, int owned_count,
                          hipStream_t stream);
+hipError_t launch_rope(const RopeParams& p, hipStream_t stream);
 // The split-K attention kernel, then (when splits are merged by a separate
 // kernel) the merge.
 // start/stop: optional events recorded around the attention dispatch.

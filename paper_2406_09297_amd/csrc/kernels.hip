@@ -164,6 +164,60 @@ __global__ __launch_bounds__(D / 8) void append_kernel(AppendParams p) {
 }
 
 // ---------------------------------------------------------------------------
+// Rotary position embedding of the GPT-NeoX architecture (the paper's Pythia
+// models, Section 4.2), for the newest token of each sequence, in place.
+// Workgroup (x, b): the cosine and sine of every channel pair's angle at
+// position pos[b] are taken in double, one pair per thread, into LDS; then
+// each thread rotates eight pairs (channels j0..j0+7 with their partners
+// j0+dims/2..) of one head vector: a query of some layer, or a key.  The
+// rotation is evaluated in double and rounded once to bf16, nearest even.
+// ---------------------------------------------------------------------------
+constexpr int kRopeThreads = 256;
+
+__device__ __forceinline__ uint16_t f64_to_bf16_bits(double v) {
+  // Round to odd into fp32 (24 bits: no double rounding), then to nearest
+  // even into bf16.
+  const float f = __double2float_rz(v);
+  uint32_t u = __builtin_bit_cast(uint32_t, f);
+  if (static_cast<double>(f) != v && v == v) u |= 1u;
+  return f32_to_bf16_bits(__builtin_bit_cast(float, u));
+}
+
+__global__ __launch_bounds__(kRopeThreads) void rope_kernel(RopeParams p) {
+  __shared__ double cos_t[kMaxRopePairs], sin_t[kMaxRopePairs];
+  const int b = blockIdx.y;
+  const int half = p.dims / 2;
+  const double pos = static_cast<double>(p.pos[b]);
+  for (int t = threadIdx.x; t < half; t += kRopeThreads)
+    sincos(pos * p.inv_freq[t], &sin_t[t], &cos_t[t]);
+  __syncthreads();
+  const int chunks = p.dims / 16;  // eight-pair chunks per head vector
+  const int rows = p.l * p.h + p.n_kv;
+  const int item = blockIdx.x * kRopeThreads + threadIdx.x;
+  if (item >= rows * chunks) return;
+  const int row = item / chunks;
+  const int j0 = (item - row * chunks) * 8;
+  uint16_t* x;
+  if (row < p.l * p.h) {
+    const int n = row / p.h, i = row - n * p.h;
+    x = p.q + ((static_cast<size_t>(n) * p.B + b) * p.h + i) * p.D;
+  } else {
+    x = p.k + (static_cast<size_t>(b) * p.n_kv + (row - p.l * p.h)) * p.D;
+  }
+  const u16x8 a = load16(x + j0), c = load16(x + half + j0);
+  u16x8 ya, yc;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const double u = __builtin_bit_cast(float, static_cast<uint32_t>(a[e]) << 16);
+    const double w = __builtin_bit_cast(float, static_cast<uint32_t>(c[e]) << 16);
+    ya[e] = f64_to_bf16_bits(u * cos_t[j0 + e] - w * sin_t[j0 + e]);
+    yc[e] = f64_to_bf16_bits(w * cos_t[j0 + e] + u * sin_t[j0 + e]);
+  }
+  *reinterpret_cast<u16x8*>(x + j0) = ya;
+  *reinterpret_cast<u16x8*>(x + half + j0) = yc;
+}
+
+// ---------------------------------------------------------------------------
 // Split-K attention over a balanced flat tile list.
 // ---------------------------------------------------------------------------
 template <int D>
@@ -1008,6 +1062,14 @@ int resident_workgroups(int head_dim) {
   v = cus * per_cu;
   slot.store(v, std::memory_order_relaxed);
   return v;
+}
+
+hipError_t launch_rope(const RopeParams& p, hipStream_t stream) {
+  const int items = (p.l * p.h + p.n_kv) * (p.dims / 16);
+  if (items == 0 || p.B == 0) return hipSuccess;
+  const dim3 grid((items + kRopeThreads - 1) / kRopeThreads, p.B);
+  hipLaunchKernelGGL(rope_kernel, grid, dim3(kRopeThreads), 0, stream, p);
+  return hipGetLastError();
 }
 
 hipError_t launch_fill(uint32_t* dst, size_t n_words, uint32_t value, hipStream_t stream) {

@@ -577,10 +577,14 @@ mlkv_status mlkv_decode_attention(int layer, const void* q, const mlkv_cache* ca
   return ok();
 }
 
-mlkv_status mlkv_decode_step(const void* q_all, const void* k_new_all, const void* v_new_all,
-                             const mlkv_cache* cache, const mlkv_map* map, const int32_t* ctx_lens,
-                             void* out_all, mlkv_out_dtype out_dtype, int max_len_hint,
-                             void* workspace, size_t workspace_bytes, hipStream_t stream) {
+namespace {
+
+// Argument checks of a decode step, done before anything is launched.
+mlkv_status decode_step_check(const void* q_all, const void* k_new_all, const void* v_new_all,
+                              const mlkv_cache* cache, const mlkv_map* map,
+                              const int32_t* ctx_lens, void* out_all, mlkv_out_dtype out_dtype,
+                              int max_len_hint, void* workspace, size_t workspace_bytes,
+                              hipStream_t stream) {
   mlkv_status s;
   if ((s = check_map(map)) != MLKV_OK) return s;
   if ((s = check_cache(cache, map)) != MLKV_OK) return s;
@@ -596,7 +600,7 @@ mlkv_status mlkv_decode_step(const void* q_all, const void* k_new_all, const voi
   if (max_len_hint > cache->capacity)
     return fail(MLKV_ERR_CAPACITY, "max_len_hint %d above capacity %d", max_len_hint,
                 cache->capacity);
-  const int B = cache->batch, h = map->h, D = cache->head_dim, n_kv = map->n_kv;
+  const int B = cache->batch, h = map->h, D = cache->head_dim;
   // Workspace check up front so that no layer is half-launched.
   {
     const int max_len = max_len_hint <= 0 ? cache->capacity : max_len_hint;
@@ -611,6 +615,18 @@ mlkv_status mlkv_decode_step(const void* q_all, const void* k_new_all, const voi
   }
   const int limit = (max_len_hint <= 0 ? cache->capacity : max_len_hint);
   if ((s = check_lengths_if_requested(ctx_lens, B, 1, limit, stream)) != MLKV_OK) return s;
+  return MLKV_OK;
+}
+
+// The step's launches: per layer, the append it owns (when not fused) and
+// its attention.
+mlkv_status decode_step_launch(const void* q_all, const void* k_new_all, const void* v_new_all,
+                               const mlkv_cache* cache, const mlkv_map* map,
+                               const int32_t* ctx_lens, void* out_all, mlkv_out_dtype out_dtype,
+                               int max_len_hint, void* workspace, size_t workspace_bytes,
+                               hipStream_t stream) {
+  mlkv_status s;
+  const int B = cache->batch, h = map->h, D = cache->head_dim, n_kv = map->n_kv;
   const size_t layer_elems = static_cast<size_t>(B) * h * D;
   const size_t out_elem_bytes = out_dtype == MLKV_OUT_BF16 ? 2 : 4;
   const uint16_t* k_new = static_cast<const uint16_t*>(k_new_all);
@@ -641,6 +657,55 @@ mlkv_status mlkv_decode_step(const void* q_all, const void* k_new_all, const voi
     planned_key = key;
   }
   return ok();
+}
+
+}  // namespace
+
+mlkv_status mlkv_decode_step(const void* q_all, const void* k_new_all, const void* v_new_all,
+                             const mlkv_cache* cache, const mlkv_map* map, const int32_t* ctx_lens,
+                             void* out_all, mlkv_out_dtype out_dtype, int max_len_hint,
+                             void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  const mlkv_status s =
+      decode_step_check(q_all, k_new_all, v_new_all, cache, map, ctx_lens, out_all, out_dtype,
+                        max_len_hint, workspace, workspace_bytes, stream);
+  if (s != MLKV_OK) return s;
+  return decode_step_launch(q_all, k_new_all, v_new_all, cache, map, ctx_lens, out_all, out_dtype,
+                            max_len_hint, workspace, workspace_bytes, stream);
+}
+
+mlkv_status mlkv_decode_step_rope(void* q_all, void* k_new_all, const void* v_new_all,
+                                  const mlkv_cache* cache, const mlkv_map* map,
+                                  const int32_t* ctx_lens, int rotary_dims, double rotary_base,
+                                  void* out_all, mlkv_out_dtype out_dtype, int max_len_hint,
+                                  void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  mlkv_status s;
+  if ((s = check_map(map)) != MLKV_OK) return s;
+  if ((s = check_cache(cache, map)) != MLKV_OK) return s;
+  if (rotary_dims < 0 || rotary_dims > cache->head_dim || rotary_dims % 16 != 0)
+    return fail(MLKV_ERR_UNSUPPORTED, "rotary_dims %d: a multiple of 16 in [0, head_dim] required",
+                rotary_dims);
+  if (!(rotary_base > 0.0) || !std::isfinite(rotary_base))
+    return fail(MLKV_ERR_INVALID_ARG, "rotary_base must be positive and finite");
+  if ((s = decode_step_check(q_all, k_new_all, v_new_all, cache, map, ctx_lens, out_all, out_dtype,
+                             max_len_hint, workspace, workspace_bytes, stream)) != MLKV_OK)
+    return s;
+  if (rotary_dims > 0) {
+    mlkv::RopeParams p{};
+    p.q = static_cast<uint16_t*>(q_all);
+    p.k = static_cast<uint16_t*>(k_new_all);
+    p.pos = ctx_lens;
+    p.l = map->l;
+    p.B = cache->batch;
+    p.h = map->h;
+    p.n_kv = map->n_kv;
+    p.D = cache->head_dim;
+    p.dims = rotary_dims;
+    for (int j = 0; j < rotary_dims / 2; ++j) p.inv_freq[j] = std::pow(rotary_base, -2.0 * j / rotary_dims);
+    const hipError_t err = mlkv::launch_rope(p, stream);
+    if (err != hipSuccess) return fail(MLKV_ERR_HIP, "rotary launch: %s", hipGetErrorString(err));
+  }
+  return decode_step_launch(q_all, k_new_all, v_new_all, cache, map, ctx_lens, out_all, out_dtype,
+                            max_len_hint, workspace, workspace_bytes, stream);
 }
 
 mlkv_status mlkv_profile_enable(int max_launches) {

@@ -126,6 +126,18 @@ def test_entry_points_reject_bad_arguments():
     assert names[L.mlkv_cache_append(0, mp.handle, ref, 0x30000, 0x30000, 60, 0x40000, None)] == "MLKV_ERR_INVALID_ARG"
     assert names[L.mlkv_cache_append(0, mp.handle, ref, 0x30008, 0x30000, 64, 0x40000, None)] == "MLKV_ERR_ALIGNMENT"
     assert names[L.mlkv_cache_append(1, mp.handle, ref, None, None, 0, None, None)] == "MLKV_OK"
+    # rotary embedding: dims a multiple of 16 in [0, head_dim], base positive and finite
+    for rd, base, want in [(8, 1e4, "MLKV_ERR_UNSUPPORTED"), (-16, 1e4, "MLKV_ERR_UNSUPPORTED"),
+                           (80, 1e4, "MLKV_ERR_UNSUPPORTED"), (16, 0.0, "MLKV_ERR_INVALID_ARG"),
+                           (16, -2.0, "MLKV_ERR_INVALID_ARG"),
+                           (16, float("nan"), "MLKV_ERR_INVALID_ARG"),
+                           (16, float("inf"), "MLKV_ERR_INVALID_ARG")]:
+        got = names[L.mlkv_decode_step_rope(0x30000, 0x30000, 0x30000, ref, mp.handle, 0x40000, rd,
+                                            base, 0x50000, 0, 0, None, 0, None)]
+        assert got == want, (rd, base, got)
+    # with valid rotary arguments the step's own checks apply (workspace here)
+    assert names[L.mlkv_decode_step_rope(0x30000, 0x30000, 0x30000, ctypes.byref(big), mp.handle,
+                                         0x40000, 16, 1e4, 0x50000, 0, 0, None, 0, None)] == "MLKV_ERR_WORKSPACE"
     # group size above 16 query heads per KV head is reported as unsupported
     mq = mlkv.Map.uniform(2, 32, 2, 1)
     c2 = mlkv._Cache(0x10000, 0x20000, 2, 2, 64, 64)

@@ -378,6 +378,77 @@ def test_step_owner_that_does_not_read_its_head():
     check_close(out, ref, "general map")
 
 
+# ------------------------------------------------------ rotary embedding --
+
+def _check_rope_step(dw, rd, label, base=10000.0):
+    """The step with rotary embedding against the oracle: the newest token's
+    queries and keys are rotated in place bit for bit, the cache (rotated
+    keys) matches bit for bit, the outputs within tolerance."""
+    w = dw.w
+    out = torch.empty((w.l, w.B, w.h, w.D), dtype=torch.float32, device="cuda")
+    mlkv.decode_step(dw.q, dw.k_new, dw.v_new, dw.cache, dw.map, dw.ctx, out, ws=dw.ws,
+                     rotary_dims=rd, rotary_base=base)
+    torch.cuda.synchronize()
+    out = out.cpu().numpy()
+    k_gpu, v_gpu = dw.read_cache()
+    k, v = dw.host["k_cache"].copy(), dw.host["v_cache"].copy()
+    ref, q_rot, k_rot = oracle.decode_step_rope(dw.host["q"], k, v, dw.host["k_new"],
+                                                dw.host["v_new"], dw.kv_of, dw.owner_of,
+                                                dw.host["ctx"], rd, base, return_rotated=True)
+    q_gpu = mlkv.bf16_bits(dw.q)
+    k_new_gpu = mlkv.bf16_bits(dw.k_new).reshape(k_rot.shape)
+    bad = np.argwhere(q_gpu != q_rot)
+    assert bad.size == 0, f"{label}: rotated queries differ at {bad[:4].tolist()}"
+    bad = np.argwhere(k_new_gpu != k_rot)
+    assert bad.size == 0, f"{label}: rotated keys differ at {bad[:4].tolist()}"
+    assert np.array_equal(v_gpu, v) and np.array_equal(k_gpu, k), f"{label}: cache differs"
+    check_close(out, ref, label)
+
+
+@pytest.mark.parametrize("D,m,g,rd,wide,qk", [
+    (64, 4, 1, 16, "", ""), (64, 4, 1, 64, "", ""), (64, 4, 3, 32, "1", ""),
+    (128, 2, 4, 128, "", ""), (128, 2, 4, 32, "1", ""),
+    (64, 4, 1, 16, "", "valu"), (128, 2, 4, 64, "", "valu")])
+def test_step_rope_across_tile_boundaries(D, m, g, rd, wide, qk):
+    """Rotary embedding of the newest token inside the step: its queries are
+    rotated as each layer loads them and its keys as the owner appends them,
+    at every offset of a 32-token tile; the cache (rotated keys) matches the
+    oracle bit for bit and the outputs within tolerance."""
+    w = synth.Workload("rope_sweep", l=4, h=12, m=m, g=g, D=D, B=len(APPEND_CTX),
+                       ctx=max(APPEND_CTX), seed=78)
+    dw = _with_contexts(DeviceWorkload(w), APPEND_CTX)
+    say(f"rope step D={D} m={m} g={g} rd={rd} wide={wide or 'auto'} qk={qk or 'mfma'}")
+    with plan_env(wide=wide, qk=qk):
+        _check_rope_step(dw, rd, f"rope D{D} m{m} g{g} rd{rd} {wide} {qk}")
+
+
+def test_step_rope_general_map_separate_append():
+    """Rotated keys through the separate append launch (an owner that does
+    not read its head), with a base other than the default."""
+    w = synth.Workload("general_rope", l=4, h=4, m=2, g=1, D=64, B=3, ctx=100, seed=12)
+    dw = DeviceWorkload(w)
+    kv_of = np.array([[0] * 4, [1] * 4, [0] * 4, [1] * 4], np.int32)
+    owner_of = np.array([0, 0], np.int32)
+    dw.map = mlkv.Map.from_tables(kv_of, owner_of)
+    dw.kv_of, dw.owner_of = kv_of, owner_of
+    _with_contexts(dw, [0, 37, 100])
+    say("rope general map")
+    _check_rope_step(dw, 32, "rope general map", base=500.0)
+
+
+@pytest.mark.parametrize("wname,rd", [("mlkv4_b8_long", 16), ("mlkv4_b128_ragged", 16),
+                                      ("mlkv4_b128_ragged", 64)])
+def test_full_size_step_rope(wname, rd):
+    """Full-size steps with the Pythia-160M rotary (16 of 64 channels, base
+    10000) and with every channel rotated; the long contexts put the new
+    token at positions near 32768."""
+    w = synth.get_workload(wname)
+    say(f"full rope step {wname} rd={rd}: uploading")
+    dw = DeviceWorkload(w)
+    say(f"full rope step {wname} rd={rd}: running")
+    _check_rope_step(dw, rd, f"full rope {wname} rd{rd}")
+
+
 # ------------------------------------------------------------ edge cases --
 
 def test_step_bf16_output_is_the_rounded_fp32_step():
