@@ -65,6 +65,12 @@ def _load():
         lib.oracle_decode_step_rope.argtypes = [I, I, I, I, I, I, I, D_, P, P, P, P, P, P, P, P,
                                                 P, P, P, P]
         lib.oracle_decode_step_rope.restype = None
+        lib.oracle_prefill_attention.argtypes = [I, I, I, I, I, I, I, P, P, P, P, P, P]
+        lib.oracle_prefill_attention.restype = None
+        lib.oracle_append_rows.argtypes = [I, I, I, I, I, I, P, P, P, P, P, P]
+        lib.oracle_append_rows.restype = I
+        lib.oracle_prefill_step.argtypes = [I, I, I, I, I, I, I, P, P, P, P, P, P, P, P, P]
+        lib.oracle_prefill_step.restype = None
         _lib = lib
     return _lib
 
@@ -168,6 +174,46 @@ def decode_step(q_all, k_cache, v_cache, k_new, v_new, kv_of, owner_of, ctx):
                                _p(_bf16(q_all)), _p(k_cache), _p(v_cache),
                                _p(_bf16(k_new, (B, n_kv, D))), _p(_bf16(v_new, (B, n_kv, D))),
                                _p(_i32(ctx)), _p(scratch), _p(out))
+    return out
+
+
+def prefill_attention(layer, q, k_cache, v_cache, kv_of, ctx):
+    """One layer of causal prefill attention: q [B][T][h][D]; token t of
+    sequence b attends positions 0 .. ctx[b] + t.  Returns [B][T][h][D] float64."""
+    B, T, h, D = q.shape
+    n_kv, B2, S, D2 = k_cache.shape
+    assert (B2, D2) == (B, D)
+    out = np.empty((B, T, h, D), dtype=np.float64)
+    _load().oracle_prefill_attention(layer, B, T, h, n_kv, S, D, _p(_i32(kv_of)), _p(_bf16(q)),
+                                     _p(_bf16(k_cache)), _p(_bf16(v_cache)), _p(_i32(ctx)),
+                                     _p(out))
+    return out
+
+
+def append_rows(layer, k_cache, v_cache, k_new, v_new, owner_of, ctx) -> int:
+    """Owners of `layer` store T new rows [B][T][n_kv][D] at slots ctx[b] + t
+    (in place); returns the number of KV heads appended."""
+    n_kv, B, S, D = k_cache.shape
+    T = k_new.shape[1]
+    assert k_cache.flags.c_contiguous and v_cache.flags.c_contiguous
+    return _load().oracle_append_rows(layer, B, T, n_kv, S, D, _p(_i32(owner_of)), _p(k_cache),
+                                      _p(v_cache), _p(_bf16(k_new, (B, T, n_kv, D))),
+                                      _p(_bf16(v_new, (B, T, n_kv, D))), _p(_i32(ctx)))
+
+
+def prefill_step(q_all, k_cache, v_cache, k_new, v_new, kv_of, owner_of, ctx):
+    """Whole prefill (Eq. 17 order): per layer the owners append the T new
+    rows, then every head attends causally.  q_all [l][B][T][h][D], k/v_new
+    [B][T][n_kv][D].  Updates the caches in place; returns [l][B][T][h][D]."""
+    l, B, T, h, D = q_all.shape
+    n_kv, B2, S, D2 = k_cache.shape
+    assert (B2, D2) == (B, D)
+    assert k_cache.flags.c_contiguous and v_cache.flags.c_contiguous
+    out = np.empty((l, B, T, h, D), dtype=np.float64)
+    _load().oracle_prefill_step(l, B, T, h, n_kv, S, D, _p(_i32(kv_of)), _p(_i32(owner_of)),
+                                _p(_bf16(q_all)), _p(k_cache), _p(v_cache),
+                                _p(_bf16(k_new, (B, T, n_kv, D))),
+                                _p(_bf16(v_new, (B, T, n_kv, D))), _p(_i32(ctx)), _p(out))
     return out
 
 

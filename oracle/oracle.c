@@ -20,6 +20,9 @@
  *   KV caching ............. Section 2.4
  *   MLKV sharing ........... Section 3, Eqs. (13)-(17); the shared head comes
  *                            from the bottom layer of its group (Figure 2)
+ *   prefill ................ the cache of Section 2.4 filled from a prompt of
+ *                            T tokens, causally (each token attends to the
+ *                            positions up to its own)
  *   rotary embedding ....... the GPT-NeoX architecture of the Pythia models
  *                            (Section 4.2): rotate-half pairs of the first
  *                            rd channels, angle pos * base^(-2j/rd)
@@ -39,7 +42,11 @@
  * cache-size ratios.  Rotary (tests/test_oracle_rope.py): identity at
  * position 0, a four-channel closed form, pair lengths kept, scores that
  * depend only on the position difference, bf16 rounding against an
- * enumeration of neighbouring bf16 values.
+ * enumeration of neighbouring bf16 values.  Prefill
+ * (tests/test_oracle_prefill.py): one token equals the decode step; T tokens
+ * equal T decode steps in sequence; torch SDPA with a causal mask; later
+ * tokens leave earlier outputs unchanged; a two-token closed form; rows
+ * appended at consecutive slots with nothing else touched.
  */
 #include <math.h>
 #include <stdint.h>
@@ -197,6 +204,85 @@ void oracle_decode_step(int l, int B, int h, int n_kv, int S, int D, const int32
     oracle_append(n, B, n_kv, S, D, owner_of, Kc, Vc, k_new, v_new, ctx);
     oracle_decode_attention(n, B, h, n_kv, S, D, kv_of, q_all + (size_t)n * B * h * D, Kc, Vc,
                             lens_scratch, out_all + (size_t)n * B * h * D);
+  }
+}
+
+/* ------------------------------------------------------------------------ */
+/* Prefill: T new tokens of every sequence in one call.  The cache of        */
+/* Section 2.4 is filled from the prompt; under MLKV (Section 3) the owning  */
+/* layer stores the new keys/values and every layer of the group attends to  */
+/* them.  Token t of sequence b sits at position ctx[b] + t and attends      */
+/* causally: positions 0 .. ctx[b] + t (cached tokens, earlier new tokens    */
+/* and itself).                                                              */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * For every sequence b, new token t < T and query head i of `layer`:
+ *   kv = kv_of[layer][i],  L = ctx[b] + t + 1  (clamped to [0, S])
+ *   out[b][t][i][:] = attend(q[b][t][i], Kc[kv][b][0:L], Vc[kv][b][0:L])
+ * q [B][T][h][D], out [B][T][h][D] (double).
+ */
+void oracle_prefill_attention(int layer, int B, int T, int h, int n_kv, int S, int D,
+                              const int32_t* kv_of, const uint16_t* q, const uint16_t* Kc,
+                              const uint16_t* Vc, const int32_t* ctx, double* out) {
+#pragma omp parallel for collapse(3) schedule(dynamic)
+  for (int b = 0; b < B; ++b) {
+    for (int t = 0; t < T; ++t) {
+      for (int i = 0; i < h; ++i) {
+        int kv = kv_of[layer * h + i];
+        long L = (long)ctx[b] + t + 1;
+        if (L < 0) L = 0;
+        if (L > S) L = S;
+        size_t row = ((size_t)kv * B + b) * (size_t)S * D;
+        size_t qo = (((size_t)b * T + t) * h + i) * D;
+        oracle_attend_one(q + qo, Kc + row, Vc + row, L, D, D, out + qo, NULL);
+      }
+    }
+  }
+  (void)n_kv;
+}
+
+/*
+ * For every KV head kv whose owner is `layer`, every b and t < T with
+ * 0 <= ctx[b] + t < S:  Kc[kv][b][ctx[b] + t] = k_new[b][t][kv],  Vc likewise.
+ * k_new, v_new [B][T][n_kv][D].  Returns the number of KV heads appended.
+ */
+int oracle_append_rows(int layer, int B, int T, int n_kv, int S, int D, const int32_t* owner_of,
+                       uint16_t* Kc, uint16_t* Vc, const uint16_t* k_new, const uint16_t* v_new,
+                       const int32_t* ctx) {
+  int owned = 0;
+  for (int kv = 0; kv < n_kv; ++kv) {
+    if (owner_of[kv] != layer) continue;
+    ++owned;
+    for (int b = 0; b < B; ++b) {
+      for (int t = 0; t < T; ++t) {
+        long slot = (long)ctx[b] + t;
+        if (slot < 0 || slot >= S) continue;
+        size_t dst = (((size_t)kv * B + b) * S + (size_t)slot) * D;
+        size_t src = (((size_t)b * T + t) * n_kv + kv) * D;
+        memcpy(Kc + dst, k_new + src, sizeof(uint16_t) * D);
+        memcpy(Vc + dst, v_new + src, sizeof(uint16_t) * D);
+      }
+    }
+  }
+  return owned;
+}
+
+/*
+ * for n = 0 .. l-1:
+ *   the heads layer n owns take the T new rows at slots ctx[b] .. ctx[b]+T-1;
+ *   every query head of layer n attends causally as above.
+ * q_all [l][B][T][h][D], out_all [l][B][T][h][D] (double).  Kc/Vc are updated.
+ */
+void oracle_prefill_step(int l, int B, int T, int h, int n_kv, int S, int D,
+                         const int32_t* kv_of, const int32_t* owner_of, const uint16_t* q_all,
+                         uint16_t* Kc, uint16_t* Vc, const uint16_t* k_new,
+                         const uint16_t* v_new, const int32_t* ctx, double* out_all) {
+  const size_t layer_elems = (size_t)B * T * h * D;
+  for (int n = 0; n < l; ++n) {
+    oracle_append_rows(n, B, T, n_kv, S, D, owner_of, Kc, Vc, k_new, v_new, ctx);
+    oracle_prefill_attention(n, B, T, h, n_kv, S, D, kv_of, q_all + (size_t)n * layer_elems, Kc,
+                             Vc, ctx, out_all + (size_t)n * layer_elems);
   }
 }
 

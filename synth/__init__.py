@@ -148,3 +148,30 @@ def step_inputs(w: Workload, fill: int = 0, with_cache: bool = True) -> dict:
         out["v_cache"] = rows_bf16(w.seed, STREAM_V_CACHE, w.n_kv * w.B, S, w.D, lens,
                                    fill=fill).reshape(w.n_kv, w.B, S, w.D)
     return out
+
+
+def prefill_inputs(w: Workload, fill: int = 0, with_cache: bool = True) -> dict:
+    """Host inputs of one prefill of w.T new tokens per sequence, logical order.
+
+    q        [l][B][T][h][D]   bf16 bits (uint16)
+    k_new    [B][T][n_kv][D]   the new tokens' keys (scaled by k_scale), v_new likewise
+    k_cache  [n_kv][B][S][D]   tokens [0, ctx_b) valid, the rest = fill
+    v_cache  [n_kv][B][S][D]
+    ctx      [B] int32         tokens cached before the prefill
+    """
+    ctx = context_lengths(w)
+    S = w.capacity
+    out = {
+        "ctx": ctx,
+        "q": normal_bf16(w.seed, STREAM_Q, (w.l, w.B, w.T, w.h, w.D)),
+        "k_new": normal_bf16(w.seed, STREAM_K_NEW, (w.B, w.T, w.n_kv, w.D), scale=w.k_scale),
+        "v_new": normal_bf16(w.seed, STREAM_V_NEW, (w.B, w.T, w.n_kv, w.D)),
+        "capacity": S,
+    }
+    if with_cache:
+        lens = np.tile(ctx, w.n_kv)
+        out["k_cache"] = rows_bf16(w.seed, STREAM_K_CACHE, w.n_kv * w.B, S, w.D, lens,
+                                   scale=w.k_scale, fill=fill).reshape(w.n_kv, w.B, S, w.D)
+        out["v_cache"] = rows_bf16(w.seed, STREAM_V_CACHE, w.n_kv * w.B, S, w.D, lens,
+                                   fill=fill).reshape(w.n_kv, w.B, S, w.D)
+    return out

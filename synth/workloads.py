@@ -32,6 +32,7 @@ class Workload:
     seed: int = 0x4D4C4B56
     note: str = ""
     sweep: tuple = field(default_factory=tuple)   # (m, g) points of a map sweep
+    T: int = 1                        # new tokens per sequence (prefill when > 1)
 
     @property
     def n_kv(self) -> int:
@@ -44,15 +45,16 @@ class Workload:
     @property
     def capacity(self) -> int:
         """Cache capacity: the longest attended length rounded up to 64."""
-        need = self.max_ctx + 1
+        need = self.max_ctx + self.T
         return (need + 63) // 64 * 64
 
     def with_map(self, m: int, g: int) -> "Workload":
         return Workload(self.name + f"-m{m}g{g}", self.l, self.h, m, g, self.D, self.B,
-                        self.ctx, self.ctx_range, self.k_scale, self.seed, self.note)
+                        self.ctx, self.ctx_range, self.k_scale, self.seed, self.note, T=self.T)
 
-    def scaled(self, B: int | None = None, ctx: int | None = None) -> "Workload":
-        """Same map and statistics with a smaller batch / context (test sizes)."""
+    def scaled(self, B: int | None = None, ctx: int | None = None,
+               T: int | None = None) -> "Workload":
+        """Same map and statistics with a smaller batch / context / prompt (test sizes)."""
         c, cr = self.ctx, self.ctx_range
         if ctx is not None:
             if cr is not None:
@@ -60,7 +62,7 @@ class Workload:
             else:
                 c = ctx
         return Workload(self.name + "-small", self.l, self.h, self.m, self.g, self.D,
-                        B or self.B, c, cr, self.k_scale, self.seed, self.note)
+                        B or self.B, c, cr, self.k_scale, self.seed, self.note, T=T or self.T)
 
 
 WORKLOADS = {
@@ -85,6 +87,11 @@ WORKLOADS = {
         "7b_mlkv8x8", l=32, h=32, m=8, g=8, D=128, B=64, ctx=8192, seed=0x4D4C4B56 + 4,
         note="7B-like shape, 32 layers x 32 heads, head dim 128, 8 owning layers with 8 KV "
              "heads each (64 KV heads, 4 query heads per KV head), batch 64, context 8192"),
+    "prefill_b8_2000": Workload(
+        "prefill_b8_2000", l=12, h=12, m=4, g=1, D=64, B=8, ctx=0, T=2000,
+        seed=0x4D4C4B56 + 5,
+        note="Pythia-160M shape, MLKV-4, batch 8: a 2000-token prompt prefilled into an "
+             "empty cache (the paper's inference runs first fill a 2000-token cache)"),
 }
 
 

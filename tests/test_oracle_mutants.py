@@ -10,6 +10,7 @@ import pytest
 
 import oracle
 import test_oracle as pins
+import test_oracle_prefill as prefill_pins
 import test_oracle_rope as rope_pins
 
 SRC = os.path.join(os.path.dirname(oracle.__file__), "oracle.c")
@@ -20,14 +21,16 @@ MUTANTS = [
     ("scale_by_D", "1.0 / sqrt((double)D)", "1.0 / (double)D"),
     ("no_max_shift", "w[t] = exp(w[t] - s_max);", "w[t] = exp(w[t]);"),
     ("no_normalisation", "o[d] /= Z;", "o[d] /= 1.0;"),
-    ("swap_k_and_v", "Kc + row, Vc + row, L", "Vc + row, Kc + row, L"),
+    ("swap_k_and_v", "q + ((size_t)b * h + i) * D, Kc + row, Vc + row, L",
+     "q + ((size_t)b * h + i) * D, Vc + row, Kc + row, L"),
     ("drop_last_token", "long L = seq_lens[b];", "long L = seq_lens[b] - 1;"),
     ("interleaved_q_groups", "int j = (i - 1) / heads_per_kv + 1;", "int j = (i - 1) % g + 1;"),
     ("interleaved_layer_groups", "int k = (n - 1) / layers_per_group + 1;",
      "int k = (n - 1) % m + 1;"),
     ("top_layer_owns", "(k - 1) * layers_per_group; /* bottom layer */",
      "k * layers_per_group - 1;"),
-    ("append_swaps_k_v", "memcpy(Kc + dst, k_new + src", "memcpy(Kc + dst, v_new + src"),
+    ("append_swaps_k_v", "size_t src = ((size_t)b * n_kv + kv) * D;\n      memcpy(Kc + dst, k_new + src",
+     "size_t src = ((size_t)b * n_kv + kv) * D;\n      memcpy(Kc + dst, v_new + src"),
     ("attend_before_append",
      "    oracle_append(n, B, n_kv, S, D, owner_of, Kc, Vc, k_new, v_new, ctx);\n"
      "    oracle_decode_attention(n, B, h, n_kv, S, D, kv_of, q_all + (size_t)n * B * h * D, Kc, Vc,\n"
@@ -45,6 +48,22 @@ MUTANTS = [
     ("rope_rounding_truncates", "nearbyint(m * 256.0)", "trunc(m * 256.0)"),
     ("rope_step_key_position", "oracle_rope(k_new + off, D, rd, base, ctx[b], k_rot + off);",
      "oracle_rope(k_new + off, D, rd, base, ctx[b] + 1, k_rot + off);"),
+    # prefill
+    ("prefill_excludes_itself", "long L = (long)ctx[b] + t + 1;", "long L = (long)ctx[b] + t;"),
+    ("prefill_sees_next_token", "long L = (long)ctx[b] + t + 1;", "long L = (long)ctx[b] + t + 2;"),
+    ("prefill_ignores_new_tokens", "long L = (long)ctx[b] + t + 1;", "long L = (long)ctx[b] + 1;"),
+    ("prefill_swap_k_and_v", "oracle_attend_one(q + qo, Kc + row, Vc + row,",
+     "oracle_attend_one(q + qo, Vc + row, Kc + row,"),
+    ("prefill_append_swaps_k_v",
+     "size_t src = (((size_t)b * T + t) * n_kv + kv) * D;\n        memcpy(Kc + dst, k_new + src",
+     "size_t src = (((size_t)b * T + t) * n_kv + kv) * D;\n        memcpy(Kc + dst, v_new + src"),
+    ("prefill_slot_shifted", "long slot = (long)ctx[b] + t;", "long slot = (long)ctx[b] + t + 1;"),
+    ("prefill_rows_token_major", "size_t src = (((size_t)b * T + t) * n_kv + kv) * D;",
+     "size_t src = (((size_t)t * B + b) * n_kv + kv) * D;"),
+    ("prefill_query_of_first_token", "size_t qo = (((size_t)b * T + t) * h + i) * D;\n"
+     "        oracle_attend_one(q + qo,",
+     "size_t qo = (((size_t)b * T + t) * h + i) * D;\n"
+     "        oracle_attend_one(q + qo - (size_t)t * h * D,"),
 ]
 
 
@@ -74,6 +93,13 @@ def _pin_calls():
         ("rope relative position", rope_pins.test_scores_depend_only_on_the_position_difference),
         ("rope bf16", rope_pins.test_bf16_rope_is_the_rounded_double_rotation),
         ("rope step", rope_pins.test_step_with_rope_is_the_step_on_rotated_inputs),
+        ("prefill T=1", prefill_pins.test_one_new_token_is_the_decode_step),
+        ("prefill = decode steps",
+         lambda: prefill_pins.test_prompt_equals_decode_steps_one_token_at_a_time((4, 6, 2, 2))),
+        ("prefill sdpa", prefill_pins.test_matches_torch_sdpa_with_a_causal_mask),
+        ("prefill causal", prefill_pins.test_later_tokens_do_not_change_earlier_outputs),
+        ("prefill two tokens", prefill_pins.test_two_new_tokens_closed_form),
+        ("prefill rows", prefill_pins.test_owners_write_the_new_rows_at_consecutive_slots),
     ]
     return calls
 
