@@ -222,6 +222,60 @@ mlkv_status mlkv_decode_step_rope(void* q_all, void* k_new_all, const void* v_ne
                                   void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /* ----------------------------------------------------------------------- */
+/* Prefill: T new tokens per sequence (a prompt, or a chunk of one)          */
+/* ----------------------------------------------------------------------- */
+
+/*
+ * The cache of Section 2.4 filled from a prompt; under MLKV (Section 3) the
+ * owning layer stores the new keys/values and every layer of its group
+ * attends to them.  Token t (0 <= t < T) of sequence b sits at position
+ * ctx_lens[b] + t and attends causally to positions 0 .. ctx_lens[b] + t
+ * (the cached prefix, the earlier new tokens and itself).
+ * ctx_lens: device int32 [batch], tokens cached before the call; each must be
+ *   in [0, capacity - T].  They are read on the device and validated only
+ *   under MLKV_CHECK=1 (which synchronizes); out-of-range values never make
+ *   a kernel leave the cache (slots outside [0, capacity) are not written,
+ *   positions are clamped to the capacity), but their results are unspecified.
+ * T: 0 <= T <= capacity (else MLKV_ERR_CAPACITY); T = 0 does nothing.
+ *   T times the query heads per KV head must not exceed 4,194,240
+ *   (MLKV_ERR_UNSUPPORTED).  Any group size is accepted (no 16-head limit).
+ * No workspace: each query row is finished by one wave.
+ */
+
+/* The T new rows of the KV heads `layer` owns, stored at slots
+ * ctx_lens[b] + t (bit copy); a no-op for layers that own none.
+ *   k_new, v_new: device bf16, row (b, t) at k_new + (b*T + t)*new_row_stride
+ *                 elements, holding the owned heads' rows back to back;
+ *                 16-byte aligned, new_row_stride a multiple of 8 and
+ *                 >= owned_count*head_dim. */
+mlkv_status mlkv_cache_append_rows(int layer, const mlkv_map* map, const mlkv_cache* cache,
+                                   const void* k_new, const void* v_new, int T,
+                                   int new_row_stride, const int32_t* ctx_lens,
+                                   hipStream_t stream);
+
+/* Causal attention of every query head of `layer` for the T new tokens.
+ *   q:   device bf16 [batch][T][h][head_dim], 16-byte aligned.
+ *   out: device [batch][T][h][head_dim] fp32 or bf16 (out_dtype), 16-byte
+ *        aligned.
+ * The owners' new rows must already be in the cache (mlkv_cache_append_rows
+ * of the owning layer). */
+mlkv_status mlkv_prefill_attention(int layer, const void* q, const mlkv_cache* cache,
+                                   const mlkv_map* map, const int32_t* ctx_lens, int T, void* out,
+                                   mlkv_out_dtype out_dtype, hipStream_t stream);
+
+/* The whole prefill of a model (Eq. 17's layer order): for n = 0..l-1 the
+ * heads layer n owns take their T new rows, then layer n attends.
+ *   q_all:     device bf16 [l][batch][T][h][head_dim].
+ *   k_new_all, v_new_all: device bf16 [batch][T][n_kv][head_dim] (every KV
+ *              head's new rows; each owner stores its columns).
+ *   out_all:   device [l][batch][T][h][head_dim], fp32 or bf16.
+ * All 16-byte aligned.  Every check is made before anything is launched. */
+mlkv_status mlkv_prefill_step(const void* q_all, const void* k_new_all, const void* v_new_all,
+                              const mlkv_cache* cache, const mlkv_map* map,
+                              const int32_t* ctx_lens, int T, void* out_all,
+                              mlkv_out_dtype out_dtype, hipStream_t stream);
+
+/* ----------------------------------------------------------------------- */
 /* Introspection (tests and benchmarks)                                      */
 /* ----------------------------------------------------------------------- */
 
@@ -253,9 +307,10 @@ mlkv_status mlkv_plan(const mlkv_map* map, int layer, int batch, int capacity, i
 /* ----------------------------------------------------------------------- */
 
 /* While enabled (on the calling thread), every split-K attention kernel that
- * mlkv_decode_attention / mlkv_decode_step launches is bracketed by a pair of
- * HIP events recorded on its launch stream (the merge kernel, when one runs,
- * and the append kernel are outside the pair).  Up to max_launches launches
+ * mlkv_decode_attention / mlkv_decode_step launches, and every prefill
+ * attention kernel of mlkv_prefill_attention / mlkv_prefill_step, is
+ * bracketed by a pair of HIP events recorded on its launch stream (the merge
+ * kernel, when one runs, and the append kernels are outside the pair).  Up to max_launches launches
  * are recorded; later ones are not timed.  Creates the events (host call, not
  * for capture).  Errors: MLKV_ERR_INVALID_ARG (max_launches <= 0),
  * MLKV_ERR_HIP. */

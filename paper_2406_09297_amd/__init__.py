@@ -38,6 +38,7 @@ EXPORTS = [
     "mlkv_workspace_bytes", "mlkv_cache_append", "mlkv_decode_attention", "mlkv_decode_step",
     "mlkv_plan", "mlkv_workspace_init", "mlkv_profile_enable", "mlkv_profile_read",
     "mlkv_profile_durations", "mlkv_profile_disable", "mlkv_decode_step_rope",
+    "mlkv_cache_append_rows", "mlkv_prefill_attention", "mlkv_prefill_step",
 ]
 
 
@@ -86,6 +87,9 @@ def lib():
             "mlkv_decode_attention": ([I, P, P, P, P, P, I, I, P, Z, P], S),
             "mlkv_decode_step": ([P, P, P, P, P, P, P, I, I, P, Z, P], S),
             "mlkv_decode_step_rope": ([P, P, P, P, P, P, I, ctypes.c_double, P, I, I, P, Z, P], S),
+            "mlkv_cache_append_rows": ([I, P, P, P, P, I, I, P, P], S),
+            "mlkv_prefill_attention": ([I, P, P, P, P, I, P, I, P], S),
+            "mlkv_prefill_step": ([P, P, P, P, P, P, I, P, I, P], S),
             "mlkv_plan": ([P, I, I, I, I, I, ctypes.POINTER(I), ctypes.POINTER(I)], S),
             "mlkv_workspace_init": ([P, Z, P], S),
             "mlkv_profile_enable": ([I], S),
@@ -319,6 +323,50 @@ def decode_step(q_all: torch.Tensor, k_new_all: torch.Tensor, v_new_all: torch.T
         _check(lib().mlkv_decode_step_rope(*args, rotary_dims, float(rotary_base), *tail))
     else:
         _check(lib().mlkv_decode_step(*args, *tail))
+
+
+def cache_append_rows(layer: int, map_: Map, cache: Cache, k_new: torch.Tensor,
+                      v_new: torch.Tensor, ctx_lens: torch.Tensor, T: int,
+                      row_stride: int | None = None, stream=None):
+    """mlkv_cache_append_rows: k_new/v_new [B][T][owned][D] (or rows of
+    `row_stride` elements), stored at slots ctx_lens[b] + t."""
+    if row_stride is None:
+        row_stride = k_new[0, 0].numel()
+    _check(lib().mlkv_cache_append_rows(layer, map_.handle, cache.struct,
+                                        _dev_ptr(k_new, torch.bfloat16, "k_new"),
+                                        _dev_ptr(v_new, torch.bfloat16, "v_new"), T, row_stride,
+                                        _dev_ptr(ctx_lens, torch.int32, "ctx_lens"),
+                                        _stream(stream)))
+
+
+def prefill_attention(layer: int, q: torch.Tensor, cache: Cache, map_: Map,
+                      ctx_lens: torch.Tensor, out: torch.Tensor, stream=None):
+    """mlkv_prefill_attention: q [B][T][h][D] bf16 -> out [B][T][h][D] (fp32
+    or bf16); token t of sequence b attends positions 0 .. ctx_lens[b] + t."""
+    if out.dtype not in (torch.float32, torch.bfloat16):
+        raise ValueError("out must be float32 or bfloat16")
+    out_dt = OUT_BF16 if out.dtype == torch.bfloat16 else OUT_F32
+    _check(lib().mlkv_prefill_attention(layer, _dev_ptr(q, torch.bfloat16, "q"), cache.struct,
+                                        map_.handle, _dev_ptr(ctx_lens, torch.int32, "ctx_lens"),
+                                        q.shape[1], _dev_ptr(out, out.dtype, "out"), out_dt,
+                                        _stream(stream)))
+
+
+def prefill_step(q_all: torch.Tensor, k_new_all: torch.Tensor, v_new_all: torch.Tensor,
+                 cache: Cache, map_: Map, ctx_lens: torch.Tensor, out_all: torch.Tensor,
+                 stream=None):
+    """mlkv_prefill_step: q_all [l][B][T][h][D], k/v_new_all [B][T][n_kv][D]
+    -> out_all [l][B][T][h][D]; owners store their rows, every layer attends
+    causally."""
+    if out_all.dtype not in (torch.float32, torch.bfloat16):
+        raise ValueError("out_all must be float32 or bfloat16")
+    out_dt = OUT_BF16 if out_all.dtype == torch.bfloat16 else OUT_F32
+    _check(lib().mlkv_prefill_step(_dev_ptr(q_all, torch.bfloat16, "q_all"),
+                                   _dev_ptr(k_new_all, torch.bfloat16, "k_new_all"),
+                                   _dev_ptr(v_new_all, torch.bfloat16, "v_new_all"), cache.struct,
+                                   map_.handle, _dev_ptr(ctx_lens, torch.int32, "ctx_lens"),
+                                   q_all.shape[2], _dev_ptr(out_all, out_all.dtype, "out_all"),
+                                   out_dt, _stream(stream)))
 
 
 # ------------------------------------------------------------------ timing ---

@@ -28,6 +28,33 @@ struct AppendParams {
   int B, S, kv_begin, row_stride;
 };
 
+// Owners' rows of a prompt: row (b, t) at k_new + (b*T + t)*row_stride,
+// [owned][D]; stored at slot ctx[b] + t (skipped outside [0, S)).
+struct AppendRowsParams {
+  const uint16_t* k_new;
+  const uint16_t* v_new;
+  const int32_t* ctx;        // [B] tokens cached before the prompt
+  uint16_t* k;               // key plane
+  uint16_t* v;               // value plane
+  int B, T, S, kv_begin, row_stride;
+};
+
+// Causal prefill attention of one layer: token t of sequence b attends
+// positions 0 .. ctx[b] + t of the KV heads [kv_begin, kv_begin + n_groups).
+// A workgroup takes kPrefillRows query rows (token, head) of one KV head.
+constexpr int kPrefillRows = 64;
+struct PrefillParams {
+  const uint16_t* q;         // [B][T][h][D]
+  const uint16_t* k;         // key plane   [n_kv][B][S][D]
+  const uint16_t* v;         // value plane [n_kv][B][S/32][D][32]
+  const int32_t* ctx;        // [B] tokens cached before the prompt
+  void* out;                 // [B][T][h][D] fp32 or bf16
+  int B, T, h, S;
+  int kv_begin, G, n_groups;
+  int out_bf16;
+  float scale_log2;          // log2(e) / sqrt(D)
+};
+
 struct AttnParams {
   const uint16_t* q;         // [B][h][D]
   const uint16_t* k;         // key plane   [n_kv][B][S][D]
@@ -64,6 +91,11 @@ struct AttnParams {
 hipError_t launch_append(const AppendParams& p, int head_dim, int owned_count,
                          hipStream_t stream);
 hipError_t launch_rope(const RopeParams& p, hipStream_t stream);
+hipError_t launch_append_rows(const AppendRowsParams& p, int head_dim, int owned_count,
+                              hipStream_t stream);
+// start/stop: optional events recorded around the prefill dispatch.
+hipError_t launch_prefill(const PrefillParams& p, int head_dim, hipStream_t stream,
+                          hipEvent_t start, hipEvent_t stop);
 // The split-K attention kernel, then (when splits are merged by a separate
 // kernel) the merge.
 // start/stop: optional events recorded around the attention dispatch.

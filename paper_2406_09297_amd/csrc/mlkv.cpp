@@ -367,6 +367,89 @@ mlkv_status append_impl(int layer, const mlkv_map* map, const mlkv_cache* cache,
   return MLKV_OK;
 }
 
+mlkv_status append_rows_impl(int layer, const mlkv_map* map, const mlkv_cache* cache,
+                             const void* k_new, const void* v_new, int T, int row_stride,
+                             const int32_t* ctx_lens, hipStream_t stream) {
+  const int owned = map->own_count[layer];
+  if (owned == 0 || T == 0) return MLKV_OK;
+  mlkv::AppendRowsParams p{};
+  p.k_new = static_cast<const uint16_t*>(k_new);
+  p.v_new = static_cast<const uint16_t*>(v_new);
+  p.ctx = ctx_lens;
+  p.k = static_cast<uint16_t*>(cache->k);
+  p.v = static_cast<uint16_t*>(cache->v);
+  p.B = cache->batch;
+  p.T = T;
+  p.S = cache->capacity;
+  p.kv_begin = map->own_begin[layer];
+  p.row_stride = row_stride;
+  const hipError_t err = mlkv::launch_append_rows(p, cache->head_dim, owned, stream);
+  if (err != hipSuccess) return fail(MLKV_ERR_HIP, "append launch: %s", hipGetErrorString(err));
+  return MLKV_OK;
+}
+
+// Prefill shape checks shared by the entry points: 0 <= T <= capacity and the
+// launch grid within its limits for every layer.
+constexpr long kMaxGridY = 65535;
+mlkv_status check_prefill_shape(const mlkv_map* map, const mlkv_cache* cache, int T) {
+  if (T < 0 || T > cache->capacity)
+    return fail(MLKV_ERR_CAPACITY, "T = %d new tokens: must be in [0, capacity %d]", T,
+                cache->capacity);
+  for (int n = 0; n < map->l; ++n) {
+    const long blocks = (static_cast<long>(T) * map->group[n] + mlkv::kPrefillRows - 1) /
+                        mlkv::kPrefillRows;
+    if (blocks > kMaxGridY)
+      return fail(MLKV_ERR_UNSUPPORTED, "T * (query heads per KV head) = %ld rows: at most %ld",
+                  static_cast<long>(T) * map->group[n], kMaxGridY * mlkv::kPrefillRows);
+  }
+  return MLKV_OK;
+}
+
+// MLKV_CHECK=1: every ctx_lens[b] in [0, capacity - T] (synchronizes).
+mlkv_status check_prefill_lengths_if_requested(const int32_t* ctx, int batch, int T, int S,
+                                               hipStream_t stream) {
+  const char* env = std::getenv("MLKV_CHECK");
+  if (!env || std::strcmp(env, "1") != 0) return MLKV_OK;
+  std::vector<int32_t> host(batch);
+  if (hipStreamSynchronize(stream) != hipSuccess ||
+      hipMemcpy(host.data(), ctx, sizeof(int32_t) * batch, hipMemcpyDeviceToHost) != hipSuccess)
+    return fail(MLKV_ERR_HIP, "MLKV_CHECK: could not read lengths back");
+  for (int b = 0; b < batch; ++b)
+    if (host[b] < 0 || static_cast<long>(host[b]) + T > S)
+      return fail(MLKV_ERR_CAPACITY, "MLKV_CHECK: sequence %d has %d cached + %d new tokens, "
+                  "capacity %d", b, host[b], T, S);
+  return MLKV_OK;
+}
+
+mlkv_status prefill_impl(int layer, const void* q, const mlkv_cache* cache, const mlkv_map* map,
+                         const int32_t* ctx_lens, int T, void* out, mlkv_out_dtype dt,
+                         hipStream_t stream) {
+  if (T == 0) return MLKV_OK;
+  const int D = cache->head_dim;
+  mlkv::PrefillParams p{};
+  p.q = static_cast<const uint16_t*>(q);
+  p.k = static_cast<const uint16_t*>(cache->k);
+  p.v = static_cast<const uint16_t*>(cache->v);
+  p.ctx = ctx_lens;
+  p.out = out;
+  p.B = cache->batch;
+  p.T = T;
+  p.h = map->h;
+  p.S = cache->capacity;
+  p.kv_begin = map->kv_begin[layer];
+  p.G = map->group[layer];
+  p.n_groups = map->kv_count[layer];
+  p.out_bf16 = dt == MLKV_OUT_BF16 ? 1 : 0;
+  p.scale_log2 = static_cast<float>(1.4426950408889634 / std::sqrt(static_cast<double>(D)));
+  Profile& prof = g_profile;
+  const bool timed = prof.on && prof.used < static_cast<int>(prof.start.size());
+  const hipError_t err = mlkv::launch_prefill(p, D, stream, timed ? prof.start[prof.used] : nullptr,
+                                              timed ? prof.stop[prof.used] : nullptr);
+  if (err == hipSuccess && timed) ++prof.used;
+  if (err != hipSuccess) return fail(MLKV_ERR_HIP, "prefill launch: %s", hipGetErrorString(err));
+  return MLKV_OK;
+}
+
 mlkv_status check_group_size(const mlkv_map* map, int layer) {
   if (map->group[layer] > 16)
     return fail(MLKV_ERR_UNSUPPORTED,
@@ -706,6 +789,93 @@ mlkv_status mlkv_decode_step_rope(void* q_all, void* k_new_all, const void* v_ne
   }
   return decode_step_launch(q_all, k_new_all, v_new_all, cache, map, ctx_lens, out_all, out_dtype,
                             max_len_hint, workspace, workspace_bytes, stream);
+}
+
+mlkv_status mlkv_cache_append_rows(int layer, const mlkv_map* map, const mlkv_cache* cache,
+                                   const void* k_new, const void* v_new, int T,
+                                   int new_row_stride, const int32_t* ctx_lens,
+                                   hipStream_t stream) {
+  mlkv_status s;
+  if ((s = check_map(map)) != MLKV_OK) return s;
+  if (layer < 0 || layer >= map->l) return fail(MLKV_ERR_INVALID_ARG, "layer %d out of range", layer);
+  if ((s = check_cache(cache, map)) != MLKV_OK) return s;
+  if ((s = check_prefill_shape(map, cache, T)) != MLKV_OK) return s;
+  const int owned = map->own_count[layer];
+  if (owned == 0 || T == 0) return ok();
+  if (!k_new || !v_new || !ctx_lens)
+    return fail(MLKV_ERR_INVALID_ARG, "k_new, v_new and ctx_lens must be non-NULL");
+  if (!aligned16(k_new) || !aligned16(v_new))
+    return fail(MLKV_ERR_ALIGNMENT, "k_new and v_new must be 16-byte aligned");
+  if (!aligned4(ctx_lens)) return fail(MLKV_ERR_ALIGNMENT, "ctx_lens must be 4-byte aligned");
+  if (new_row_stride % 8 != 0 || new_row_stride < owned * cache->head_dim)
+    return fail(MLKV_ERR_INVALID_ARG, "new_row_stride %d must be a multiple of 8 and >= %d",
+                new_row_stride, owned * cache->head_dim);
+  if ((s = check_prefill_lengths_if_requested(ctx_lens, cache->batch, T, cache->capacity,
+                                              stream)) != MLKV_OK)
+    return s;
+  if ((s = append_rows_impl(layer, map, cache, k_new, v_new, T, new_row_stride, ctx_lens,
+                            stream)) != MLKV_OK)
+    return s;
+  return ok();
+}
+
+mlkv_status mlkv_prefill_attention(int layer, const void* q, const mlkv_cache* cache,
+                                   const mlkv_map* map, const int32_t* ctx_lens, int T, void* out,
+                                   mlkv_out_dtype out_dtype, hipStream_t stream) {
+  mlkv_status s;
+  if ((s = check_map(map)) != MLKV_OK) return s;
+  if (layer < 0 || layer >= map->l) return fail(MLKV_ERR_INVALID_ARG, "layer %d out of range", layer);
+  if ((s = check_cache(cache, map)) != MLKV_OK) return s;
+  if ((s = check_prefill_shape(map, cache, T)) != MLKV_OK) return s;
+  if (!q || !ctx_lens || !out) return fail(MLKV_ERR_INVALID_ARG, "q, ctx_lens, out must be non-NULL");
+  if (!aligned16(q) || !aligned16(out)) return fail(MLKV_ERR_ALIGNMENT, "q and out must be 16-byte aligned");
+  if (!aligned4(ctx_lens)) return fail(MLKV_ERR_ALIGNMENT, "ctx_lens must be 4-byte aligned");
+  if (out_dtype != MLKV_OUT_F32 && out_dtype != MLKV_OUT_BF16)
+    return fail(MLKV_ERR_INVALID_ARG, "bad out_dtype");
+  if ((s = check_prefill_lengths_if_requested(ctx_lens, cache->batch, T, cache->capacity,
+                                              stream)) != MLKV_OK)
+    return s;
+  if ((s = prefill_impl(layer, q, cache, map, ctx_lens, T, out, out_dtype, stream)) != MLKV_OK)
+    return s;
+  return ok();
+}
+
+mlkv_status mlkv_prefill_step(const void* q_all, const void* k_new_all, const void* v_new_all,
+                              const mlkv_cache* cache, const mlkv_map* map,
+                              const int32_t* ctx_lens, int T, void* out_all,
+                              mlkv_out_dtype out_dtype, hipStream_t stream) {
+  mlkv_status s;
+  if ((s = check_map(map)) != MLKV_OK) return s;
+  if ((s = check_cache(cache, map)) != MLKV_OK) return s;
+  if ((s = check_prefill_shape(map, cache, T)) != MLKV_OK) return s;
+  if (!q_all || !k_new_all || !v_new_all || !ctx_lens || !out_all)
+    return fail(MLKV_ERR_INVALID_ARG, "q_all, k_new_all, v_new_all, ctx_lens, out_all must be non-NULL");
+  if (!aligned16(q_all) || !aligned16(k_new_all) || !aligned16(v_new_all) || !aligned16(out_all))
+    return fail(MLKV_ERR_ALIGNMENT, "q_all, k/v_new_all and out_all must be 16-byte aligned");
+  if (!aligned4(ctx_lens)) return fail(MLKV_ERR_ALIGNMENT, "ctx_lens must be 4-byte aligned");
+  if (out_dtype != MLKV_OUT_F32 && out_dtype != MLKV_OUT_BF16)
+    return fail(MLKV_ERR_INVALID_ARG, "bad out_dtype");
+  if ((s = check_prefill_lengths_if_requested(ctx_lens, cache->batch, T, cache->capacity,
+                                              stream)) != MLKV_OK)
+    return s;
+  const int B = cache->batch, h = map->h, D = cache->head_dim, n_kv = map->n_kv;
+  const size_t layer_elems = static_cast<size_t>(B) * T * h * D;
+  const size_t out_elem_bytes = out_dtype == MLKV_OUT_BF16 ? 2 : 4;
+  const uint16_t* k_new = static_cast<const uint16_t*>(k_new_all);
+  const uint16_t* v_new = static_cast<const uint16_t*>(v_new_all);
+  for (int n = 0; n < map->l; ++n) {
+    if (map->own_count[n] > 0) {
+      const size_t col = static_cast<size_t>(map->own_begin[n]) * D;
+      if ((s = append_rows_impl(n, map, cache, k_new + col, v_new + col, T, n_kv * D, ctx_lens,
+                                stream)) != MLKV_OK)
+        return s;
+    }
+    const void* q = static_cast<const uint16_t*>(q_all) + layer_elems * n;
+    void* out = static_cast<char*>(out_all) + layer_elems * out_elem_bytes * n;
+    if ((s = prefill_impl(n, q, cache, map, ctx_lens, T, out, out_dtype, stream)) != MLKV_OK)
+      return s;
+  }
+  return ok();
 }
 
 mlkv_status mlkv_profile_enable(int max_launches) {

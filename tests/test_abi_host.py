@@ -144,6 +144,48 @@ def test_entry_points_reject_bad_arguments():
     assert names[L.mlkv_decode_attention(0, 0x30000, ctypes.byref(c2), mq.handle, 0x40000, 0x50000, 0, 0, 0x60000, 1 << 30, None)] == "MLKV_ERR_UNSUPPORTED"
 
 
+def test_prefill_entry_points_reject_bad_arguments():
+    """Prefill argument checks happen on the host before any HIP call."""
+    mp = mlkv.Map.uniform(12, 12, 4, 1)
+    ref, _keep = _fake_cache()          # B=2, S=64, D=64
+    L = mlkv.lib()
+    names = mlkv.STATUS_NAMES
+    F = mlkv.OUT_F32
+    # T above the capacity, negative T
+    assert names[L.mlkv_prefill_step(0x30000, 0x30000, 0x30000, ref, mp.handle, 0x40000, 65,
+                                     0x50000, F, None)] == "MLKV_ERR_CAPACITY"
+    assert names[L.mlkv_prefill_step(0x30000, 0x30000, 0x30000, ref, mp.handle, 0x40000, -1,
+                                     0x50000, F, None)] == "MLKV_ERR_CAPACITY"
+    # null pointers, misalignment, bad dtype
+    assert names[L.mlkv_prefill_step(None, 0x30000, 0x30000, ref, mp.handle, 0x40000, 4,
+                                     0x50000, F, None)] == "MLKV_ERR_INVALID_ARG"
+    assert names[L.mlkv_prefill_step(0x30008, 0x30000, 0x30000, ref, mp.handle, 0x40000, 4,
+                                     0x50000, F, None)] == "MLKV_ERR_ALIGNMENT"
+    assert names[L.mlkv_prefill_step(0x30000, 0x30000, 0x30000, ref, mp.handle, 0x40002, 4,
+                                     0x50000, F, None)] == "MLKV_ERR_ALIGNMENT"
+    assert names[L.mlkv_prefill_step(0x30000, 0x30000, 0x30000, ref, mp.handle, 0x40000, 4,
+                                     0x50000, 7, None)] == "MLKV_ERR_INVALID_ARG"
+    assert names[L.mlkv_prefill_attention(12, 0x30000, ref, mp.handle, 0x40000, 4, 0x50000, F,
+                                          None)] == "MLKV_ERR_INVALID_ARG"
+    assert names[L.mlkv_prefill_attention(0, 0x30000, ref, mp.handle, None, 4, 0x50000, F,
+                                          None)] == "MLKV_ERR_INVALID_ARG"
+    assert names[L.mlkv_cache_append_rows(0, mp.handle, ref, 0x30000, 0x30000, 4, 60, 0x40000,
+                                          None)] == "MLKV_ERR_INVALID_ARG"
+    assert names[L.mlkv_cache_append_rows(0, mp.handle, ref, 0x30008, 0x30000, 4, 64, 0x40000,
+                                          None)] == "MLKV_ERR_ALIGNMENT"
+    # a layer that owns nothing, and T = 0: nothing to do, no HIP call
+    assert names[L.mlkv_cache_append_rows(1, mp.handle, ref, None, None, 4, 0, None,
+                                          None)] == "MLKV_OK"
+    assert names[L.mlkv_prefill_step(0x30000, 0x30000, 0x30000, ref, mp.handle, 0x40000, 0,
+                                     0x50000, F, None)] == "MLKV_OK"
+    # more query rows per KV head than the launch grid holds: 64 heads per KV
+    # head x 70000 tokens
+    mq = mlkv.Map.uniform(1, 64, 1, 1)
+    big = mlkv._Cache(0x10000, 0x20000, 1, 1, 1 << 17, 64)
+    assert names[L.mlkv_prefill_step(0x30000, 0x30000, 0x30000, ctypes.byref(big), mq.handle,
+                                     0x40000, 70000, 0x50000, F, None)] == "MLKV_ERR_UNSUPPORTED"
+
+
 @pytest.mark.parametrize("env", [{}, {"MLKV_WIDE": "1"}, {"MLKV_WIDE": "0"},
                                  {"MLKV_COMBINE": "fused"}, {"MLKV_WORKGROUPS": "5"},
                                  {"MLKV_WORKGROUPS": "100000", "MLKV_WIDE": "0"}])
