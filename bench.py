@@ -13,6 +13,11 @@ Prints ONE JSON line:
   CPU-oracle baseline on the host cores.
 
   python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cold]
+
+A workload with T > 1 new tokens per sequence (prefill_b8_2000) runs the
+prefill instead (mlkv_prefill_step: owners store the prompt's rows, every
+layer attends causally): value = algorithmic attention TFLOP/s, with the
+prefill kernel's roofline against the bf16 matrix-core peak.
 """
 from __future__ import annotations
 
@@ -32,19 +37,30 @@ HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published
 DEFAULT_WORKLOAD = "mlkv4_b128_ragged"
 REF_COPY_BYTES = 256 << 20
 SLEEP_CYCLES = 40_000_000  # ~17 ms at 2.4 GHz: longer than the host needs to enqueue 10 steps
+MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix cores, published
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attention_kernel_traffic.md")
-KERNEL_SOURCE = os.path.join(ROOT, "paper_2406_09297_amd", "csrc", "kernels.hip")
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2406_09297_amd", "csrc", f)
+                  for f in ("kernels.hip", "tile.h")]
+
+
+def kernel_source_sha256() -> str:
+    """SHA-256 over the decode kernels' sources (kernels.hip then tile.h)."""
+    import hashlib
+
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
 
 
 def measured_traffic(workload: str):
     """HBM bytes per attention launch from the committed rocprofv3 counter
     summary, or None if it does not cover this workload or the kernel source
     changed since the counters were taken."""
-    import hashlib
-
     try:
         text = open(TRAFFIC_FILE).read()
-        sha = hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest()
+        sha = kernel_source_sha256()
     except OSError:
         return None
     fields = {}
@@ -107,6 +123,135 @@ def cpu_baseline(w, inp, kv_of, owner_of, bytes_per_step, budget_s=12.0, rotary=
                       f"OpenMP over (sequence, head)), {spent:.1f} s"}
 
 
+def prefill_flops(w, ctx):
+    """Algorithmic flops of one prefill (all layers): every (query row, key
+    position) pair the causal mask admits costs 2*D for q.k and 2*D for the
+    weighted value sum."""
+    pairs = sum(int(c) * w.T + w.T * (w.T + 1) // 2 for c in ctx)  # per query head
+    return w.l * w.h * pairs * 4 * w.D
+
+
+def run_prefill(args, w):
+    import torch
+    import synth
+    import paper_2406_09297_amd as mlkv
+
+    dev = "cuda:0"
+    log(f"[bench] prefill workload {w.name}: generating inputs")
+    inp = synth.prefill_inputs(w, fill=0)
+    S = inp["capacity"]
+    mp = mlkv.Map.uniform(w.l, w.h, w.m, w.g)
+    cache = mlkv.Cache.empty(w.n_kv, w.B, S, w.D, dev)
+    log("[bench] uploading")
+    cache.load_rows(inp["k_cache"], inp["v_cache"])
+    q = mlkv.bf16_tensor(inp["q"], dev)
+    kn = mlkv.bf16_tensor(inp["k_new"], dev)
+    vn = mlkv.bf16_tensor(inp["v_new"], dev)
+    ctx = torch.from_numpy(inp["ctx"]).to(dev)
+    out = torch.empty((w.l, w.B, w.T, w.h, w.D), dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream()
+    flops = prefill_flops(w, inp["ctx"])
+    tokens = w.B * w.T
+
+    def one_step():
+        mlkv.prefill_step(q, kn, vn, cache, mp, ctx, out)
+
+    if args.pmc_pass:  # counter pass: one warm prefill, then two in the timed configuration
+        for _ in range(3):
+            one_step()
+        torch.cuda.synchronize()
+        log("[bench] pmc pass done")
+        return
+
+    log(f"[bench] warmup {args.warmup}")
+    for _ in range(args.warmup):
+        one_step()
+    torch.cuda.synchronize()
+    log(f"[bench] timing {args.steps} prefills")
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(args.steps):
+        one_step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms_step = e0.elapsed_time(e1) / args.steps
+
+    log("[bench] timing prefill kernels (event pairs)")
+    mlkv.profile_enable(args.steps * w.l)
+    torch.cuda.synchronize()
+    done = 0
+    while done < args.steps:
+        n = min(10, args.steps - done)
+        torch.cuda._sleep(SLEEP_CYCLES)
+        for _ in range(n):
+            one_step()
+        torch.cuda.synchronize()
+        done += n
+    n_launch, tot_ms, min_ms, max_ms = mlkv.profile_read()
+    durations = mlkv.profile_durations(n_launch)
+    mlkv.profile_disable()
+    avg = tot_ms * 1e-3 / n_launch
+    p10, p50, p90 = (float(np.percentile(durations, pq)) for pq in (10, 50, 90))
+    flops_launch = flops / w.l
+    achieved = flops_launch / avg / 1e12
+    result = {
+        "metric": "prefill-attention TFLOP/s (% of bf16 MFMA peak) + prompt tokens/s, "
+                  "MLKV Pythia-160M shape",
+        "value": round(flops / (ms_step * 1e-3) / 1e12, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "prompt_tokens_per_s": round(tokens / (ms_step * 1e-3), 0),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded N(0,1) bf16 q/K/V; no weights)",
+        "config": {"workload": w.name, "l": w.l, "h": w.h, "m": w.m, "g": w.g, "head_dim": w.D,
+                   "batch": w.B, "ctx": w.ctx, "new_tokens": w.T, "capacity": S,
+                   "flops_per_step": int(flops)},
+        "roofline": {"bound": "mfma", "achieved": round(achieved, 2),
+                     "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": None,
+                     "kernel": "prefill_kernel", "avg_launch_us": round(avg * 1e6, 2),
+                     "min_launch_us": round(min_ms * 1e3, 2),
+                     "max_launch_us": round(max_ms * 1e3, 2),
+                     "p10_p50_p90_launch_us": [round(p10 * 1e3, 2), round(p50 * 1e3, 2),
+                                               round(p90 * 1e3, 2)],
+                     "launches": n_launch, "flops_per_launch": int(flops_launch)},
+    }
+    if not args.no_cpu_baseline:
+        log("[bench] cpu baseline (oracle)")
+        import oracle
+
+        kv_of, _ = oracle.map_uniform(w.l, w.h, w.m, w.g)
+        # Bounded sample: layer 0 of the first sequence (its owners' rows
+        # stored first), repeated for about 10 s.
+        k, v = inp["k_cache"][:, :1].copy(), inp["v_cache"][:, :1].copy()
+        _, owner_of = oracle.map_uniform(w.l, w.h, w.m, w.g)
+        oracle.append_rows(0, k, v, inp["k_new"][:1], inp["v_new"][:1], owner_of, inp["ctx"][:1])
+        one = w.__class__(w.name, w.l, w.h, w.m, w.g, w.D, 1, w.ctx, w.ctx_range, w.k_scale,
+                          w.seed, w.note, T=w.T)
+        sample_flops = prefill_flops(one, inp["ctx"][:1]) / w.l
+        threads = int(os.environ.get("OMP_NUM_THREADS", len(os.sched_getaffinity(0))))
+        runs, spent = 0, 0.0
+        while spent < 10.0 or runs == 0:
+            ts = time.perf_counter()
+            oracle.prefill_attention(0, inp["q"][0, :1], k, v, kv_of, inp["ctx"][:1])
+            spent += time.perf_counter() - ts
+            runs += 1
+        result["cpu_baseline"] = {
+            "value": round(sample_flops * runs / spent / 1e12, 6), "unit": "TFLOP/s",
+            "cores": threads, "kind": "oracle",
+            "prompt_tokens_per_s": round(w.T * runs / spent / w.l, 1),
+            "sample": f"{runs} x layer 0 of one sequence ({w.T} tokens, fp64 oracle, "
+                      f"OpenMP over (token, head)), {spent:.1f} s; tokens/s scaled to all "
+                      f"{w.l} layers"}
+    print(json.dumps(result), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -140,6 +285,9 @@ def main():
     dev = "cuda:0"
     torch.cuda.set_device(0)
     w = synth.get_workload(args.workload)
+    if w.T > 1:
+        run_prefill(args, w)
+        return
     if args.map:
         m, g = (int(x) for x in args.map.split(","))
         w = w.with_map(m, g)

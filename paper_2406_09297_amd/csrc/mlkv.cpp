@@ -395,12 +395,12 @@ mlkv_status check_prefill_shape(const mlkv_map* map, const mlkv_cache* cache, in
   if (T < 0 || T > cache->capacity)
     return fail(MLKV_ERR_CAPACITY, "T = %d new tokens: must be in [0, capacity %d]", T,
                 cache->capacity);
+  const long per_wg = mlkv::prefill_rows_per_workgroup(cache->head_dim);
   for (int n = 0; n < map->l; ++n) {
-    const long blocks = (static_cast<long>(T) * map->group[n] + mlkv::kPrefillRows - 1) /
-                        mlkv::kPrefillRows;
+    const long blocks = (static_cast<long>(T) * map->group[n] + per_wg - 1) / per_wg;
     if (blocks > kMaxGridY)
       return fail(MLKV_ERR_UNSUPPORTED, "T * (query heads per KV head) = %ld rows: at most %ld",
-                  static_cast<long>(T) * map->group[n], kMaxGridY * mlkv::kPrefillRows);
+                  static_cast<long>(T) * map->group[n], kMaxGridY * per_wg);
   }
   return MLKV_OK;
 }

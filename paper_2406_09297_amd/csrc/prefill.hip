@@ -21,17 +21,101 @@ namespace mlkv {
 // ---------------------------------------------------------------------------
 // Prefill (Section 2.4's cache filled from a prompt, causal): T new tokens per
 // sequence.  Unit (b, r) has T*G query rows, row rho = t*G + hh (token t,
-// query head hh of KV group r).  A workgroup takes 64 consecutive rows, 16 per
-// wave as the MFMA columns; each wave streams the key/value tiles from
-// position 0 to its last row's limit with its own online softmax (the same
-// tile arithmetic as decode: S^T = K Q^T, O^T += V^T P^T), so there is no
-// split over tokens and nothing to merge.  Token t attends positions
-// 0 .. ctx_b + t; only the tiles from the wave's smallest limit on are masked.
-// Grid: x = unit, y = block of 64 rows, heaviest blocks (latest tokens) first.
+// query head hh of KV group r).  A wave takes NB blocks of 16 consecutive
+// rows (the MFMA columns) and streams the key/value tiles from position 0 to
+// its last row's limit with one online softmax per block (the tile
+// arithmetic of decode: S^T = K Q^T, O^T += V^T P^T); each tile's key and
+// value registers serve all NB blocks, so a loaded byte feeds NB times the
+// matrix work.  Nothing is split over tokens, nothing is merged.  Token t
+// attends positions 0 .. ctx_b + t; only the tiles from the wave's smallest
+// limit on are masked.  A workgroup is four waves (64*NB consecutive rows).
+// Grid: x = unit, y = row block, heaviest blocks (latest tokens) first.
 // ---------------------------------------------------------------------------
-template <int D>
-__global__ __launch_bounds__(256) void prefill_kernel(PrefillParams p) {
+// One 32-token tile against the wave's NB column blocks.  The tile's key and
+// value registers serve every block.  Phases: the scores of all blocks
+// (MFMA); the causal mask (MASK: the tile may cross some column's limit);
+// one wave-wide vote on whether any score exceeds its column's reference max
+// by more than kLazyRescale (each lane tests its own eight scores, so the
+// common case needs no cross-lane traffic); on a yes, the column maxima
+// through the wave and the rescale of the blocks that need it; then the
+// weights and the value products of all blocks.
+template <int D, int NB, bool MASK>
+__device__ __forceinline__ void prefill_tile(WaveState<D> (&st)[NB], Tile<D>& t,
+                                             const bf16x8 (&qf)[NB][Tile<D>::KK], int t0, int L,
+                                             const int (&lim)[NB], int grp, float scale_log2) {
   constexpr int KK = Tile<D>::KK, DB = Tile<D>::DB;
+  float x[NB][8];
+#pragma unroll
+  for (int c = 0; c < NB; ++c) {
+    f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) {
+      s0 = mfma_bf16(as_bf16(t.k[0][kk]), qf[c][kk], s0);
+      s1 = mfma_bf16(as_bf16(t.k[1][kk]), qf[c][kk], s1);
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      x[c][i] = s0[i];
+      x[c][4 + i] = s1[i];
+    }
+  }
+  if (MASK) {  // positions past a column's limit take no weight, positions >= L no value
+    const int first = t0 + grp * 8;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+#pragma unroll
+      for (int c = 0; c < NB; ++c)
+        if (first + e > lim[c]) x[c][e] = -INFINITY;
+      if (first + e >= L) {
+#pragma unroll
+        for (int db = 0; db < DB; ++db) t.v[db][e] = 0;
+      }
+    }
+  }
+  float lmax[NB];
+  bool up = false;
+#pragma unroll
+  for (int c = 0; c < NB; ++c) {
+    lmax[c] = fmaxf(fmaxf(fmaxf(x[c][0], x[c][1]), fmaxf(x[c][2], x[c][3])),
+                    fmaxf(fmaxf(x[c][4], x[c][5]), fmaxf(x[c][6], x[c][7])));
+    up = up || fmaf(lmax[c], scale_log2, -st[c].m) > kLazyRescale;
+  }
+  if (__ballot(up)) {  // some column needs a new reference max
+#pragma unroll
+    for (int c = 0; c < NB; ++c) {
+      float cm = fmaxf(lmax[c], __shfl_xor(lmax[c], 16));
+      cm = fmaxf(cm, __shfl_xor(cm, 32)) * scale_log2;
+      const bool raise = cm > st[c].m + kLazyRescale;  // uniform over the column's lanes
+      if (__ballot(raise)) {
+        const float m_new = raise ? cm : st[c].m;
+        const float alpha = fast_exp2(st[c].m - m_new);  // 0 on the first tile
+        st[c].m = m_new;
+        st[c].den *= alpha;
+#pragma unroll
+        for (int db = 0; db < DB; ++db) st[c].acc[db] *= alpha;
+      }
+    }
+  }
+  const u16x8 ones = {0x3F80, 0x3F80, 0x3F80, 0x3F80, 0x3F80, 0x3F80, 0x3F80, 0x3F80};
+#pragma unroll
+  for (int c = 0; c < NB; ++c) {
+    u16x8 pbits;
+    const float neg_m = -st[c].m;
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+      pbits[e] = f32_to_bf16_bits(fast_exp2(fmaf(x[c][e], scale_log2, neg_m)));
+    const bf16x8 pf = as_bf16(pbits);
+    st[c].den = mfma_bf16(as_bf16(ones), pf, st[c].den);
+#pragma unroll
+    for (int db = 0; db < DB; ++db) st[c].acc[db] = mfma_bf16(as_bf16(t.v[db]), pf, st[c].acc[db]);
+  }
+}
+
+template <int D, int NB>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(D == 64 ? 2 : 1)))
+void prefill_kernel(PrefillParams p) {
+  constexpr int KK = Tile<D>::KK, DB = Tile<D>::DB;
+  constexpr int WAVE_ROWS = 16 * NB;
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int col = lane & 15;
@@ -41,16 +125,11 @@ __global__ __launch_bounds__(256) void prefill_kernel(PrefillParams p) {
   const int r = unit - b * p.n_groups;
   const int rows = p.T * p.G;
   const int blk = gridDim.y - 1 - blockIdx.y;
-  const int row0 = blk * kPrefillRows + wave * 16;
+  const int row0 = (blk * 4 + wave) * WAVE_ROWS;
   if (row0 >= rows) return;  // no barrier below: a wave past the end leaves alone
-  const int rho = row0 + col;
-  const bool valid = rho < rows;
-  const int t = valid ? rho / p.G : 0;
-  const int hh = valid ? rho - t * p.G : 0;
   const int c0 = max(p.ctx[b], 0);
-  const int L = min(c0 + p.T, p.S);          // filled positions of the sequence
-  const int lim = min(c0 + t, p.S - 1);       // last position this column attends
-  const int last_row = min(row0 + 15, rows - 1);
+  const int L = min(c0 + p.T, p.S);  // filled positions of the sequence
+  const int last_row = min(row0 + WAVE_ROWS - 1, rows - 1);
   const int lim_max = min(c0 + last_row / p.G, p.S - 1);
   const int lim_min = min(c0 + row0 / p.G, p.S - 1);
   const int n_tiles = lim_max / kTile + 1;
@@ -63,29 +142,37 @@ __global__ __launch_bounds__(256) void prefill_kernel(PrefillParams p) {
 
   Tile<D> ta, tb;
   load_tile<D, false>(ta, kbase, vbase, 0, col, grp);
-  bf16x8 qf[KK];
-  {
+
+  // Column block c: row row0 + 16c + col, its token, head and causal limit.
+  bool valid[NB];
+  int tok[NB], head[NB], lim[NB];
+  bf16x8 qf[NB][KK];
+  WaveState<D> st[NB];
+#pragma unroll
+  for (int c = 0; c < NB; ++c) {
+    const int rho = row0 + 16 * c + col;
+    valid[c] = rho < rows;
+    tok[c] = valid[c] ? rho / p.G : 0;
+    head[c] = valid[c] ? rho - tok[c] * p.G : 0;
+    lim[c] = min(c0 + tok[c], p.S - 1);
     const uint16_t* qrow =
-        p.q + ((static_cast<size_t>(b) * p.T + t) * p.h + r * p.G + hh) * D + grp * 8;
+        p.q + ((static_cast<size_t>(b) * p.T + tok[c]) * p.h + r * p.G + head[c]) * D + grp * 8;
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
       const u16x8 v = load16(qrow + kk * 32);
       const u16x8 zero = {0, 0, 0, 0, 0, 0, 0, 0};
-      qf[kk] = as_bf16(valid ? v : zero);  // rows past the end: scores 0, output unused
+      qf[c][kk] = as_bf16(valid[c] ? v : zero);  // rows past the end: scores 0, output unused
     }
-  }
-  WaveState<D> st;
-  st.den = f32x4{0.f, 0.f, 0.f, 0.f};
+    st[c].den = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-  for (int db = 0; db < DB; ++db) st.acc[db] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int db = 0; db < DB; ++db) st[c].acc[db] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
 
   auto process = [&](Tile<D>& tile, int it) {
     if (it >= first_masked)
-      process_tile<D, true, false, true>(st, tile, qf, it * kTile, L, col, grp, p.scale_log2, -1,
-                                         nullptr, nullptr, nullptr, 16, lim);
+      prefill_tile<D, NB, true>(st, tile, qf, it * kTile, L, lim, grp, p.scale_log2);
     else
-      process_tile<D, false, false, true>(st, tile, qf, it * kTile, L, col, grp, p.scale_log2,
-                                          -1, nullptr, nullptr, nullptr, 16, lim);
+      prefill_tile<D, NB, false>(st, tile, qf, it * kTile, L, lim, grp, p.scale_log2);
   };
   int it = 0;
   for (;;) {  // tile it is in ta; the next one's loads go out before it is used
@@ -97,21 +184,27 @@ __global__ __launch_bounds__(256) void prefill_kernel(PrefillParams p) {
     if (++it >= n_tiles) break;
   }
 
-  if (!valid) return;
-  // Lane (col, grp) holds channels db*16 + 4*grp .. +3 of its row.
-  const float inv = 1.f / st.den[0];
-  const size_t orow = ((static_cast<size_t>(b) * p.T + t) * p.h + r * p.G + hh) * D;
+  // Lane (col, grp) holds channels db*16 + 4*grp .. +3 of its row in each block.
 #pragma unroll
-  for (int db = 0; db < DB; ++db) {
-    const f32x4 o = st.acc[db] * inv;
-    const size_t off = orow + db * 16 + grp * 4;
-    if (p.out_bf16) {
-      uint16_t* dst = static_cast<uint16_t*>(p.out) + off;
-      const uint32_t lo = f32_to_bf16_bits(o[0]) | (static_cast<uint32_t>(f32_to_bf16_bits(o[1])) << 16);
-      const uint32_t hi = f32_to_bf16_bits(o[2]) | (static_cast<uint32_t>(f32_to_bf16_bits(o[3])) << 16);
-      *reinterpret_cast<uint2*>(dst) = make_uint2(lo, hi);
-    } else {
-      *reinterpret_cast<f32x4*>(static_cast<float*>(p.out) + off) = o;
+  for (int c = 0; c < NB; ++c) {
+    if (!valid[c]) continue;
+    const float inv = 1.f / st[c].den[0];
+    const size_t orow =
+        ((static_cast<size_t>(b) * p.T + tok[c]) * p.h + r * p.G + head[c]) * D;
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      const f32x4 o = st[c].acc[db] * inv;
+      const size_t off = orow + db * 16 + grp * 4;
+      if (p.out_bf16) {
+        uint16_t* dst = static_cast<uint16_t*>(p.out) + off;
+        const uint32_t lo =
+            f32_to_bf16_bits(o[0]) | (static_cast<uint32_t>(f32_to_bf16_bits(o[1])) << 16);
+        const uint32_t hi =
+            f32_to_bf16_bits(o[2]) | (static_cast<uint32_t>(f32_to_bf16_bits(o[3])) << 16);
+        *reinterpret_cast<uint2*>(dst) = make_uint2(lo, hi);
+      } else {
+        *reinterpret_cast<f32x4*>(static_cast<float*>(p.out) + off) = o;
+      }
     }
   }
 }
@@ -141,9 +234,11 @@ __global__ __launch_bounds__(256) void append_rows_kernel(AppendRowsParams p) {
 
 hipError_t launch_prefill(const PrefillParams& p, int head_dim, hipStream_t stream,
                           hipEvent_t start, hipEvent_t stop) {
-  const int blocks = (p.T * p.G + kPrefillRows - 1) / kPrefillRows;
+  const int per_wg = prefill_rows_per_workgroup(head_dim);
+  const int blocks = (p.T * p.G + per_wg - 1) / per_wg;
   const dim3 grid(p.B * p.n_groups, blocks);
-  auto kernel = head_dim == 64 ? prefill_kernel<64> : prefill_kernel<128>;
+  auto kernel = head_dim == 64 ? prefill_kernel<64, prefill_wave_blocks(64)>
+                               : prefill_kernel<128, prefill_wave_blocks(128)>;
   if (start || stop) {
     hipExtLaunchKernelGGL(kernel, grid, dim3(256), 0, stream, start, stop, 0, p);
   } else {
