@@ -237,8 +237,8 @@ mlkv_status mlkv_decode_step_rope(void* q_all, void* k_new_all, const void* v_ne
  *   a kernel leave the cache (slots outside [0, capacity) are not written,
  *   positions are clamped to the capacity), but their results are unspecified.
  * T: 0 <= T <= capacity (else MLKV_ERR_CAPACITY); T = 0 does nothing.
- *   T times the query heads per KV head must not exceed 16,776,960 for
- *   head_dim 64 and 8,388,480 for 128 (65535 workgroups of 256 / 128 query
+ *   T times the query heads per KV head must not exceed 8,388,480 for
+ *   head_dim 64 and 4,194,240 for 128 (65535 workgroups of 128 / 64 query
  *   rows; else MLKV_ERR_UNSUPPORTED).  Any group size is accepted (no
  *   16-head limit).
  * No workspace: each query row is finished by one wave.

@@ -43,7 +43,7 @@ struct AppendRowsParams {
 // positions 0 .. ctx[b] + t of the KV heads [kv_begin, kv_begin + n_groups).
 // A prefill wave takes prefill_wave_blocks(D) blocks of 16 query rows (token,
 // head) of one KV head; a workgroup is four such waves.
-constexpr int prefill_wave_blocks(int head_dim) { return head_dim == 64 ? 4 : 2; }
+constexpr int prefill_wave_blocks(int head_dim) { return head_dim == 64 ? 2 : 1; }
 constexpr int prefill_rows_per_workgroup(int head_dim) {
   return 4 * 16 * prefill_wave_blocks(head_dim);
 }

@@ -111,11 +111,76 @@ __device__ __forceinline__ void prefill_tile(WaveState<D> (&st)[NB], Tile<D>& t,
   }
 }
 
+// Key/value tiles staged in LDS, shared by the workgroup's four waves: key
+// rows padded to D + 8 and value channel rows (32 tokens) to 40 elements, so
+// that the sixteen lanes reading sixteen rows at one offset hit distinct
+// banks.
+template <int D>
+struct PrefillTileLds {
+  static constexpr int KSTR = D + 8;
+  static constexpr int VSTR = kTile + 8;
+  alignas(16) uint16_t k[kTile * KSTR];
+  alignas(16) uint16_t v[D * VSTR];
+};
+
+// Global -> register staging of one tile: thread i holds CH 16-byte chunks
+// of the key rows and CH of the value block (CH = D / 64).
+template <int D>
+struct TileStage {
+  static constexpr int CH = D / 64;
+  u16x8 k[CH], v[CH];
+};
+
+template <int D>
+__device__ __forceinline__ void stage_load(TileStage<D>& s, const uint16_t* kbase,
+                                           const uint16_t* vbase, int t0) {
+#pragma unroll
+  for (int u = 0; u < TileStage<D>::CH; ++u) {
+    const int idx = threadIdx.x + u * 256;  // chunk of the tile's 4*D (K) and 4*D (V) chunks
+    s.k[u] = load16(kbase + static_cast<size_t>(t0) * D + idx * 8);
+    s.v[u] = load16(vbase + static_cast<size_t>(t0) * D + idx * 8);
+  }
+}
+
+template <int D>
+__device__ __forceinline__ void stage_store(const TileStage<D>& s, PrefillTileLds<D>& lds) {
+#pragma unroll
+  for (int u = 0; u < TileStage<D>::CH; ++u) {
+    const int idx = threadIdx.x + u * 256;
+    // key chunk idx: row idx / (D/8), channels (idx % (D/8)) * 8
+    const int kr = idx / (D / 8), kc = idx - kr * (D / 8);
+    *reinterpret_cast<u16x8*>(&lds.k[kr * PrefillTileLds<D>::KSTR + kc * 8]) = s.k[u];
+    // value chunk idx: channel idx / 4, tokens (idx % 4) * 8 (channel-major block)
+    const int vc = idx >> 2, vp = idx & 3;
+    *reinterpret_cast<u16x8*>(&lds.v[vc * PrefillTileLds<D>::VSTR + vp * 8]) = s.v[u];
+  }
+}
+
+// A wave's MFMA operands of one tile from LDS (the same register layout as
+// load_tile: permuted key rows, V^T rows).
+template <int D>
+__device__ __forceinline__ void tile_from_lds(Tile<D>& t, const PrefillTileLds<D>& lds, int col,
+                                              int grp) {
+#pragma unroll
+  for (int sb = 0; sb < 2; ++sb) {
+    const int tok = (col >> 2) * 8 + sb * 4 + (col & 3);
+#pragma unroll
+    for (int kk = 0; kk < Tile<D>::KK; ++kk)
+      t.k[sb][kk] = *reinterpret_cast<const u16x8*>(
+          &lds.k[tok * PrefillTileLds<D>::KSTR + grp * 8 + kk * 32]);
+  }
+#pragma unroll
+  for (int db = 0; db < Tile<D>::DB; ++db)
+    t.v[db] = *reinterpret_cast<const u16x8*>(
+        &lds.v[(db * 16 + col) * PrefillTileLds<D>::VSTR + grp * 8]);
+}
+
 template <int D, int NB>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(D == 64 ? 2 : 1)))
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(D == 64 ? 4 : 2)))
 void prefill_kernel(PrefillParams p) {
   constexpr int KK = Tile<D>::KK, DB = Tile<D>::DB;
   constexpr int WAVE_ROWS = 16 * NB;
+  __shared__ PrefillTileLds<D> lds[2];
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int col = lane & 15;
@@ -125,14 +190,18 @@ void prefill_kernel(PrefillParams p) {
   const int r = unit - b * p.n_groups;
   const int rows = p.T * p.G;
   const int blk = gridDim.y - 1 - blockIdx.y;
-  const int row0 = (blk * 4 + wave) * WAVE_ROWS;
-  if (row0 >= rows) return;  // no barrier below: a wave past the end leaves alone
+  const int wg_row0 = blk * 4 * WAVE_ROWS;  // < rows: the grid has no empty workgroup
+  const int row0 = wg_row0 + wave * WAVE_ROWS;
+  const bool active = row0 < rows;  // a wave past the end still stages tiles and syncs
   const int c0 = max(p.ctx[b], 0);
   const int L = min(c0 + p.T, p.S);  // filled positions of the sequence
+  // Tiles of the workgroup (its last row's limit) and of this wave.
+  const int wg_last = min(wg_row0 + 4 * WAVE_ROWS - 1, rows - 1);
+  const int n_tiles_wg = min(c0 + wg_last / p.G, p.S - 1) / kTile + 1;
   const int last_row = min(row0 + WAVE_ROWS - 1, rows - 1);
   const int lim_max = min(c0 + last_row / p.G, p.S - 1);
-  const int lim_min = min(c0 + row0 / p.G, p.S - 1);
-  const int n_tiles = lim_max / kTile + 1;
+  const int lim_min = min(c0 + min(row0, rows - 1) / p.G, p.S - 1);
+  const int n_tiles = active ? lim_max / kTile + 1 : 0;
   const int first_masked = (lim_min + 1) / kTile;  // tiles before it lie under every limit
 
   const int kv = p.kv_begin + r;
@@ -140,57 +209,62 @@ void prefill_kernel(PrefillParams p) {
   const uint16_t* kbase = p.k + seq * p.S * D;
   const uint16_t* vbase = p.v + seq * p.S * D;
 
-  Tile<D> ta, tb;
-  load_tile<D, false>(ta, kbase, vbase, 0, col, grp);
+  TileStage<D> stg;
+  stage_load<D>(stg, kbase, vbase, 0);
 
-  // Column block c: row row0 + 16c + col, its token, head and causal limit.
-  bool valid[NB];
-  int tok[NB], head[NB], lim[NB];
+  // Column block c: row row0 + 16c + col, its token, head and causal limit
+  // (rows past the end: token 0, zero query, output not stored).
+  int lim[NB];
   bf16x8 qf[NB][KK];
   WaveState<D> st[NB];
 #pragma unroll
   for (int c = 0; c < NB; ++c) {
     const int rho = row0 + 16 * c + col;
-    valid[c] = rho < rows;
-    tok[c] = valid[c] ? rho / p.G : 0;
-    head[c] = valid[c] ? rho - tok[c] * p.G : 0;
-    lim[c] = min(c0 + tok[c], p.S - 1);
+    const bool valid = rho < rows;
+    const int tok = valid ? rho / p.G : 0;
+    const int head = valid ? rho - tok * p.G : 0;
+    lim[c] = min(c0 + tok, p.S - 1);
     const uint16_t* qrow =
-        p.q + ((static_cast<size_t>(b) * p.T + tok[c]) * p.h + r * p.G + head[c]) * D + grp * 8;
+        p.q + ((static_cast<size_t>(b) * p.T + tok) * p.h + r * p.G + head) * D + grp * 8;
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
       const u16x8 v = load16(qrow + kk * 32);
       const u16x8 zero = {0, 0, 0, 0, 0, 0, 0, 0};
-      qf[c][kk] = as_bf16(valid[c] ? v : zero);  // rows past the end: scores 0, output unused
+      qf[c][kk] = as_bf16(valid ? v : zero);
     }
     st[c].den = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int db = 0; db < DB; ++db) st[c].acc[db] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
+  stage_store<D>(stg, lds[0]);
+  __syncthreads();
 
-  auto process = [&](Tile<D>& tile, int it) {
-    if (it >= first_masked)
-      prefill_tile<D, NB, true>(st, tile, qf, it * kTile, L, lim, grp, p.scale_log2);
-    else
-      prefill_tile<D, NB, false>(st, tile, qf, it * kTile, L, lim, grp, p.scale_log2);
-  };
-  int it = 0;
-  for (;;) {  // tile it is in ta; the next one's loads go out before it is used
-    if (it + 1 < n_tiles) load_tile<D, false>(tb, kbase, vbase, (it + 1) * kTile, col, grp);
-    process(ta, it);
-    if (++it >= n_tiles) break;
-    if (it + 1 < n_tiles) load_tile<D, false>(ta, kbase, vbase, (it + 1) * kTile, col, grp);
-    process(tb, it);
-    if (++it >= n_tiles) break;
+  // Tile it sits in lds[it & 1]; the next tile's global loads are in flight
+  // while it is used, and land in the other buffer before the barrier.
+  for (int it = 0; it < n_tiles_wg; ++it) {
+    const bool more = it + 1 < n_tiles_wg;
+    if (more) stage_load<D>(stg, kbase, vbase, (it + 1) * kTile);
+    if (it < n_tiles) {
+      Tile<D> t;
+      tile_from_lds<D>(t, lds[it & 1], col, grp);
+      if (it >= first_masked)
+        prefill_tile<D, NB, true>(st, t, qf, it * kTile, L, lim, grp, p.scale_log2);
+      else
+        prefill_tile<D, NB, false>(st, t, qf, it * kTile, L, lim, grp, p.scale_log2);
+    }
+    if (more) stage_store<D>(stg, lds[(it + 1) & 1]);
+    __syncthreads();
   }
 
   // Lane (col, grp) holds channels db*16 + 4*grp .. +3 of its row in each block.
 #pragma unroll
   for (int c = 0; c < NB; ++c) {
-    if (!valid[c]) continue;
+    const int rho = row0 + 16 * c + col;
+    if (rho >= rows) continue;
+    const int tok = rho / p.G;
+    const int head = rho - tok * p.G;
     const float inv = 1.f / st[c].den[0];
-    const size_t orow =
-        ((static_cast<size_t>(b) * p.T + tok[c]) * p.h + r * p.G + head[c]) * D;
+    const size_t orow = ((static_cast<size_t>(b) * p.T + tok) * p.h + r * p.G + head) * D;
 #pragma unroll
     for (int db = 0; db < DB; ++db) {
       const f32x4 o = st[c].acc[db] * inv;

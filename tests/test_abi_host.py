@@ -179,7 +179,7 @@ def test_prefill_entry_points_reject_bad_arguments():
     assert names[L.mlkv_prefill_step(0x30000, 0x30000, 0x30000, ref, mp.handle, 0x40000, 0,
                                      0x50000, F, None)] == "MLKV_OK"
     # more query rows per KV head than the launch grid holds (65535 workgroups
-    # of 256 rows at head_dim 64): 256 heads per KV head x 70000 tokens
+    # of 128 rows at head_dim 64): 256 heads per KV head x 70000 tokens
     mq = mlkv.Map.uniform(1, 256, 1, 1)
     big = mlkv._Cache(0x10000, 0x20000, 1, 1, 1 << 17, 64)
     assert names[L.mlkv_prefill_step(0x30000, 0x30000, 0x30000, ctypes.byref(big), mq.handle,
