@@ -512,3 +512,48 @@ def test_length_check_rejects_out_of_range_lengths(monkeypatch):
                          ws=dw.ws)
     torch.cuda.synchronize()
     assert torch.count_nonzero(out) == 0  # nothing ran
+
+
+# ------------------------------------------------------------- HIP graphs --
+
+@pytest.mark.parametrize("wname,kw", [("mlkv4_b128_ragged", dict(B=24, ctx=900)),
+                                      ("mlkv4_b8_long", dict(B=2, ctx=4000))])
+def test_step_captured_in_a_hip_graph_replays_like_eager(wname, kw):
+    """The whole decode step (appends, attention, in-place or separate merge)
+    captured in one HIP graph: every replay, with eager steps in between,
+    gives the eager output bit for bit and leaves the same cache (the step
+    allocates nothing and records no memset, so it can be captured)."""
+    w = small(wname, **kw)
+    dw = DeviceWorkload(w)
+    say(f"graph step {w.name}")
+    out = torch.empty((w.l, w.B, w.h, w.D), dtype=torch.float32, device="cuda")
+
+    def step():
+        mlkv.decode_step(dw.q, dw.k_new, dw.v_new, dw.cache, dw.map, dw.ctx, out, ws=dw.ws)
+
+    step()
+    torch.cuda.synchronize()
+    ref = out.clone()
+    k_ref, v_ref = dw.read_cache()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step()
+    torch.cuda.synchronize()
+    for _ in range(3):
+        out.fill_(float("nan"))
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(out, ref)
+        step()  # eager work between replays
+        torch.cuda.synchronize()
+        assert torch.equal(out, ref)
+    k, v = dw.read_cache()
+    assert np.array_equal(k, k_ref) and np.array_equal(v, v_ref)
+    ref64, _, _ = _oracle_step(dw)
+    check_close(ref.cpu().numpy(), ref64, f"graph step {w.name}")
