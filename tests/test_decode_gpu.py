@@ -15,6 +15,7 @@ torch = pytest.importorskip("torch")
 import oracle  # noqa: E402
 import synth  # noqa: E402
 from gpu_util import DeviceWorkload, check_close, f64, say  # noqa: E402
+from layout_ref import unpack_v  # noqa: E402
 
 pytestmark = pytest.mark.gpu
 
@@ -557,3 +558,50 @@ def test_step_captured_in_a_hip_graph_replays_like_eager(wname, kw):
     assert np.array_equal(k, k_ref) and np.array_equal(v, v_ref)
     ref64, _, _ = _oracle_step(dw)
     check_close(ref.cpu().numpy(), ref64, f"graph step {w.name}")
+
+
+# --------------------------------------------------- 7B-like, full size --
+
+def test_full_size_7b_step_sampled_sequences():
+    """The 7B-like workload at full size (32 layers x 32 heads, head dim 128,
+    64 KV heads owned by 8 layers, batch 64, context 8192: a 17 GB cache,
+    filled on the device from a seeded generator).  Eight sampled sequences
+    are checked whole: their cache rows after the step equal the rows before
+    it plus the owners' new rows, and their outputs in every layer and head
+    match the oracle run on their rows (sequences are independent)."""
+    w = synth.get_workload("7b_mlkv8x8")
+    S = w.capacity
+    say("7b full: filling the cache on the device")
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(0x7B)
+    cache = mlkv.Cache.empty(w.n_kv, w.B, S, w.D)
+    cache.k.normal_(generator=gen)
+    cache.v.normal_(generator=gen)
+    inp = synth.step_inputs(w, with_cache=False)
+    mp = mlkv.Map.uniform(w.l, w.h, w.m, w.g)
+    kv_of, owner_of = oracle.map_uniform(w.l, w.h, w.m, w.g)
+    sample = [0, 9, 21, 33, 42, 50, 58, w.B - 1]
+    sel = torch.tensor(sample, device="cuda")
+
+    def rows():
+        k = mlkv.bf16_bits(cache.k.index_select(1, sel))
+        v = unpack_v(mlkv.bf16_bits(cache.v.index_select(1, sel)), w.n_kv, len(sample), S, w.D)
+        return k, v
+
+    k0, v0 = rows()
+    ws = mlkv.workspace(mp, w.B, S, w.D)
+    out = torch.empty((w.l, w.B, w.h, w.D), dtype=torch.float32, device="cuda")
+    say("7b full: running the step")
+    mlkv.decode_step(mlkv.bf16_tensor(inp["q"], "cuda"), mlkv.bf16_tensor(inp["k_new"], "cuda"),
+                     mlkv.bf16_tensor(inp["v_new"], "cuda"), cache, mp,
+                     torch.from_numpy(inp["ctx"]).cuda(), out, ws=ws)
+    torch.cuda.synchronize()
+    k1, v1 = rows()
+    out = out.cpu().numpy()[:, sample]
+    say("7b full: oracle on the sampled sequences")
+    ref = oracle.decode_step(np.ascontiguousarray(inp["q"][:, sample]), k0, v0,
+                             np.ascontiguousarray(inp["k_new"][sample]),
+                             np.ascontiguousarray(inp["v_new"][sample]), kv_of, owner_of,
+                             inp["ctx"][sample])
+    assert np.array_equal(k1, k0) and np.array_equal(v1, v0), "cache rows differ"
+    check_close(out, ref, "7b full, sampled sequences")
