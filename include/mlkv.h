@@ -278,6 +278,68 @@ mlkv_status mlkv_prefill_step(const void* q_all, const void* k_new_all, const vo
                               mlkv_out_dtype out_dtype, hipStream_t stream);
 
 /* ----------------------------------------------------------------------- */
+/* Model-level decode step: GPT-NeoX layers around the MLKV attention        */
+/* ----------------------------------------------------------------------- */
+
+/*
+ * One decode step of a GPT-NeoX model (the architecture of the paper's Pythia
+ * models, Section 4.2) whose attention follows an MLKV map (Section 3): per
+ * layer n, with x the newest token's residual stream,
+ *   h1 = LayerNorm1(x), h2 = LayerNorm2(x)
+ *   q  = h1 W_q + b_q; in a layer owning KV heads k = h1 W_k + b_k,
+ *   v = h1 W_v + b_v (a layer owning none computes no key or value: the
+ *   compute MLKV saves); q and k rotated at position ctx_lens[b] (rotary
+ *   embedding of the first rotary_dims channels of each head)
+ *   the owner stores k, v at slot ctx_lens[b]; every query head attends over
+ *   ctx_lens[b] + 1 positions of its KV head (as mlkv_decode_step)
+ *   x += (o W_o + b_o) + (GELU(h2 W_1 + b_1) W_2 + b_2)  (exact GELU; the
+ *   parallel residual)
+ * The matrix products are library GEMMs (rocBLAS; bf16 operands, fp32
+ * results); layer norms, bias, rotation, GELU and residual run in the
+ * library's kernels.  Stored in bf16: h1, h2, the rotated q and k, v, the
+ * attention output and the GELU output (nearest, ties to even); x stays fp32.
+ */
+typedef struct mlkv_model mlkv_model; /* opaque, owned by the library */
+
+/* Device pointers of one layer's weights, bf16, matrices row-major [in][out].
+ * The library keeps the pointers (not copies); the caller keeps the memory
+ * alive and unchanged while the model exists. */
+typedef struct {
+  const void* ln1_w; const void* ln1_b;   /* [d_model] */
+  const void* ln2_w; const void* ln2_b;   /* [d_model] */
+  const void* w_q;   const void* b_q;     /* [d_model][h*head_dim], [h*head_dim] */
+  const void* w_k;   const void* b_k;     /* [d_model][owned*head_dim], [owned*head_dim]; */
+  const void* w_v;   const void* b_v;     /*   NULL in a layer that owns no KV head */
+  const void* w_o;   const void* b_o;     /* [h*head_dim][d_model], [d_model] */
+  const void* w_fc1; const void* b_fc1;   /* [d_model][d_ff], [d_ff] */
+  const void* w_fc2; const void* b_fc2;   /* [d_ff][d_model], [d_model] */
+} mlkv_layer_weights;
+
+/* d_model must equal h * head_dim (head_dim 64 or 128); rotary_dims even, in
+ * [0, head_dim]; rotary_base > 0; ln_eps >= 0; layers[l] with the key/value
+ * pointers set exactly in the layers that own KV heads.  Creates the GEMM
+ * library handle (allocates).  Errors: MLKV_ERR_INVALID_ARG,
+ * MLKV_ERR_UNSUPPORTED, MLKV_ERR_HIP. */
+mlkv_status mlkv_model_create(const mlkv_map* map, int d_model, int d_ff, int head_dim,
+                              int rotary_dims, double rotary_base, double ln_eps,
+                              const mlkv_layer_weights* layers, mlkv_model** out);
+void mlkv_model_destroy(mlkv_model* model);
+
+/* Device workspace of mlkv_model_decode_step (intermediate rows plus the
+ * attention workspace of mlkv_workspace_bytes); 0 for invalid arguments.
+ * Initialise it once with mlkv_workspace_init. */
+size_t mlkv_model_workspace_bytes(const mlkv_model* model, int batch, int capacity);
+
+/* One decode step in place: x device fp32 [batch][d_model] (16-byte
+ * aligned) is the newest token's residual stream on entry and after the last
+ * layer on return; the cache gains the owners' rows at slot ctx_lens[b].
+ * ctx_lens, cache, max_len_hint as mlkv_decode_step.  The GEMM library may
+ * size its own workspace on the first call. */
+mlkv_status mlkv_model_decode_step(mlkv_model* model, float* x, const mlkv_cache* cache,
+                                   const int32_t* ctx_lens, int max_len_hint, void* workspace,
+                                   size_t workspace_bytes, hipStream_t stream);
+
+/* ----------------------------------------------------------------------- */
 /* Introspection (tests and benchmarks)                                      */
 /* ----------------------------------------------------------------------- */
 

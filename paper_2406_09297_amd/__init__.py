@@ -39,6 +39,8 @@ EXPORTS = [
     "mlkv_plan", "mlkv_workspace_init", "mlkv_profile_enable", "mlkv_profile_read",
     "mlkv_profile_durations", "mlkv_profile_disable", "mlkv_decode_step_rope",
     "mlkv_cache_append_rows", "mlkv_prefill_attention", "mlkv_prefill_step",
+    "mlkv_model_create", "mlkv_model_destroy", "mlkv_model_workspace_bytes",
+    "mlkv_model_decode_step",
 ]
 
 
@@ -90,6 +92,10 @@ def lib():
             "mlkv_cache_append_rows": ([I, P, P, P, P, I, I, P, P], S),
             "mlkv_prefill_attention": ([I, P, P, P, P, I, P, I, P], S),
             "mlkv_prefill_step": ([P, P, P, P, P, P, I, P, I, P], S),
+            "mlkv_model_create": ([P, I, I, I, I, ctypes.c_double, ctypes.c_double, P, P], S),
+            "mlkv_model_destroy": ([P], None),
+            "mlkv_model_workspace_bytes": ([P, I, I], Z),
+            "mlkv_model_decode_step": ([P, P, P, P, I, P, Z, P], S),
             "mlkv_plan": ([P, I, I, I, I, I, ctypes.POINTER(I), ctypes.POINTER(I)], S),
             "mlkv_workspace_init": ([P, Z, P], S),
             "mlkv_profile_enable": ([I], S),
@@ -367,6 +373,59 @@ def prefill_step(q_all: torch.Tensor, k_new_all: torch.Tensor, v_new_all: torch.
                                    map_.handle, _dev_ptr(ctx_lens, torch.int32, "ctx_lens"),
                                    q_all.shape[2], _dev_ptr(out_all, out_all.dtype, "out_all"),
                                    out_dt, _stream(stream)))
+
+
+# ---------------------------------------------------------------- model ---
+
+LAYER_WEIGHT_NAMES = ("ln1_w", "ln1_b", "ln2_w", "ln2_b", "w_q", "b_q", "w_k", "b_k", "w_v", "b_v",
+                      "w_o", "b_o", "w_fc1", "b_fc1", "w_fc2", "b_fc2")
+
+
+class _LayerWeights(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in LAYER_WEIGHT_NAMES]
+
+
+class Model:
+    """mlkv_model: GPT-NeoX layers around the MLKV attention.  `layers` is a
+    list (one per layer) of dicts name -> bf16 device tensor (None for the
+    key/value weights of a layer owning no KV head); the tensors are kept
+    alive by this object."""
+
+    def __init__(self, map_: Map, d_model: int, d_ff: int, head_dim: int, layers,
+                 rotary_dims: int = 16, rotary_base: float = 10000.0, ln_eps: float = 1e-5):
+        self.map, self._layers = map_, layers
+        arr = (_LayerWeights * len(layers))()
+        for i, lw in enumerate(layers):
+            for n in LAYER_WEIGHT_NAMES:
+                t = lw.get(n)
+                setattr(arr[i], n, None if t is None else _dev_ptr(t, torch.bfloat16, n))
+        self._arr = arr
+        out = ctypes.c_void_p()
+        _check(lib().mlkv_model_create(map_.handle, d_model, d_ff, head_dim, rotary_dims,
+                                       float(rotary_base), float(ln_eps), arr,
+                                       ctypes.byref(out)))
+        self._h = out
+
+    def __del__(self):
+        if getattr(self, "_h", None) and self._h.value and _lib is not None:
+            _lib.mlkv_model_destroy(self._h)
+            self._h = ctypes.c_void_p()
+
+    def workspace(self, batch: int, capacity: int, device="cuda", stream=None) -> torch.Tensor:
+        n = lib().mlkv_model_workspace_bytes(self._h, batch, capacity)
+        if n == 0:
+            raise ValueError("invalid model workspace arguments")
+        ws = torch.empty(n, dtype=torch.uint8, device=device)
+        _check(lib().mlkv_workspace_init(ws.data_ptr(), n, _stream(stream)))
+        return ws
+
+    def decode_step(self, x: torch.Tensor, cache: Cache, ctx_lens: torch.Tensor,
+                    ws: torch.Tensor, max_len_hint: int = 0, stream=None):
+        """mlkv_model_decode_step: x [B][d_model] fp32, updated in place."""
+        _check(lib().mlkv_model_decode_step(self._h, _dev_ptr(x, torch.float32, "x"), cache.struct,
+                                            _dev_ptr(ctx_lens, torch.int32, "ctx_lens"),
+                                            max_len_hint, ws.data_ptr(),
+                                            ws.numel() * ws.element_size(), _stream(stream)))
 
 
 # ------------------------------------------------------------------ timing ---

@@ -19,7 +19,7 @@ DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 
 
 def sources():
-    return [os.path.join(CSRC, f) for f in ("kernels.hip", "prefill.hip", "mlkv.cpp")]
+    return [os.path.join(CSRC, f) for f in ("kernels.hip", "prefill.hip", "model.hip", "mlkv.cpp")]
 
 
 def build(verbose: bool = False) -> str:
@@ -27,7 +27,8 @@ def build(verbose: bool = False) -> str:
     tmp = LIB + ".tmp"
     cmd = [HIPCC, f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-shared",
            "-mcode-object-version=5", "-Wall", "-I", INCLUDE, "-I", CSRC,
-           *DEVICE_FLAGS, *sources(), "-o", tmp]
+           *DEVICE_FLAGS, *sources(), "-L/opt/rocm/lib", "-lrocblas", "-Wl,-rpath,/opt/rocm/lib",
+           "-o", tmp]
     if verbose:
         print(" ".join(cmd))
     res = subprocess.run(cmd, capture_output=True, text=True)

@@ -92,6 +92,42 @@ struct AttnParams {
   int new_stride, own_begin, own_count;
 };
 
+// ---- GPT-NeoX layer pieces around attention (model.hip) ----
+struct NormParams {  // h1 = LN1(x), h2 = LN2(x), per row
+  const float* x;             // [rows][d]
+  const uint16_t *w1, *b1, *w2, *b2;  // [d] bf16
+  uint16_t *h1, *h2;          // [rows][d] bf16
+  int rows, d;
+  float eps;
+};
+struct QkvEpilogueParams {  // bias, rotation at pos[b], bf16 rounding
+  const float* q32;           // [rows][q_width] (GEMM result)
+  const uint16_t* b_q;        // [q_width]
+  uint16_t* q16;              // [rows][q_width]
+  const float *k32, *v32;     // [rows][kv_stride], owned block at kv_offset (kv_width wide)
+  const uint16_t *b_k, *b_v;  // [kv_width]
+  uint16_t *k16, *v16;        // [rows][kv_stride], same block
+  const int32_t* pos;         // [rows]
+  int rows, q_width, kv_width, kv_stride, kv_offset, D, dims;
+  double inv_freq[kMaxRopePairs];
+};
+struct GeluParams {  // out16 = bf16(GELU(y32 + bias))
+  const float* y32;
+  const uint16_t* bias;
+  uint16_t* out16;
+  int rows, width;
+};
+struct ResidualParams {  // x += (a32 + b_o) + (m32 + b_2)
+  float* x;
+  const float *a32, *m32;
+  const uint16_t *b_o, *b_2;
+  int rows, d;
+};
+hipError_t launch_norm2(const NormParams& p, hipStream_t stream);
+hipError_t launch_qkv_epilogue(const QkvEpilogueParams& p, hipStream_t stream);
+hipError_t launch_gelu(const GeluParams& p, hipStream_t stream);
+hipError_t launch_residual(const ResidualParams& p, hipStream_t stream);
+
 hipError_t launch_append(const AppendParams& p, int head_dim, int owned_count,
                          hipStream_t stream);
 hipError_t launch_rope(const RopeParams& p, hipStream_t stream);

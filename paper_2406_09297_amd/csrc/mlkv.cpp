@@ -12,6 +12,8 @@
 #include <string>
 #include <vector>
 
+#include <rocblas/rocblas.h>
+
 #include "kernels.h"
 
 struct mlkv_map {
@@ -22,6 +24,15 @@ struct mlkv_map {
   std::vector<int> kv_begin, kv_count, group;
   // per layer: the KV heads appended form [own_begin, own_begin + own_count)
   std::vector<int> own_begin, own_count;
+};
+
+struct mlkv_model {
+  const mlkv_map* map = nullptr;
+  int d = 0, d_ff = 0, D = 0, dims = 0;
+  float eps = 1e-5f;
+  double inv_freq[mlkv::kMaxRopePairs] = {};
+  std::vector<mlkv_layer_weights> layers;
+  rocblas_handle blas = nullptr;
 };
 
 namespace {
@@ -874,6 +885,228 @@ mlkv_status mlkv_prefill_step(const void* q_all, const void* k_new_all, const vo
     void* out = static_cast<char*>(out_all) + layer_elems * out_elem_bytes * n;
     if ((s = prefill_impl(n, q, cache, map, ctx_lens, T, out, out_dtype, stream)) != MLKV_OK)
       return s;
+  }
+  return ok();
+}
+
+// ---------------------------------------------------------------------------
+// Model-level decode step
+// ---------------------------------------------------------------------------
+
+namespace {
+
+// Workspace of a model step: intermediate rows, then the attention workspace.
+struct ModelWs {
+  size_t h1, h2, q32, k32, v32, q16, k16, v16, o16, a32, f32, f16, m32, attn, attn_bytes, total;
+};
+
+ModelWs model_ws(const mlkv_model* m, int B, int S) {
+  ModelWs w{};
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off = align_up(off + bytes, 256);
+    return at;
+  };
+  const size_t b = static_cast<size_t>(B), d = m->d, hD = static_cast<size_t>(m->map->h) * m->D;
+  const size_t kvD = static_cast<size_t>(m->map->n_kv) * m->D, ff = m->d_ff;
+  w.h1 = take(b * d * 2);
+  w.h2 = take(b * d * 2);
+  w.q32 = take(b * hD * 4);
+  w.k32 = take(b * kvD * 4);
+  w.v32 = take(b * kvD * 4);
+  w.q16 = take(b * hD * 2);
+  w.k16 = take(b * kvD * 2);
+  w.v16 = take(b * kvD * 2);
+  w.o16 = take(b * hD * 2);
+  w.a32 = take(b * d * 4);
+  w.f32 = take(b * ff * 4);
+  w.f16 = take(b * ff * 2);
+  w.m32 = take(b * d * 4);
+  w.attn = off;
+  w.attn_bytes = mlkv_workspace_bytes(m->map, B, S, m->D);
+  w.total = off + w.attn_bytes;
+  return w;
+}
+
+// Y[rows][n] (fp32, row stride ldy) = X[rows][k] (bf16, row stride ldx) * W[k][n]
+// (bf16, row-major): the column-major product Y^T = W^T X^T.
+mlkv_status gemm(rocblas_handle h, int rows, int n, int k, const void* X, int ldx, const void* W,
+                 float* Y, int ldy) {
+  const float one = 1.f, zero = 0.f;
+  const rocblas_status st = rocblas_gemm_ex(
+      h, rocblas_operation_none, rocblas_operation_none, n, rows, k, &one, W,
+      rocblas_datatype_bf16_r, n, X, rocblas_datatype_bf16_r, ldx, &zero, Y,
+      rocblas_datatype_f32_r, ldy, Y, rocblas_datatype_f32_r, ldy, rocblas_datatype_f32_r,
+      rocblas_gemm_algo_standard, 0, 0);
+  if (st != rocblas_status_success)
+    return fail(MLKV_ERR_HIP, "rocblas_gemm_ex: %s", rocblas_status_to_string(st));
+  return MLKV_OK;
+}
+
+mlkv_status hip_ok(hipError_t e, const char* what) {
+  if (e != hipSuccess) return fail(MLKV_ERR_HIP, "%s launch: %s", what, hipGetErrorString(e));
+  return MLKV_OK;
+}
+
+}  // namespace
+
+mlkv_status mlkv_model_create(const mlkv_map* map, int d_model, int d_ff, int head_dim,
+                              int rotary_dims, double rotary_base, double ln_eps,
+                              const mlkv_layer_weights* layers, mlkv_model** out) {
+  mlkv_status s;
+  if (!out) return fail(MLKV_ERR_INVALID_ARG, "out must be non-NULL");
+  *out = nullptr;
+  if ((s = check_map(map)) != MLKV_OK) return s;
+  if (head_dim != 64 && head_dim != 128)
+    return fail(MLKV_ERR_UNSUPPORTED, "head_dim %d: 64 or 128 supported", head_dim);
+  if (d_model != map->h * head_dim)
+    return fail(MLKV_ERR_INVALID_ARG, "d_model %d must equal h * head_dim = %d", d_model,
+                map->h * head_dim);
+  if (d_ff <= 0) return fail(MLKV_ERR_INVALID_ARG, "d_ff must be positive");
+  if (rotary_dims < 0 || rotary_dims > head_dim || rotary_dims % 2 != 0)
+    return fail(MLKV_ERR_INVALID_ARG, "rotary_dims %d: even, in [0, head_dim]", rotary_dims);
+  if (!(rotary_base > 0.0) || !std::isfinite(rotary_base) || !(ln_eps >= 0.0))
+    return fail(MLKV_ERR_INVALID_ARG, "rotary_base must be positive, ln_eps non-negative");
+  if (!layers) return fail(MLKV_ERR_INVALID_ARG, "layers must be non-NULL");
+  for (int n = 0; n < map->l; ++n) {
+    const mlkv_layer_weights& w = layers[n];
+    if (!w.ln1_w || !w.ln1_b || !w.ln2_w || !w.ln2_b || !w.w_q || !w.b_q || !w.w_o || !w.b_o ||
+        !w.w_fc1 || !w.b_fc1 || !w.w_fc2 || !w.b_fc2)
+      return fail(MLKV_ERR_INVALID_ARG, "layer %d: a weight pointer is NULL", n);
+    const bool owns = map->own_count[n] > 0;
+    const bool has_kv = w.w_k && w.b_k && w.w_v && w.b_v;
+    const bool no_kv = !w.w_k && !w.b_k && !w.w_v && !w.b_v;
+    if (owns ? !has_kv : !no_kv)
+      return fail(MLKV_ERR_INVALID_ARG,
+                  "layer %d: key/value weights must be given exactly when it owns KV heads", n);
+  }
+  mlkv_model* m = new (std::nothrow) mlkv_model;
+  if (!m) return fail(MLKV_ERR_INVALID_ARG, "out of host memory");
+  m->map = map;
+  m->d = d_model;
+  m->d_ff = d_ff;
+  m->D = head_dim;
+  m->dims = rotary_dims;
+  m->eps = static_cast<float>(ln_eps);
+  for (int j = 0; j < rotary_dims / 2; ++j)
+    m->inv_freq[j] = std::pow(rotary_base, -2.0 * j / rotary_dims);
+  m->layers.assign(layers, layers + map->l);
+  if (rocblas_create_handle(&m->blas) != rocblas_status_success) {
+    delete m;
+    return fail(MLKV_ERR_HIP, "rocblas_create_handle failed");
+  }
+  *out = m;
+  return ok();
+}
+
+void mlkv_model_destroy(mlkv_model* model) {
+  if (!model) return;
+  if (model->blas) (void)rocblas_destroy_handle(model->blas);
+  delete model;
+}
+
+size_t mlkv_model_workspace_bytes(const mlkv_model* model, int batch, int capacity) {
+  if (!model || batch <= 0 || batch > mlkv::max_batch() || capacity <= 0) return 0;
+  return model_ws(model, batch, capacity).total;
+}
+
+mlkv_status mlkv_model_decode_step(mlkv_model* model, float* x, const mlkv_cache* cache,
+                                   const int32_t* ctx_lens, int max_len_hint, void* workspace,
+                                   size_t workspace_bytes, hipStream_t stream) {
+  mlkv_status s;
+  if (!model) return fail(MLKV_ERR_INVALID_ARG, "model must be non-NULL");
+  const mlkv_map* map = model->map;
+  if ((s = check_cache(cache, map)) != MLKV_OK) return s;
+  if (cache->head_dim != model->D)
+    return fail(MLKV_ERR_INVALID_ARG, "cache head_dim %d differs from the model's %d",
+                cache->head_dim, model->D);
+  for (int n = 0; n < map->l; ++n)
+    if ((s = check_group_size(map, n)) != MLKV_OK) return s;
+  if (!x || !ctx_lens) return fail(MLKV_ERR_INVALID_ARG, "x and ctx_lens must be non-NULL");
+  if (!aligned16(x)) return fail(MLKV_ERR_ALIGNMENT, "x must be 16-byte aligned");
+  if (!aligned4(ctx_lens)) return fail(MLKV_ERR_ALIGNMENT, "ctx_lens must be 4-byte aligned");
+  if (max_len_hint > cache->capacity)
+    return fail(MLKV_ERR_CAPACITY, "max_len_hint %d above capacity %d", max_len_hint,
+                cache->capacity);
+  const int B = cache->batch, D = model->D, n_kv = map->n_kv, h = map->h;
+  const ModelWs w = model_ws(model, B, cache->capacity);
+  if (!workspace || workspace_bytes < w.total)
+    return fail(MLKV_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", w.total,
+                workspace ? workspace_bytes : 0);
+  if (!aligned16(workspace)) return fail(MLKV_ERR_ALIGNMENT, "workspace not 16-byte aligned");
+  const int limit = max_len_hint <= 0 ? cache->capacity : max_len_hint;
+  if ((s = check_lengths_if_requested(ctx_lens, B, 1, limit, stream)) != MLKV_OK) return s;
+  if (rocblas_set_stream(model->blas, stream) != rocblas_status_success)
+    return fail(MLKV_ERR_HIP, "rocblas_set_stream failed");
+
+  char* base = static_cast<char*>(workspace);
+  auto bf = [&](size_t off) { return reinterpret_cast<uint16_t*>(base + off); };
+  auto f32 = [&](size_t off) { return reinterpret_cast<float*>(base + off); };
+  const int hD = h * D, kvD = n_kv * D, d = model->d, ff = model->d_ff;
+  auto u16 = [](const void* p) { return static_cast<const uint16_t*>(p); };
+  int planned_key = -1;
+  for (int n = 0; n < map->l; ++n) {
+    const mlkv_layer_weights& lw = model->layers[n];
+    mlkv::NormParams np{x, u16(lw.ln1_w), u16(lw.ln1_b), u16(lw.ln2_w), u16(lw.ln2_b),
+                        bf(w.h1), bf(w.h2), B, d, model->eps};
+    if ((s = hip_ok(mlkv::launch_norm2(np, stream), "layer norm")) != MLKV_OK) return s;
+    if ((s = gemm(model->blas, B, hD, d, bf(w.h1), d, lw.w_q, f32(w.q32), hD)) != MLKV_OK)
+      return s;
+    const int owned = map->own_count[n];
+    const int own0 = owned ? map->own_begin[n] * D : 0;
+    if (owned) {
+      if ((s = gemm(model->blas, B, owned * D, d, bf(w.h1), d, lw.w_k, f32(w.k32) + own0,
+                    kvD)) != MLKV_OK ||
+          (s = gemm(model->blas, B, owned * D, d, bf(w.h1), d, lw.w_v, f32(w.v32) + own0,
+                    kvD)) != MLKV_OK)
+        return s;
+    }
+    mlkv::QkvEpilogueParams qp{};
+    qp.q32 = f32(w.q32);
+    qp.b_q = u16(lw.b_q);
+    qp.q16 = bf(w.q16);
+    qp.k32 = f32(w.k32);
+    qp.v32 = f32(w.v32);
+    qp.b_k = u16(lw.b_k);
+    qp.b_v = u16(lw.b_v);
+    qp.k16 = bf(w.k16);
+    qp.v16 = bf(w.v16);
+    qp.pos = ctx_lens;
+    qp.rows = B;
+    qp.q_width = hD;
+    qp.kv_width = owned * D;
+    qp.kv_stride = kvD;
+    qp.kv_offset = own0;
+    qp.D = D;
+    qp.dims = model->dims;
+    std::memcpy(qp.inv_freq, model->inv_freq, sizeof qp.inv_freq);
+    if ((s = hip_ok(mlkv::launch_qkv_epilogue(qp, stream), "q/k/v epilogue")) != MLKV_OK)
+      return s;
+    // Attention with the owner's append (fused when the layer reads all it owns).
+    const bool fused_append = owned > 0 && map->own_begin[n] >= map->kv_begin[n] &&
+                              map->own_begin[n] + owned <= map->kv_begin[n] + map->kv_count[n];
+    if (owned > 0 && !fused_append &&
+        (s = append_impl(n, map, cache, bf(w.k16) + own0, bf(w.v16) + own0, kvD, ctx_lens,
+                         stream)) != MLKV_OK)
+      return s;
+    const int key = map->kv_count[n];
+    const int mode = key == planned_key ? 2 : 1;
+    if ((s = attention_impl(n, bf(w.q16), cache, map, ctx_lens, 1, bf(w.o16), MLKV_OUT_BF16,
+                            max_len_hint, base + w.attn, w.attn_bytes, stream, mode,
+                            fused_append ? bf(w.k16) : nullptr,
+                            fused_append ? bf(w.v16) : nullptr)) != MLKV_OK)
+      return s;
+    planned_key = key;
+    if ((s = gemm(model->blas, B, d, hD, bf(w.o16), hD, lw.w_o, f32(w.a32), d)) != MLKV_OK ||
+        (s = gemm(model->blas, B, ff, d, bf(w.h2), d, lw.w_fc1, f32(w.f32), ff)) != MLKV_OK)
+      return s;
+    mlkv::GeluParams gp{f32(w.f32), u16(lw.b_fc1), bf(w.f16), B, ff};
+    if ((s = hip_ok(mlkv::launch_gelu(gp, stream), "GELU")) != MLKV_OK) return s;
+    if ((s = gemm(model->blas, B, d, ff, bf(w.f16), ff, lw.w_fc2, f32(w.m32), d)) != MLKV_OK)
+      return s;
+    mlkv::ResidualParams rp{x, f32(w.a32), f32(w.m32), u16(lw.b_o), u16(lw.b_fc2), B, d};
+    if ((s = hip_ok(mlkv::launch_residual(rp, stream), "residual")) != MLKV_OK) return s;
   }
   return ok();
 }

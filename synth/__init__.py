@@ -175,3 +175,38 @@ def prefill_inputs(w: Workload, fill: int = 0, with_cache: bool = True) -> dict:
         out["v_cache"] = rows_bf16(w.seed, STREAM_V_CACHE, w.n_kv * w.B, S, w.D, lens,
                                    fill=fill).reshape(w.n_kv, w.B, S, w.D)
     return out
+
+
+STREAM_WEIGHTS = 16  # first stream of the model weights (one stream per tensor)
+
+
+def model_weights(seed: int, l: int, h: int, D: int, d_ff: int, owned_per_layer,
+                  std: float = 0.02) -> list:
+    """Synthetic GPT-NeoX layer weights (bf16 bits, uint16), row-major [in][out]:
+    layer-norm scales 1 + 0.1 N(0,1), every other tensor std * N(0,1); a layer
+    with owned_per_layer[n] == 0 gets no key/value weights (None)."""
+    d = h * D
+    names = [("ln1_w", (d,)), ("ln1_b", (d,)), ("ln2_w", (d,)), ("ln2_b", (d,)),
+             ("w_q", (d, h * D)), ("b_q", (h * D,)), ("w_k", None), ("b_k", None),
+             ("w_v", None), ("b_v", None), ("w_o", (h * D, d)), ("b_o", (d,)),
+             ("w_fc1", (d, d_ff)), ("b_fc1", (d_ff,)), ("w_fc2", (d_ff, d)), ("b_fc2", (d,))]
+    layers = []
+    for n in range(l):
+        owned = int(owned_per_layer[n])
+        lw = {}
+        for t, (name, shape) in enumerate(names):
+            if name in ("w_k", "w_v"):
+                shape = (d, owned * D) if owned else None
+            if name in ("b_k", "b_v"):
+                shape = (owned * D,) if owned else None
+            if shape is None:
+                lw[name] = None
+                continue
+            stream = STREAM_WEIGHTS + n * len(names) + t
+            if name in ("ln1_w", "ln2_w"):
+                z = bf16_to_f32(normal_bf16(seed, stream, shape))
+                lw[name] = f32_to_bf16(1.0 + 0.1 * z)
+            else:
+                lw[name] = normal_bf16(seed, stream, shape, scale=std)
+        layers.append(lw)
+    return layers

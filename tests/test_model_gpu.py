@@ -1,0 +1,146 @@
+"""GPU parity of the model-level decode step (GPT-NeoX layers around the MLKV
+attention, mlkv_model_decode_step) against the float64 model oracle with the
+same bf16 rounding points (oracle/model.py).
+
+Tolerance.  The attention kernels round the softmax weights to bf16 before
+the value product (relative error up to 2^-9 per weight, the decode path's
+documented arithmetic) where the oracle keeps them exact, so each layer's
+attention output differs from the oracle's by up to about one bf16 step in
+many elements; through W_o that adds a perturbation of order 2^-9 |a| to the
+residual stream per layer, and over the layers these add up (the GEMMs' fp32
+accumulation, which only occasionally flips a stored bf16 value, is far
+smaller).  Bars: max |diff| <= 1e-2 * max(1, max |x|) and mean |diff| <=
+1e-2 * mean |x| after the last layer; a cache row appended by layer 0
+(computed from the step's input, before any attention) within one bf16 step
+of the oracle's, later owners' rows within the same bar as the output.
+"""
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+import oracle  # noqa: E402
+import oracle.model as om  # noqa: E402
+import synth  # noqa: E402
+from gpu_util import say  # noqa: E402
+from layout_ref import unpack_k, unpack_v  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+mlkv = pytest.importorskip("paper_2406_09297_amd")
+
+MAX_REL = 1e-2
+MEAN_REL = 1e-2
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    mlkv.lib()
+    yield
+
+
+def _run_case(l, h, D, d_ff, m, g, B, ctx, seed, rd=16, kv_of=None, owner_of=None, label=""):
+    ctx = np.asarray(ctx, dtype=np.int32)
+    if kv_of is None:
+        kv_of, owner_of = oracle.map_uniform(l, h, m, g)
+        mp = mlkv.Map.uniform(l, h, m, g)
+    else:
+        mp = mlkv.Map.from_tables(kv_of, owner_of)
+    n_kv = len(owner_of)
+    owned = [int((np.asarray(owner_of) == n).sum()) for n in range(l)]
+    weights = synth.model_weights(seed, l, h, D, d_ff, owned)
+    dev = [{k: (None if v is None else mlkv.bf16_tensor(v, "cuda")) for k, v in lw.items()}
+           for lw in weights]
+    d = h * D
+    model = mlkv.Model(mp, d, d_ff, D, dev, rotary_dims=rd)
+    S = (int(ctx.max()) + 1 + 63) // 64 * 64
+    lens = np.tile(ctx, n_kv)
+    kc = synth.rows_bf16(seed, 1, n_kv * B, S, D, lens, fill=synth.BF16_NAN).reshape(n_kv, B, S, D)
+    vc = synth.rows_bf16(seed, 2, n_kv * B, S, D, lens, fill=synth.BF16_NAN).reshape(n_kv, B, S, D)
+    cache = mlkv.Cache.empty(n_kv, B, S, D)
+    cache.load_rows(kc, vc)
+    x_bits = synth.normal_bf16(seed, 0, (B, d))
+    x0 = synth.bf16_to_f32(x_bits)
+    x = torch.from_numpy(x0.copy()).cuda()
+    ctx_dev = torch.from_numpy(ctx).cuda()
+    ws = model.workspace(B, S)
+    say(f"model step {label}")
+    model.decode_step(x, cache, ctx_dev, ws)
+    torch.cuda.synchronize()
+    out = x.cpu().numpy().astype(np.float64)
+    k_gpu = unpack_k(mlkv.bf16_bits(cache.k), n_kv, B, S, D)
+    v_gpu = unpack_v(mlkv.bf16_bits(cache.v), n_kv, B, S, D)
+    kr, vr = om._f64(kc), om._f64(vc)
+    ref = om.decode_step_model(x0.astype(np.float64), weights, kv_of, owner_of, kr, vr, ctx, h, D,
+                               rd)
+    diff = np.abs(out - ref)
+    scale = max(1.0, float(np.abs(ref).max()))
+    mean_x = float(np.abs(ref).mean())
+    say(f"  {label}: max|d|={diff.max():.3e} mean|d|={diff.mean():.3e} max|x|={np.abs(ref).max():.3f} "
+        f"mean|x|={mean_x:.3f}")
+    assert np.all(np.isfinite(out))
+    assert diff.max() <= MAX_REL * scale and diff.mean() <= MEAN_REL * mean_x, label
+    # cache: untouched slots bit-exact.  The rows appended by layer 0 come
+    # from the step's input x: within one bf16 step of the oracle's.  Later
+    # owners' rows come from a residual stream already carrying the earlier
+    # layers' attention error: within the output bar.
+    appended = np.zeros((n_kv, B, S), dtype=bool)
+    for kv in range(n_kv):
+        appended[kv, np.arange(B), ctx] = True
+    first = np.asarray(owner_of) == 0
+    for got, orig, r in ((k_gpu, kc, kr), (v_gpu, vc, vr)):
+        assert np.array_equal(got[~appended], orig[~appended]), f"{label}: untouched slots changed"
+        for kv in range(n_kv):
+            g64 = om._f64(got[kv, np.arange(B), ctx])
+            rr = r[kv, np.arange(B), ctx]
+            if first[kv]:
+                assert np.all(np.abs(g64 - rr) <= np.abs(rr) * 2.0 ** -7 + 1e-30), \
+                    f"{label}: layer-0 row of KV head {kv} off by more than one bf16 step"
+                assert np.mean(g64 != rr) <= 0.01, f"{label}: too many layer-0 values differ"
+            else:
+                assert np.abs(g64 - rr).max() <= MAX_REL * max(1.0, float(np.abs(rr).max())), \
+                    f"{label}: row of KV head {kv} outside the bar"
+    return diff.max() / scale, diff.mean()
+
+
+def test_model_step_pythia160m_shape_mlkv4():
+    """Pythia-160M layer shapes (12 layers, 12 heads of 64, d_ff 3072, rotary
+    on 16 channels) with MLKV-4 (owners 0, 3, 6, 9): ragged contexts."""
+    _run_case(12, 12, 64, 3072, 4, 1, B=4, ctx=[0, 33, 100, 257], seed=91, label="pythia MLKV-4")
+
+
+@pytest.mark.parametrize("m,g", [(4, 12), (1, 1), (2, 3)])
+def test_model_step_maps(m, g):
+    """Plain multi-head attention (every layer owns its 12 heads), MLKV-1 (one
+    KV head for the whole model) and a grouped map (3 KV heads per owning layer)."""
+    _run_case(4, 12, 64, 512, m, g, B=3, ctx=[5, 64, 130], seed=92, label=f"m{m} g{g}")
+
+
+def test_model_step_head_dim_128_and_full_rotation():
+    _run_case(2, 4, 128, 640, 2, 2, B=2, ctx=[31, 96], seed=93, rd=128, label="D128 rd128")
+
+
+def test_model_step_general_map_owner_not_reading_its_head():
+    """Layer 0 owns KV heads 0 and 1 but reads only head 0 (its append runs
+    separately); layer 1 reads head 1."""
+    kv_of = np.array([[0] * 4, [1] * 4, [0] * 4, [1] * 4], np.int32)
+    owner_of = np.array([0, 0], np.int32)
+    _run_case(4, 4, 64, 384, None, None, B=2, ctx=[7, 70], seed=94, kv_of=kv_of,
+              owner_of=owner_of, label="general map")
+
+
+def test_model_rejects_missing_or_extra_key_weights():
+    mp = mlkv.Map.uniform(2, 4, 1, 1)  # layer 0 owns the KV head, layer 1 none
+    weights = synth.model_weights(95, 2, 4, 64, 256, [1, 0])
+    dev = [{k: (None if v is None else mlkv.bf16_tensor(v, "cuda")) for k, v in lw.items()}
+           for lw in weights]
+    bad = [dict(dev[0]), dict(dev[1])]
+    bad[1]["w_k"] = dev[0]["w_k"]  # a non-owner with key weights
+    with pytest.raises(mlkv.MLKVError):
+        mlkv.Model(mp, 256, 256, 64, bad)
+    bad = [dict(dev[0]), dict(dev[1])]
+    bad[0]["w_v"] = None  # the owner without value weights
+    with pytest.raises(mlkv.MLKVError):
+        mlkv.Model(mp, 256, 256, 64, bad)
