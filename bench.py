@@ -252,6 +252,110 @@ def run_prefill(args, w):
     print(json.dumps(result), flush=True)
 
 
+def run_model(args, w):
+    """Whole-model decode step (mlkv_model_decode_step): tokens/s at batch B."""
+    import torch
+    import synth
+    import oracle
+    import paper_2406_09297_amd as mlkv
+
+    dev = "cuda:0"
+    log(f"[bench] model workload {w.name}: generating weights and cache")
+    mp = mlkv.Map.uniform(w.l, w.h, w.m, w.g)
+    kv_of, owner_of = oracle.map_uniform(w.l, w.h, w.m, w.g)
+    owned = [int((owner_of == n).sum()) for n in range(w.l)]
+    weights = synth.model_weights(w.seed, w.l, w.h, w.D, w.d_ff, owned)
+    dev_w = [{k: (None if v is None else mlkv.bf16_tensor(v, dev)) for k, v in lw.items()}
+             for lw in weights]
+    d = w.h * w.D
+    model = mlkv.Model(mp, d, w.d_ff, w.D, dev_w, rotary_dims=16)
+    inp = synth.step_inputs(w, fill=0)
+    S = inp["capacity"]
+    cache = mlkv.Cache.empty(w.n_kv, w.B, S, w.D, dev)
+    cache.load_rows(inp["k_cache"], inp["v_cache"])
+    x0 = synth.bf16_to_f32(synth.normal_bf16(w.seed, 0, (w.B, d)))
+    x = torch.from_numpy(x0.copy()).to(dev)
+    ctx = torch.from_numpy(inp["ctx"]).to(dev)
+    ws = model.workspace(w.B, S, dev)
+    max_len = int(inp["ctx"].max()) + 1
+    stream = torch.cuda.current_stream()
+
+    def one_step():
+        model.decode_step(x, cache, ctx, ws, max_len_hint=max_len)
+
+    log(f"[bench] warmup {args.warmup}")
+    for _ in range(args.warmup):
+        one_step()
+    torch.cuda.synchronize()
+    log(f"[bench] timing {args.steps} model steps")
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(args.steps):
+        one_step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms_step = e0.elapsed_time(e1) / args.steps
+    # attention launches of the same steps, timed by the library's event pairs
+    mlkv.profile_enable(args.steps * w.l)
+    done = 0
+    while done < args.steps:
+        n = min(10, args.steps - done)
+        torch.cuda._sleep(SLEEP_CYCLES)
+        for _ in range(n):
+            one_step()
+        torch.cuda.synchronize()
+        done += n
+    n_launch, tot_ms, _, _ = mlkv.profile_read()
+    mlkv.profile_disable()
+    attn_ms_step = tot_ms / args.steps
+    weight_bytes = sum(int(v.size) * 2 for lw in weights for v in lw.values() if v is not None)
+    L = inp["ctx"].astype(np.int64) + 1
+    kv_bytes = sum(mp.layer_kv_count(n) for n in range(w.l)) * int(L.sum()) * w.D * 2 * 2
+    step_bytes = weight_bytes + kv_bytes
+    achieved = step_bytes / (ms_step * 1e-3) / 1e9
+    result = {
+        "metric": "whole-model decode tokens/s (MLKV Pythia-160M shape, synthetic weights)",
+        "value": round(w.B / (ms_step * 1e-3), 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded bf16 weights std 0.02, N(0,1) cache; no trained weights)",
+        "config": {"workload": w.name, "l": w.l, "h": w.h, "m": w.m, "g": w.g, "head_dim": w.D,
+                   "d_model": d, "d_ff": w.d_ff, "batch": w.B, "ctx": w.ctx, "capacity": S,
+                   "weight_bytes": weight_bytes, "kv_bytes_per_step": kv_bytes},
+        "attention_ms_per_step": round(attn_ms_step, 4),
+        "attention_share": round(attn_ms_step / ms_step, 3),
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                     "kernel": "whole step (weights read once + KV rows read once per layer)"},
+    }
+    if not args.no_cpu_baseline:
+        log("[bench] cpu baseline (oracle)")
+        import oracle.model as om
+
+        kc, vc = om._f64(inp["k_cache"]), om._f64(inp["v_cache"])
+        threads = int(os.environ.get("OMP_NUM_THREADS", len(os.sched_getaffinity(0))))
+        runs, spent = 0, 0.0
+        while spent < 10.0 or runs == 0:
+            ts = time.perf_counter()
+            om.decode_step_model(x0.astype(np.float64), weights, kv_of, owner_of, kc, vc,
+                                 inp["ctx"], w.h, w.D, 16)
+            spent += time.perf_counter() - ts
+            runs += 1
+        result["cpu_baseline"] = {
+            "value": round(w.B * runs / spent, 2), "unit": "tokens/s", "cores": threads,
+            "kind": "oracle",
+            "sample": f"{runs} whole model step(s) of the same workload (float64 numpy oracle), "
+                      f"{spent:.1f} s"}
+    print(json.dumps(result), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -287,6 +391,15 @@ def main():
     w = synth.get_workload(args.workload)
     if w.T > 1:
         run_prefill(args, w)
+        return
+    if w.d_ff > 0:
+        if args.map:
+            m, g = (int(x) for x in args.map.split(","))
+            w = w.with_map(m, g)
+        elif w.sweep:
+            m, g = w.sweep[-1]
+            w = w.with_map(m, g)
+        run_model(args, w)
         return
     if args.map:
         m, g = (int(x) for x in args.map.split(","))

@@ -33,6 +33,7 @@ class Workload:
     note: str = ""
     sweep: tuple = field(default_factory=tuple)   # (m, g) points of a map sweep
     T: int = 1                        # new tokens per sequence (prefill when > 1)
+    d_ff: int = 0                     # > 0: a whole-model decode step (MLP width)
 
     @property
     def n_kv(self) -> int:
@@ -50,7 +51,8 @@ class Workload:
 
     def with_map(self, m: int, g: int) -> "Workload":
         return Workload(self.name + f"-m{m}g{g}", self.l, self.h, m, g, self.D, self.B,
-                        self.ctx, self.ctx_range, self.k_scale, self.seed, self.note, T=self.T)
+                        self.ctx, self.ctx_range, self.k_scale, self.seed, self.note, T=self.T,
+                        d_ff=self.d_ff)
 
     def scaled(self, B: int | None = None, ctx: int | None = None,
                T: int | None = None) -> "Workload":
@@ -62,7 +64,8 @@ class Workload:
             else:
                 c = ctx
         return Workload(self.name + "-small", self.l, self.h, self.m, self.g, self.D,
-                        B or self.B, c, cr, self.k_scale, self.seed, self.note, T=T or self.T)
+                        B or self.B, c, cr, self.k_scale, self.seed, self.note, T=T or self.T,
+                        d_ff=self.d_ff)
 
 
 WORKLOADS = {
@@ -92,6 +95,12 @@ WORKLOADS = {
         seed=0x4D4C4B56 + 5,
         note="Pythia-160M shape, MLKV-4, batch 8: a 2000-token prompt prefilled into an "
              "empty cache (the paper's inference runs first fill a 2000-token cache)"),
+    "model_b8": Workload(
+        "model_b8", l=12, h=12, m=4, g=1, D=64, B=8, ctx=2000, d_ff=3072, seed=0x4D4C4B56 + 6,
+        note="whole Pythia-160M-shaped decode step (synthetic weights, rotary on 16 channels) "
+             "at batch 8 on a 2000-token cache, the shape of the paper's throughput "
+             "measurement; map sweep over the Table 2 variants",
+        sweep=((12, 12), (12, 4), (4, 12), (12, 1), (4, 3), (6, 1), (2, 1), (1, 1), (4, 1))),
 }
 
 
