@@ -356,6 +356,148 @@ def run_model(args, w):
     print(json.dumps(result), flush=True)
 
 
+CAPACITY_MARGIN = 4 << 30  # device bytes left free beside the step's buffers
+
+
+def capacity_setup(w, dev, seed):
+    """Allocate the largest batch of a decode step at ctx = w.ctx whose cache
+    (capacity w.capacity) and step buffers fit in the free device memory, and
+    fill it from a seeded device generator (keys, values, queries and new rows
+    N(0,1) in bf16).  Returns (B, cache, q, k_new, v_new, ctx, out)."""
+    import torch
+    import synth
+    import paper_2406_09297_amd as mlkv
+
+    torch.cuda.empty_cache()
+    free, _ = torch.cuda.mem_get_info()
+    S = w.capacity
+    B = synth.capacity_batch(w, free - CAPACITY_MARGIN, S)
+    while True:  # the allocator may not hand out all of it in these pieces
+        try:
+            cache = mlkv.Cache.empty(w.n_kv, B, S, w.D, dev)
+            q = torch.empty((w.l, B, w.h, w.D), dtype=torch.bfloat16, device=dev)
+            out = torch.empty((w.l, B, w.h, w.D), dtype=torch.bfloat16, device=dev)
+            kn = torch.empty((B, w.n_kv, w.D), dtype=torch.bfloat16, device=dev)
+            vn = torch.empty((B, w.n_kv, w.D), dtype=torch.bfloat16, device=dev)
+            break
+        except torch.OutOfMemoryError:
+            cache = q = out = kn = vn = None
+            torch.cuda.empty_cache()
+            B = int(B * 0.98)
+            log(f"[bench] capacity: allocation failed, retrying at batch {B}")
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(seed)
+    for t in (cache.k, cache.v, q, kn, vn):
+        t.normal_(generator=gen)
+    ctx = torch.full((B,), w.ctx, dtype=torch.int32, device=dev)
+    torch.cuda.synchronize()
+    return B, cache, q, kn, vn, ctx, out
+
+
+def run_capacity(args, w):
+    """The largest batch a 2048-token cache allows on this GPU (the paper's
+    memory experiment: 2000 cached tokens, then decode), and decode steps
+    timed at that batch."""
+    import torch
+    import synth
+    import oracle
+    import paper_2406_09297_amd as mlkv
+
+    dev = "cuda:0"
+    log(f"[bench] capacity workload {w.name}: sizing and filling the batch")
+    B, cache, q, kn, vn, ctx, out = capacity_setup(w, dev, w.seed)
+    S = w.capacity
+    mp = mlkv.Map.uniform(w.l, w.h, w.m, w.g)
+    log(f"[bench] capacity: batch {B}, cache {cache.k.numel() * 4 / 1e9:.1f} GB")
+    stream = torch.cuda.current_stream()
+    L = w.ctx + 1
+    kv_count = [mp.layer_kv_count(n) for n in range(w.l)]
+    kv_bytes = sum(kv_count) * B * L * w.D * 2 * 2
+    qo_bytes = w.l * B * w.h * w.D * (2 + 2)
+    owned = sum(mp.layer_owned(n)[1] for n in range(w.l))
+    step_total = kv_bytes + qo_bytes + owned * B * w.D * 2 * 2 * 2
+
+    def one_step():
+        mlkv.decode_step(q, kn, vn, cache, mp, ctx, out, max_len_hint=L, ws=None)
+
+    log(f"[bench] warmup {args.warmup}")
+    for _ in range(args.warmup):
+        one_step()
+    torch.cuda.synchronize()
+    log(f"[bench] timing {args.steps} steps")
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(args.steps):
+        one_step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms_step = e0.elapsed_time(e1) / args.steps
+    mlkv.profile_enable(args.steps * w.l)
+    for _ in range(args.steps):
+        one_step()
+    torch.cuda.synchronize()
+    n_launch, tot_ms, min_ms, max_ms = mlkv.profile_read()
+    mlkv.profile_disable()
+    avg = tot_ms * 1e-3 / n_launch
+    attn_bytes = (kv_bytes + qo_bytes) / w.l
+    achieved = attn_bytes / avg / 1e9
+    per_seq = synth.step_bytes_per_sequence(w, S)
+    result = {
+        "metric": "decode tokens/s at the largest batch whose 2048-token cache fits the GPU, "
+                  "MLKV Pythia-160M shape",
+        "value": round(B / (ms_step * 1e-3), 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded N(0,1) bf16 q/K/V generated on the device; no weights)",
+        "config": {"workload": w.name, "l": w.l, "h": w.h, "m": w.m, "g": w.g, "head_dim": w.D,
+                   "n_kv": w.n_kv, "batch": B, "ctx": w.ctx, "capacity": S,
+                   "bytes_per_sequence": per_seq, "cache_bytes": int(cache.k.numel() * 4),
+                   "kv_bytes_per_step": int(kv_bytes), "out_dtype": "bf16"},
+        "max_batch": B,
+        "step_gbs": round(step_total / (ms_step * 1e-3) / 1e9, 1),
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                     "kernel": "attention_kernel", "avg_launch_us": round(avg * 1e6, 2),
+                     "min_launch_us": round(min_ms * 1e3, 2),
+                     "max_launch_us": round(max_ms * 1e3, 2), "launches": n_launch,
+                     "bytes_per_launch": int(attn_bytes)},
+    }
+    if not args.no_cpu_baseline:
+        log("[bench] cpu baseline (oracle)")
+        # Bounded sample: whole decode steps of 4 sequences (rows copied back).
+        sel = torch.arange(4, device=dev)
+        q_h = mlkv.bf16_bits(q.index_select(1, sel))
+        kn_h, vn_h = mlkv.bf16_bits(kn[:4]), mlkv.bf16_bits(vn[:4])
+        k_h = mlkv.bf16_bits(cache.k.index_select(1, sel))
+        # value plane: 32-token blocks stored channel-major -> token rows
+        v_h = np.ascontiguousarray(
+            mlkv.bf16_bits(cache.v.index_select(1, sel)).reshape(w.n_kv, 4, S // 32, w.D, 32)
+            .transpose(0, 1, 2, 4, 3)).reshape(w.n_kv, 4, S, w.D)
+        ctx_h = np.full(4, w.ctx, dtype=np.int32)
+        kv_of, owner_of = oracle.map_uniform(w.l, w.h, w.m, w.g)
+        threads = int(os.environ.get("OMP_NUM_THREADS", len(os.sched_getaffinity(0))))
+        runs, spent = 0, 0.0
+        while spent < 10.0 or runs == 0:
+            k1, v1 = k_h.copy(), v_h.copy()
+            ts = time.perf_counter()
+            oracle.decode_step(q_h, k1, v1, kn_h, vn_h, kv_of, owner_of, ctx_h)
+            spent += time.perf_counter() - ts
+            runs += 1
+        result["cpu_baseline"] = {
+            "value": round(4 * runs / spent, 2), "unit": "tokens/s", "cores": threads,
+            "kind": "oracle",
+            "sample": f"{runs} whole decode step(s) of 4 sequences of the same workload "
+                      f"(fp64 oracle), {spent:.1f} s"}
+    print(json.dumps(result), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -389,6 +531,12 @@ def main():
     dev = "cuda:0"
     torch.cuda.set_device(0)
     w = synth.get_workload(args.workload)
+    if w.B == 0:  # batch sized at run time: the capacity experiment
+        if args.map:
+            m, g = (int(x) for x in args.map.split(","))
+            w = w.with_map(m, g)
+        run_capacity(args, w)
+        return
     if w.T > 1:
         run_prefill(args, w)
         return

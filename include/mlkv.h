@@ -131,7 +131,10 @@ size_t mlkv_cache_bytes(const mlkv_map* map, int batch, int capacity, int head_d
 
 /* Device workspace needed by mlkv_decode_attention / mlkv_decode_step for any
  * max_len_hint <= capacity (split-K partial results and per-sequence split
- * counters).  0 for invalid args. */
+ * counters), sized for the current device.  0 for invalid args, and 0 when
+ * every layer has at least as many (sequence, KV head) units as the device's
+ * attention workgroup budget (two per compute unit): those launches give each
+ * unit a workgroup of its own and need no workspace. */
 size_t mlkv_workspace_bytes(const mlkv_map* map, int batch, int capacity, int head_dim);
 
 /* Zero-fill a workspace before its first use (a fill kernel enqueued on
@@ -164,7 +167,10 @@ mlkv_status mlkv_cache_append(int layer, const mlkv_map* map, const mlkv_cache* 
  *   out: device [batch][h][head_dim], fp32 or bf16 per out_dtype.
  *   max_len_hint: an upper bound of every L_b (<= 0 means capacity); it sizes
  *        the work plan.  Lengths above it are truncated to it.
- *   batch: at most 2048 sequences (else MLKV_ERR_UNSUPPORTED).
+ *   batch: any size when the layer's (sequence, KV head) units are at least
+ *        the device's workgroup budget (two per compute unit; then each
+ *        unit is one workgroup and no workspace is used); otherwise at most
+ *        2048 sequences (else MLKV_ERR_UNSUPPORTED, before any launch).
  *   workspace: device memory of at least mlkv_workspace_bytes(...) bytes,
  *        16-byte aligned, zeroed once by mlkv_workspace_init (the split
  *        counters must start at zero; each call returns them to zero).

@@ -301,7 +301,17 @@ void attention_kernel(AttnParams p) {
 
   int b, r, j, nb, L, k0, k1;
   const bool single = !p.plan && p.n_blocks == 1 && p.B == 1 && p.n_groups == 1;
-  if (p.plan) {  // the step's plan, written by the step's first attention launch
+  if (p.direct) {
+    // One workgroup per (sequence, KV group) unit, in unit order: the run is
+    // the whole unit, so no schedule, plan or partials (any batch size).
+    b = static_cast<int>(static_cast<unsigned>(g) / static_cast<unsigned>(p.n_groups));
+    r = g - b * p.n_groups;
+    j = 0;
+    nb = 1;
+    L = attended_len(p, b);
+    k0 = 0;
+    k1 = tiles_of(L);
+  } else if (p.plan) {  // the step's plan, written by the step's first attention launch
     const RunItem item = reinterpret_cast<const RunItem*>(p.plan)[g];
     if (item.z >= 0)
       for (int i = threadIdx.x; i < p.h * D4; i += NT)

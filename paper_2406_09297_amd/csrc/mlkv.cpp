@@ -124,8 +124,6 @@ mlkv_status check_cache(const mlkv_cache* c, const mlkv_map* map) {
     return fail(MLKV_ERR_CAPACITY, "cache capacity %d is not a multiple of 32", c->capacity);
   if (c->head_dim != 64 && c->head_dim != 128)
     return fail(MLKV_ERR_UNSUPPORTED, "head_dim %d not supported (64 or 128)", c->head_dim);
-  if (c->batch > mlkv::max_batch())
-    return fail(MLKV_ERR_UNSUPPORTED, "batch %d above the supported %d", c->batch, mlkv::max_batch());
   if (c->n_kv != map->n_kv)
     return fail(MLKV_ERR_INVALID_ARG, "cache has %d KV heads, map has %d", c->n_kv, map->n_kv);
   const double elems = 2.0 * c->n_kv * c->batch * static_cast<double>(c->capacity) * c->head_dim;
@@ -149,6 +147,7 @@ struct Plan {
   int min_tiles;  // least tiles per run
   int fused;      // 1: every unit's runs are merged in place (no merge kernel)
   int waves;      // waves per attention workgroup
+  int direct;     // 1: one workgroup per unit in unit order (no schedule, no workspace)
 };
 constexpr int kMinTiles = 4;
 constexpr int kMaxRunsPerUnit = 128;
@@ -171,16 +170,13 @@ long workgroups_for(long resident, long units, long t_max, int min_tiles) {
 // Otherwise a separate merge kernel runs.  MLKV_COMBINE=kernel forces the
 // merge kernel; MLKV_COMBINE=fused also accepts a floor that keeps at least
 // half of the workgroups.
-Plan plan(const mlkv_map* map, int layer, int batch, int max_len, int head_dim) {
-  Plan pl{};
-  pl.max_tiles = tiles_of(max_len < 1 ? 1 : max_len);
-  const long units = static_cast<long>(batch) * map->kv_count[layer];
-  const long t_max = units * pl.max_tiles;
+// The attention launch's workgroup budget on the current device.  Two
+// workgroups per compute unit: on MI355X fewer, longer runs beat filling
+// every resident slot (fewer partials, longer pipelines), and a whole
+// multiple of the compute units keeps their bandwidth shares equal.
+long workgroup_budget(int head_dim) {
   long resident = mlkv::resident_workgroups(head_dim);
   if (resident <= 0) resident = kFallbackResident;
-  // Two workgroups per compute unit: on MI355X fewer, longer runs beat
-  // filling every resident slot (fewer partials, longer pipelines), and a
-  // whole multiple of the compute units keeps their bandwidth shares equal.
   long cus = mlkv::compute_units();
   if (cus <= 0) cus = kFallbackResident / 3;
   if (resident > kWorkgroupsPerCu * cus) resident = kWorkgroupsPerCu * cus;
@@ -188,6 +184,15 @@ Plan plan(const mlkv_map* map, int layer, int batch, int max_len, int head_dim) 
     const long w = std::atol(env);
     if (w > 0) resident = w;
   }
+  return resident;
+}
+
+Plan plan(const mlkv_map* map, int layer, int batch, int max_len, int head_dim) {
+  Plan pl{};
+  pl.max_tiles = tiles_of(max_len < 1 ? 1 : max_len);
+  const long units = static_cast<long>(batch) * map->kv_count[layer];
+  const long t_max = units * pl.max_tiles;
+  const long resident = workgroup_budget(head_dim);
   pl.min_tiles = kMinTiles;
   pl.fused = 0;
   const long cap_parts = mlkv::stage_floats() / (static_cast<long>(map->group[layer]) * head_dim);
@@ -223,12 +228,25 @@ Plan plan(const mlkv_map* map, int layer, int batch, int max_len, int head_dim) 
   if (g == units) {  // one workgroup per unit: runs cover whole units, nothing to merge
     pl.min_tiles = pl.max_tiles;
     pl.fused = 0;
+    // Workgroup g is unit g, except the lone short unit of a one-sequence
+    // batch, which keeps the single-workgroup path (first tiles requested
+    // before its length arrives).
+    pl.direct = !(g == 1 && batch == 1 && map->kv_count[layer] == 1);
   }
   pl.max_parts = (pl.max_tiles + pl.min_tiles - 1) / pl.min_tiles + 1;
   return pl;
 }
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// Plans that schedule runs inside the kernel keep per-sequence tables in LDS,
+// which bounds the batch; direct plans (a workgroup per unit) have no bound.
+mlkv_status check_plan_batch(const Plan& pl, int batch) {
+  if (pl.direct || pl.n_blocks <= 1 || batch <= mlkv::max_batch()) return MLKV_OK;
+  return fail(MLKV_ERR_UNSUPPORTED,
+              "batch %d above %d needs one workgroup per (sequence, KV head): %d workgroups "
+              "planned", batch, mlkv::max_batch(), pl.n_blocks);
+}
 
 // Workspace layout of one call (nothing when one workgroup does all):
 //   counters  int32 [batch * h]  finished runs per unit, zero between calls
@@ -244,7 +262,7 @@ struct WsLayout {
 
 WsLayout ws_layout(int batch, int h, int head_dim, const Plan& pl) {
   WsLayout w{};
-  if (pl.n_blocks <= 1) return w;
+  if (pl.n_blocks <= 1 || pl.direct) return w;
   const size_t rows = static_cast<size_t>(batch) * h * pl.max_parts;
   w.counters = 0;
   w.runs = align_up(static_cast<size_t>(batch) * h * sizeof(int32_t), 256);
@@ -297,6 +315,7 @@ mlkv_status attention_impl(int layer, const void* q, const mlkv_cache* cache, co
   const int B = cache->batch, S = cache->capacity, D = cache->head_dim;
   const int max_len = max_len_hint <= 0 ? S : max_len_hint;
   const Plan pl = plan(map, layer, B, max_len, D);
+  if (const mlkv_status bs = check_plan_batch(pl, B); bs != MLKV_OK) return bs;
   const size_t need = workspace_need(B, map->h, D, pl);
   if (need > 0 && (!ws || ws_bytes < need))
     return fail(MLKV_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need,
@@ -328,6 +347,7 @@ mlkv_status attention_impl(int layer, const void* q, const mlkv_cache* cache, co
   p.max_parts = pl.max_parts;
   p.fused = pl.fused;
   p.waves = pl.waves;
+  p.direct = pl.direct;
   if (const char* env = std::getenv("MLKV_QK")) p.qk_valu = std::strcmp(env, "valu") == 0 ? 1 : 0;
   // One wave merges a row when units average at most 16 runs, else four;
   // the merge's first reads cover twice the average runs per unit.
@@ -583,8 +603,13 @@ size_t mlkv_cache_bytes(const mlkv_map* map, int batch, int capacity, int head_d
 size_t mlkv_workspace_bytes(const mlkv_map* map, int batch, int capacity, int head_dim) {
   if (!map || batch <= 0 || capacity <= 0 || (head_dim != 64 && head_dim != 128)) return 0;
   size_t best = 0;
+  const long budget = workgroup_budget(head_dim);
   for (int n = 0; n < map->l; ++n) {
-    // The largest plan any device or launch layout can pick: the most
+    // At least as many units as the device's workgroup budget: every plan is
+    // one workgroup per unit, which needs no workspace.
+    const long units = static_cast<long>(batch) * map->kv_count[n];
+    if (units > 1 && units >= budget) continue;
+    // Otherwise the largest plan any launch layout can pick: the most
     // workgroups (kMaxRunsPerUnit per unit) and the shortest runs (kMinTiles).
     Plan pl{};
     pl.max_tiles = tiles_of(capacity);
@@ -699,7 +724,9 @@ mlkv_status decode_step_check(const void* q_all, const void* k_new_all, const vo
   {
     const int max_len = max_len_hint <= 0 ? cache->capacity : max_len_hint;
     for (int n = 0; n < map->l; ++n) {
-      const size_t need = workspace_need(B, h, D, plan(map, n, B, max_len, D));
+      const Plan pl = plan(map, n, B, max_len, D);
+      if ((s = check_plan_batch(pl, B)) != MLKV_OK) return s;
+      const size_t need = workspace_need(B, h, D, pl);
       if (need > 0 && (!workspace || workspace_bytes < need))
         return fail(MLKV_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need,
                     workspace ? workspace_bytes : 0);

@@ -14,7 +14,8 @@ import subprocess
 
 import numpy as np
 
-from .workloads import WORKLOADS, Workload, get_workload  # noqa: F401
+from .workloads import (WORKLOADS, Workload, capacity_batch, get_workload,  # noqa: F401
+                        step_bytes_per_sequence)
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "gen.c")

@@ -101,8 +101,30 @@ WORKLOADS = {
              "at batch 8 on a 2000-token cache, the shape of the paper's throughput "
              "measurement; map sweep over the Table 2 variants",
         sweep=((12, 12), (12, 4), (4, 12), (12, 1), (4, 3), (6, 1), (2, 1), (1, 1), (4, 1))),
+    "capacity_ctx2048": Workload(
+        "capacity_ctx2048", l=12, h=12, m=2, g=1, D=64, B=0, ctx=2000, seed=0x4D4C4B56 + 7,
+        note="Pythia-160M shape: the largest batch whose 2048-token cache (2000 cached tokens "
+             "plus 48 decode steps, the paper's memory protocol) and step buffers fit in the "
+             "GPU's free memory, per Table 2 map; B is set at run time",
+        sweep=((12, 12), (12, 4), (4, 12), (12, 1), (4, 3), (6, 1), (4, 1), (2, 1), (1, 1))),
 }
 
 
 def get_workload(name: str) -> Workload:
     return WORKLOADS[name]
+
+
+def step_bytes_per_sequence(w: Workload, capacity: int, out_bytes: int = 2) -> int:
+    """Device bytes one sequence of a decode step occupies: its cache rows (keys
+    and values of every KV head, ``capacity`` slots, bf16: the per-sequence
+    share of the cache size 2*b*s*m*g*d_k), the queries and outputs of every
+    layer, the new token's key and value rows, and its length."""
+    cache = 2 * w.n_kv * capacity * w.D * 2
+    q_out = w.l * w.h * w.D * (2 + out_bytes)
+    new_rows = 2 * w.n_kv * w.D * 2
+    return cache + q_out + new_rows + 4
+
+
+def capacity_batch(w: Workload, budget_bytes: int, capacity: int, out_bytes: int = 2) -> int:
+    """The largest batch whose decode-step buffers fit in ``budget_bytes``."""
+    return max(0, int(budget_bytes) // step_bytes_per_sequence(w, capacity, out_bytes))

@@ -207,9 +207,31 @@ def test_workspace_covers_every_plan(env, monkeypatch):
             if B == 1 and tiles <= 16:
                 assert wg == 1
             rows = B * 12 * parts
-            need = 0 if wg == 1 else (al(B * 12 * 4) + al(B * 4) + al(wg * 32)
-                                      + al(rows * 64 * 4) + rows * 8)
+            direct = wg == B  # one workgroup per (sequence, KV head): no workspace
+            need = 0 if wg == 1 or direct else (al(B * 12 * 4) + al(B * 4) + al(wg * 32)
+                                                + al(rows * 64 * 4) + rows * 8)
             assert need <= ws
+
+
+def test_large_batch_plans_one_workgroup_per_unit(monkeypatch):
+    """Batches above the in-kernel schedule's table size (2048 sequences) run
+    with one workgroup per (sequence, KV head) and no workspace; a launch
+    layout that would still schedule runs for such a batch is refused before
+    any HIP call."""
+    mp = mlkv.Map.uniform(12, 12, 1, 1)  # MLKV-1: one KV head read by every layer
+    B, S = 5000, 2048
+    wg, parts = mp.plan(0, B, S, 64, S)
+    assert wg == B
+    assert mp.workspace_bytes(B, S, 64) == 0
+    L, names = mlkv.lib(), mlkv.STATUS_NAMES
+    F = mlkv.OUT_F32
+    ref = ctypes.byref(mlkv._Cache(0x10000, 0x20000, 1, B, S, 64))
+    monkeypatch.setenv("MLKV_WORKGROUPS", "100000")  # a budget above the unit count
+    assert mp.plan(0, B, S, 64, S)[0] > B
+    assert names[L.mlkv_decode_attention(0, 0x30000, ref, mp.handle, 0x40000, 0x50000, F, S,
+                                         0x60000, 1 << 30, None)] == "MLKV_ERR_UNSUPPORTED"
+    assert names[L.mlkv_decode_step(0x30000, 0x30000, 0x30000, ref, mp.handle, 0x40000, 0x50000,
+                                    F, S, 0x60000, 1 << 30, None)] == "MLKV_ERR_UNSUPPORTED"
 
 
 def test_layout_reference_matches_binding_packer():
@@ -234,3 +256,24 @@ def test_binding_fails_loudly_without_the_library(tmp_path):
     r = subprocess.run([sys.executable, "-c", code], env=env, capture_output=True, text=True,
                        cwd=os.path.dirname(os.path.dirname(os.path.abspath(__file__))), timeout=120)
     assert "raised" in r.stdout and "no fallback" in r.stdout, r.stdout + r.stderr
+
+
+def test_capacity_sizing_matches_the_cache_formula():
+    """The capacity experiment's per-sequence bytes: the cache part is the
+    paper's 2*b*s*m*g*d_k elements (b = 1) in bf16, which is what the library
+    reports for one sequence; the chosen batch is the largest that fits."""
+    import synth
+
+    w0 = synth.get_workload("capacity_ctx2048")
+    S = w0.capacity
+    assert S == 2048
+    for m, g in w0.sweep:
+        w = w0.with_map(m, g)
+        mp = mlkv.Map.uniform(w.l, w.h, m, g)
+        cache_part = 2 * S * m * g * w.D * 2
+        assert mp.cache_bytes(1, S, w.D) == cache_part
+        per_seq = synth.step_bytes_per_sequence(w, S)
+        assert per_seq == cache_part + w.l * w.h * w.D * 4 + 2 * m * g * w.D * 2 + 4
+        budget = 280 * 10**9
+        B = synth.capacity_batch(w, budget, S)
+        assert B * per_seq <= budget < (B + 1) * per_seq

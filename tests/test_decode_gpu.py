@@ -605,3 +605,99 @@ def test_full_size_7b_step_sampled_sequences():
                              inp["ctx"][sample])
     assert np.array_equal(k1, k0) and np.array_equal(v1, v0), "cache rows differ"
     check_close(out, ref, "7b full, sampled sequences")
+
+
+# ------------------------------------ batches above the schedule's tables --
+
+@pytest.mark.parametrize("m,g,B", [(1, 1, 4096), (4, 1, 3000), (12, 12, 2100)])
+def test_large_batch_step_sampled_sequences(m, g, B):
+    """Batches above 2048 sequences (the in-kernel schedule's table size) run
+    with one workgroup per (sequence, KV head).  The cache (ragged contexts
+    0..300, some sequences attending only their new token) is filled on the
+    device from a seeded generator; eight sampled sequences are checked
+    whole against the oracle run on their rows."""
+    w = synth.Workload(f"large_b{B}_m{m}g{g}", l=12, h=12, m=m, g=g, D=64, B=B,
+                       ctx_range=(0, 300), seed=0x4D4C + B)
+    inp = synth.step_inputs(w, with_cache=False)
+    S = inp["capacity"]
+    say(f"large batch {w.name}: filling the cache on the device")
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(B)
+    cache = mlkv.Cache.empty(w.n_kv, w.B, S, w.D)
+    cache.k.normal_(generator=gen)
+    cache.v.normal_(generator=gen)
+    mp = mlkv.Map.uniform(w.l, w.h, w.m, w.g)
+    assert mp.plan(0, B, S, w.D, S)[0] == B * w.g  # a workgroup per (sequence, KV head)
+    assert mp.workspace_bytes(B, S, w.D) == 0
+    kv_of, owner_of = oracle.map_uniform(w.l, w.h, w.m, w.g)
+    sample = sorted({0, 1, B // 3, B // 2, 2047, 2048, B - 2, B - 1})
+    sel = torch.tensor(sample, device="cuda")
+
+    def rows():
+        k = mlkv.bf16_bits(cache.k.index_select(1, sel))
+        v = unpack_v(mlkv.bf16_bits(cache.v.index_select(1, sel)), w.n_kv, len(sample), S, w.D)
+        return k, v
+
+    k0, v0 = rows()
+    out = torch.empty((w.l, w.B, w.h, w.D), dtype=torch.float32, device="cuda")
+    say(f"large batch {w.name}: running the step")
+    mlkv.decode_step(mlkv.bf16_tensor(inp["q"], "cuda"), mlkv.bf16_tensor(inp["k_new"], "cuda"),
+                     mlkv.bf16_tensor(inp["v_new"], "cuda"), cache, mp,
+                     torch.from_numpy(inp["ctx"]).cuda(), out, ws=None)
+    torch.cuda.synchronize()
+    k1, v1 = rows()
+    out = out.cpu().numpy()[:, sample]
+    say(f"large batch {w.name}: oracle on the sampled sequences")
+    k_ref, v_ref = k0.copy(), v0.copy()
+    ref = oracle.decode_step(np.ascontiguousarray(inp["q"][:, sample]), k_ref, v_ref,
+                             np.ascontiguousarray(inp["k_new"][sample]),
+                             np.ascontiguousarray(inp["v_new"][sample]), kv_of, owner_of,
+                             inp["ctx"][sample])
+    assert np.array_equal(k1, k_ref) and np.array_equal(v1, v_ref), "cache rows differ"
+    check_close(out, ref, f"large batch {w.name}, sampled sequences")
+
+
+def test_capacity_batch_step_sampled_sequences():
+    """The capacity experiment's configuration (bench.py --workload
+    capacity_ctx2048, MLKV-2): the largest batch whose 2048-token cache fits
+    the free device memory (about 2.6e5 sequences, a cache of ~270 GB with
+    sequences at offsets beyond 2^37 bytes), 2000 cached tokens each.  Six
+    sampled sequences, the last ones included, are checked whole against the
+    oracle run on their rows."""
+    import bench
+
+    w = synth.get_workload("capacity_ctx2048")
+    say("capacity batch: sizing and filling the cache on the device")
+    B, cache, q, kn, vn, ctx, out = bench.capacity_setup(w, "cuda", seed=0xCA9)
+    S = w.capacity
+    assert B > 100_000, B
+    say(f"capacity batch: B={B}")
+    mp = mlkv.Map.uniform(w.l, w.h, w.m, w.g)
+    kv_of, owner_of = oracle.map_uniform(w.l, w.h, w.m, w.g)
+    sample = [0, 1, B // 2, B - 3, B - 2, B - 1]
+    sel = torch.tensor(sample, device="cuda")
+
+    def rows():
+        k = mlkv.bf16_bits(cache.k.index_select(1, sel))
+        v = unpack_v(mlkv.bf16_bits(cache.v.index_select(1, sel)), w.n_kv, len(sample), S, w.D)
+        return k, v
+
+    k0, v0 = rows()
+    say("capacity batch: running the step")
+    mlkv.decode_step(q, kn, vn, cache, mp, ctx, out, max_len_hint=w.ctx + 1, ws=None)
+    torch.cuda.synchronize()
+    k1, v1 = rows()
+    got = out.index_select(1, sel).float().cpu().numpy().astype(np.float64)
+    q_h = mlkv.bf16_bits(q.index_select(1, sel))
+    kn_h = mlkv.bf16_bits(kn.index_select(0, sel))
+    vn_h = mlkv.bf16_bits(vn.index_select(0, sel))
+    del cache, q, kn, vn, out
+    torch.cuda.empty_cache()
+    say("capacity batch: oracle on the sampled sequences")
+    k_ref, v_ref = k0.copy(), v0.copy()
+    ref = oracle.decode_step(q_h, k_ref, v_ref, kn_h, vn_h, kv_of, owner_of,
+                             np.full(len(sample), w.ctx, dtype=np.int32))
+    assert np.array_equal(k1, k_ref) and np.array_equal(v1, v_ref), "cache rows differ"
+    # bf16 output (the benchmark's): its rounding (at most 2^-9 relative) fits
+    # inside the same bars as the fp32 output
+    check_close(got, ref, "capacity batch, sampled sequences (bf16 out)")
