@@ -287,14 +287,36 @@ def run_model(args, w):
     for _ in range(args.warmup):
         one_step()
     torch.cuda.synchronize()
-    log(f"[bench] timing {args.steps} model steps")
+    log(f"[bench] timing {args.steps} eager model steps")
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record(stream)
     for _ in range(args.steps):
         one_step()
     e1.record(stream)
     torch.cuda.synchronize()
-    ms_step = e0.elapsed_time(e1) / args.steps
+    ms_eager = e0.elapsed_time(e1) / args.steps
+    ms_step = ms_eager
+    if not args.no_graph:
+        # The step captured once in a HIP graph and replayed: the ~140
+        # dependent launches of a step go to the GPU without host launch
+        # gaps (replays equal the eager step bit for bit: GPU test).
+        log("[bench] capturing one model step in a HIP graph")
+        side = torch.cuda.Stream()
+        side.wait_stream(stream)
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph, stream=side):
+            one_step()
+        torch.cuda.synchronize()
+        for _ in range(max(args.warmup, 1)):
+            graph.replay()
+        torch.cuda.synchronize()
+        log(f"[bench] timing {args.steps} graph replays")
+        e0.record(stream)
+        for _ in range(args.steps):
+            graph.replay()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms_step = e0.elapsed_time(e1) / args.steps
     # attention launches of the same steps, timed by the library's event pairs
     mlkv.profile_enable(args.steps * w.l)
     done = 0
@@ -329,6 +351,8 @@ def run_model(args, w):
         "config": {"workload": w.name, "l": w.l, "h": w.h, "m": w.m, "g": w.g, "head_dim": w.D,
                    "d_model": d, "d_ff": w.d_ff, "batch": w.B, "ctx": w.ctx, "capacity": S,
                    "weight_bytes": weight_bytes, "kv_bytes_per_step": kv_bytes},
+        "launch": "one HIP graph per step" if not args.no_graph else "eager launches",
+        "eager_ms_per_step": round(ms_eager, 4),
         "attention_ms_per_step": round(attn_ms_step, 4),
         "attention_share": round(attn_ms_step / ms_step, 3),
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
@@ -442,6 +466,7 @@ def run_capacity(args, w):
     attn_bytes = (kv_bytes + qo_bytes) / w.l
     achieved = attn_bytes / avg / 1e9
     per_seq = synth.step_bytes_per_sequence(w, S)
+    floor = launch_floor(min(B * mp.layer_kv_count(0), 1 << 20))
     result = {
         "metric": "decode tokens/s at the largest batch whose 2048-token cache fits the GPU, "
                   "MLKV Pythia-160M shape",
@@ -467,7 +492,8 @@ def run_capacity(args, w):
                      "kernel": "attention_kernel", "avg_launch_us": round(avg * 1e6, 2),
                      "min_launch_us": round(min_ms * 1e3, 2),
                      "max_launch_us": round(max_ms * 1e3, 2), "launches": n_launch,
-                     "bytes_per_launch": int(attn_bytes)},
+                     "bytes_per_launch": int(attn_bytes), **floor,
+                     "attainable_frac": attainable(attn_bytes, floor["launch_floor_us"])},
     }
     if not args.no_cpu_baseline:
         log("[bench] cpu baseline (oracle)")
@@ -498,6 +524,25 @@ def run_capacity(args, w):
     print(json.dumps(result), flush=True)
 
 
+def launch_floor(workgroups: int) -> dict:
+    """The event-timing floor: the median event-pair duration of an empty
+    kernel with the attention launch's workgroup count, launched back to back
+    behind a GPU sleep (as the timed attention launches are)."""
+    import torch
+    import paper_2406_09297_amd as mlkv
+
+    torch.cuda.synchronize()
+    torch.cuda._sleep(SLEEP_CYCLES // 4)
+    return {"launch_floor_us": round(mlkv.profile_launch_floor(workgroups, 256, 100) * 1e3, 3)}
+
+
+def attainable(bytes_per_launch: float, floor_us: float) -> float:
+    """Highest fraction of the HBM peak a launch timed this way can show:
+    its bytes at peak rate plus the empty-launch floor."""
+    t_peak = bytes_per_launch / (HBM_PEAK_GBS * 1e3)  # microseconds
+    return round(t_peak / (t_peak + floor_us), 4)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -513,6 +558,8 @@ def main():
                     help="rotate the newest token's queries and keys inside the step "
                          "(GPT-NeoX rotary embedding; Pythia-160M: 16)")
     ap.add_argument("--rotary-base", type=float, default=10000.0)
+    ap.add_argument("--no-graph", action="store_true",
+                    help="model workload: time eager launches only (default: graph replays)")
     ap.add_argument("--pmc-pass", action="store_true",
                     help="for rocprofv3 --pmc runs: a 256 MiB reference copy, then a few steps")
     args = ap.parse_args()
@@ -667,6 +714,7 @@ def main():
                 "achieved": round(attn_bytes / c_avg / 1e9, 1),
                 "frac": round(attn_bytes / c_avg / 1e9 / HBM_PEAK_GBS, 4)}
     workgroups, max_parts = mp.plan(0, w.B, S, w.D, max_len)
+    floor = launch_floor(workgroups)
 
     result = {
         "metric": "decode-attention HBM GB/s (% of peak) + decode steps/s, MLKV Pythia-160M shape",
@@ -703,7 +751,8 @@ def main():
                      "bytes_per_launch": int(attn_bytes),
                      "cache_state": "natural layer order, back-to-back steps",
                      "ms_per_step_while_timed": round(ms_step_profiled, 5),
-                     "cold": cold},
+                     "cold": cold, **floor,
+                     "attainable_frac": attainable(attn_bytes, floor["launch_floor_us"])},
     }
     if not args.no_cpu_baseline:
         log("[bench] cpu baseline (oracle)")

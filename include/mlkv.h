@@ -395,6 +395,13 @@ mlkv_status mlkv_profile_read(int* launches, double* total_ms, double* min_ms, d
 mlkv_status mlkv_profile_durations(double* ms, int capacity, int* count);
 /* Stops timing and destroys the events. */
 void mlkv_profile_disable(void);
+/* The floor of that timing: `reps` launches of an empty kernel with
+ * `workgroups` x `threads` work-items, each bracketed by an event pair
+ * recorded with its dispatch exactly as above, enqueued on `stream` back to
+ * back; synchronizes and returns the median duration (ms).  What no kernel
+ * timed this way can go below.  Errors: MLKV_ERR_INVALID_ARG, MLKV_ERR_HIP. */
+mlkv_status mlkv_profile_launch_floor(int workgroups, int threads, int reps, hipStream_t stream,
+                                      double* median_ms);
 
 #ifdef __cplusplus
 }

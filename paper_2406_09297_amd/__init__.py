@@ -37,7 +37,8 @@ EXPORTS = [
     "mlkv_map_layer_owned_count", "mlkv_map_layer_owned_begin", "mlkv_cache_bytes",
     "mlkv_workspace_bytes", "mlkv_cache_append", "mlkv_decode_attention", "mlkv_decode_step",
     "mlkv_plan", "mlkv_workspace_init", "mlkv_profile_enable", "mlkv_profile_read",
-    "mlkv_profile_durations", "mlkv_profile_disable", "mlkv_decode_step_rope",
+    "mlkv_profile_durations", "mlkv_profile_disable", "mlkv_profile_launch_floor",
+    "mlkv_decode_step_rope",
     "mlkv_cache_append_rows", "mlkv_prefill_attention", "mlkv_prefill_step",
     "mlkv_model_create", "mlkv_model_destroy", "mlkv_model_workspace_bytes",
     "mlkv_model_decode_step",
@@ -102,6 +103,8 @@ def lib():
             "mlkv_profile_read": ([ctypes.POINTER(I)] + [ctypes.POINTER(ctypes.c_double)] * 3, S),
             "mlkv_profile_durations": ([ctypes.POINTER(ctypes.c_double), I, ctypes.POINTER(I)], S),
             "mlkv_profile_disable": ([], None),
+            "mlkv_profile_launch_floor": ([I, I, I, ctypes.c_void_p,
+                                           ctypes.POINTER(ctypes.c_double)], S),
         }
         for name, (args, res) in sig.items():
             f = getattr(L, name)
@@ -454,3 +457,13 @@ def profile_durations(capacity: int) -> np.ndarray:
 
 def profile_disable():
     lib().mlkv_profile_disable()
+
+
+def profile_launch_floor(workgroups: int, threads: int = 256, reps: int = 100,
+                         stream=None) -> float:
+    """Median event-pair duration (ms) of an empty kernel of the given shape
+    (mlkv_profile_launch_floor)."""
+    ms = ctypes.c_double()
+    _check(lib().mlkv_profile_launch_floor(workgroups, threads, reps, _stream(stream),
+                                           ctypes.byref(ms)))
+    return ms.value

@@ -150,5 +150,8 @@ int wide_waves();                      // waves per workgroup of the one-run-per
 int compute_units();                   // compute units of the current device (0: unknown)
 int default_waves();                   // waves per workgroup otherwise
 hipError_t launch_fill(uint32_t* dst, size_t n_words, uint32_t value, hipStream_t stream);
+// An empty kernel bracketed by start/stop (launch-overhead reference).
+hipError_t launch_empty_timed(int workgroups, int threads, hipStream_t stream, hipEvent_t start,
+                              hipEvent_t stop);
 
 }  // namespace mlkv

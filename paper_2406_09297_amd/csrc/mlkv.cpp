@@ -3,6 +3,7 @@
 // Every argument error is reported before any HIP call.
 #include "mlkv.h"
 
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -1191,6 +1192,37 @@ mlkv_status mlkv_profile_durations(double* ms, int capacity, int* count) {
     ms[i] = t;
   }
   *count = n;
+  return ok();
+}
+
+mlkv_status mlkv_profile_launch_floor(int workgroups, int threads, int reps, hipStream_t stream,
+                                      double* median_ms) {
+  if (workgroups <= 0 || threads <= 0 || threads > 1024 || reps <= 0 || !median_ms)
+    return fail(MLKV_ERR_INVALID_ARG, "workgroups, threads (<= 1024), reps must be positive");
+  std::vector<hipEvent_t> ev(2 * static_cast<size_t>(reps), nullptr);
+  mlkv_status s = MLKV_OK;
+  for (auto& e : ev)
+    if (hipEventCreateWithFlags(&e, hipEventDisableSystemFence) != hipSuccess) {
+      s = fail(MLKV_ERR_HIP, "hipEventCreate failed");
+      break;
+    }
+  std::vector<double> ms;
+  for (int i = 0; s == MLKV_OK && i < reps; ++i)
+    if (mlkv::launch_empty_timed(workgroups, threads, stream, ev[2 * i], ev[2 * i + 1]) !=
+        hipSuccess)
+      s = fail(MLKV_ERR_HIP, "empty launch failed");
+  for (int i = 0; s == MLKV_OK && i < reps; ++i) {
+    float t = 0.f;
+    if (hipEventSynchronize(ev[2 * i + 1]) != hipSuccess ||
+        hipEventElapsedTime(&t, ev[2 * i], ev[2 * i + 1]) != hipSuccess)
+      s = fail(MLKV_ERR_HIP, "reading floor events failed");
+    ms.push_back(t);
+  }
+  for (hipEvent_t e : ev)
+    if (e) (void)hipEventDestroy(e);
+  if (s != MLKV_OK) return s;
+  std::sort(ms.begin(), ms.end());
+  *median_ms = ms[ms.size() / 2];
   return ok();
 }
 

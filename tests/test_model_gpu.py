@@ -144,3 +144,65 @@ def test_model_rejects_missing_or_extra_key_weights():
     bad[0]["w_v"] = None  # the owner without value weights
     with pytest.raises(mlkv.MLKVError):
         mlkv.Model(mp, 256, 256, 64, bad)
+
+
+@pytest.mark.parametrize("mg", [(4, 1), (12, 12)])
+def test_model_step_captured_in_a_hip_graph_replays_like_eager(mg):
+    """The benchmark replays a captured model step (torch's graph capture on
+    the library's stream, rocBLAS included).  Every replay, with eager steps
+    between replays, must give the eager step's residual stream and cache
+    rows bit for bit."""
+    m, g = mg
+    w = synth.get_workload("model_b8").with_map(m, g).scaled(B=4, ctx=300)
+    say(f"model graph {w.name}: building")
+    mp = mlkv.Map.uniform(w.l, w.h, w.m, w.g)
+    _, owner_of = oracle.map_uniform(w.l, w.h, w.m, w.g)
+    owned = [int((owner_of == n).sum()) for n in range(w.l)]
+    weights = synth.model_weights(w.seed, w.l, w.h, w.D, w.d_ff, owned)
+    dev = [{k: (None if v is None else mlkv.bf16_tensor(v, "cuda")) for k, v in lw.items()}
+           for lw in weights]
+    d = w.h * w.D
+    model = mlkv.Model(mp, d, w.d_ff, w.D, dev, rotary_dims=16)
+    inp = synth.step_inputs(w, fill=0)
+    S = inp["capacity"]
+    cache = mlkv.Cache.empty(w.n_kv, w.B, S, w.D)
+    cache.load_rows(inp["k_cache"], inp["v_cache"])
+    k0, v0 = cache.k.clone(), cache.v.clone()
+    x0 = torch.from_numpy(synth.bf16_to_f32(synth.normal_bf16(w.seed, 0, (w.B, d))).copy()).cuda()
+    x = x0.clone()
+    ctx = torch.from_numpy(inp["ctx"]).cuda()
+    ws = model.workspace(w.B, S)
+
+    def step():
+        model.decode_step(x, cache, ctx, ws)
+
+    step()  # first call outside capture (library and rocBLAS set-up)
+    torch.cuda.synchronize()
+
+    def reset():
+        x.copy_(x0)
+        cache.k.copy_(k0)
+        cache.v.copy_(v0)
+        torch.cuda.synchronize()
+
+    reset()
+    step()
+    torch.cuda.synchronize()
+    x_ref, k_ref, v_ref = x.clone(), cache.k.clone(), cache.v.clone()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    graph = torch.cuda.CUDAGraph()
+    reset()
+    say(f"model graph {w.name}: capturing")
+    with torch.cuda.graph(graph, stream=side):
+        step()
+    torch.cuda.synchronize()
+    for rep in range(3):
+        reset()
+        say(f"model graph {w.name}: replay {rep}")
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(x, x_ref), f"replay {rep}: residual stream differs"
+        assert torch.equal(cache.k, k_ref) and torch.equal(cache.v, v_ref), f"replay {rep}: cache"
+        step()  # eager work between replays
+        torch.cuda.synchronize()
