@@ -724,15 +724,6 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(AttnParams p) {
   }
 }
 
-// Launch-overhead reference for timing: no work at all.
-__global__ void empty_kernel() {}
-
-hipError_t launch_empty_timed(int workgroups, int threads, hipStream_t stream, hipEvent_t start,
-                              hipEvent_t stop) {
-  hipExtLaunchKernelGGL(empty_kernel, dim3(workgroups), dim3(threads), 0, stream, start, stop, 0);
-  return hipGetLastError();
-}
-
 __global__ void fill_kernel(uint32_t* dst, size_t n, uint32_t value) {
   for (size_t i = blockIdx.x * static_cast<size_t>(blockDim.x) + threadIdx.x; i < n;
        i += static_cast<size_t>(gridDim.x) * blockDim.x)
