@@ -39,6 +39,20 @@ namespace mlkv {
 // common case needs no cross-lane traffic); on a yes, the column maxima
 // through the wave and the rescale of the blocks that need it; then the
 // weights and the value products of all blocks.
+// Maximum of a lane's eight scores in four three-input maxima.  Written as
+// instructions because fmaxf on matrix-core results makes the compiler
+// canonicalise every input first (a max of the value with itself), which
+// doubled the count; the scores are finite or -inf, never NaN.
+__device__ __forceinline__ float max8(const float (&x)[8]) {
+  float a, b, c;
+  asm("v_max3_f32 %0, %1, %2, %3" : "=v"(a) : "v"(x[0]), "v"(x[1]), "v"(x[2]));
+  asm("v_max3_f32 %0, %1, %2, %3" : "=v"(b) : "v"(x[3]), "v"(x[4]), "v"(x[5]));
+  asm("v_max3_f32 %0, %1, %2, %3" : "=v"(c) : "v"(x[6]), "v"(x[7]), "v"(a));
+  float m;
+  asm("v_max_f32 %0, %1, %2" : "=v"(m) : "v"(b), "v"(c));
+  return m;
+}
+
 template <int D, int NB, bool MASK>
 __device__ __forceinline__ void prefill_tile(WaveState<D> (&st)[NB], Tile<D>& t,
                                              const bf16x8 (&qf)[NB][Tile<D>::KK], int t0, int L,
@@ -76,8 +90,7 @@ __device__ __forceinline__ void prefill_tile(WaveState<D> (&st)[NB], Tile<D>& t,
   bool up = false;
 #pragma unroll
   for (int c = 0; c < NB; ++c) {
-    lmax[c] = fmaxf(fmaxf(fmaxf(x[c][0], x[c][1]), fmaxf(x[c][2], x[c][3])),
-                    fmaxf(fmaxf(x[c][4], x[c][5]), fmaxf(x[c][6], x[c][7])));
+    lmax[c] = max8(x[c]);
     up = up || fmaf(lmax[c], scale_log2, -st[c].m) > kLazyRescale;
   }
   if (__ballot(up)) {  // some column needs a new reference max
