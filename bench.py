@@ -428,6 +428,7 @@ def run_capacity(args, w):
     import paper_2406_09297_amd as mlkv
 
     dev = "cuda:0"
+    hbm_ref = read_reference(64 << 20)["hbm_2GiB_gbs"]  # before the batch takes the memory
     log(f"[bench] capacity workload {w.name}: sizing and filling the batch")
     B, cache, q, kn, vn, ctx, out = capacity_setup(w, dev, w.seed)
     S = w.capacity
@@ -493,7 +494,9 @@ def run_capacity(args, w):
                      "min_launch_us": round(min_ms * 1e3, 2),
                      "max_launch_us": round(max_ms * 1e3, 2), "launches": n_launch,
                      "bytes_per_launch": int(attn_bytes), **floor,
-                     "attainable_frac": attainable(attn_bytes, floor["launch_floor_us"])},
+                     "attainable_frac": attainable(attn_bytes, floor["launch_floor_us"]),
+                     "read_reference": {"hbm_2GiB_gbs": hbm_ref},
+                     "frac_of_hbm_read": round(achieved / hbm_ref, 4)},
     }
     if not args.no_cpu_baseline:
         log("[bench] cpu baseline (oracle)")
@@ -534,6 +537,27 @@ def launch_floor(workgroups: int) -> dict:
     torch.cuda.synchronize()
     torch.cuda._sleep(SLEEP_CYCLES // 4)
     return {"launch_floor_us": round(mlkv.profile_launch_floor(workgroups, 256, 100) * 1e3, 3)}
+
+
+def read_reference(bytes_per_launch: int, hbm_bytes: int = 2 << 30) -> dict:
+    """Achievable read rates, timed like the attention launches (event pairs
+    recorded with each dispatch): a plain streaming read of the same bytes as
+    one attention launch, warm in the caches (median of 20 back-to-back
+    launches), and of a 2 GiB buffer, eight times the Infinity Cache (HBM)."""
+    import torch
+    import paper_2406_09297_amd as mlkv
+
+    out = {}
+    same = torch.ones((int(bytes_per_launch) + 16 + 15) // 16 * 4, dtype=torch.int32, device="cuda")
+    mlkv.profile_read_bandwidth(same, reps=3)  # warm
+    out["same_bytes_warm_gbs"] = round(mlkv.profile_read_bandwidth(same, reps=20)[0], 1)
+    del same
+    if hbm_bytes:
+        big = torch.ones(hbm_bytes // 4, dtype=torch.int32, device="cuda")
+        out["hbm_2GiB_gbs"] = round(mlkv.profile_read_bandwidth(big, reps=5)[0], 1)
+        del big
+    torch.cuda.empty_cache()
+    return out
 
 
 def attainable(bytes_per_launch: float, floor_us: float) -> float:
@@ -715,6 +739,7 @@ def main():
                 "frac": round(attn_bytes / c_avg / 1e9 / HBM_PEAK_GBS, 4)}
     workgroups, max_parts = mp.plan(0, w.B, S, w.D, max_len)
     floor = launch_floor(workgroups)
+    ref = read_reference(int(attn_bytes))
 
     result = {
         "metric": "decode-attention HBM GB/s (% of peak) + decode steps/s, MLKV Pythia-160M shape",
@@ -752,7 +777,9 @@ def main():
                      "cache_state": "natural layer order, back-to-back steps",
                      "ms_per_step_while_timed": round(ms_step_profiled, 5),
                      "cold": cold, **floor,
-                     "attainable_frac": attainable(attn_bytes, floor["launch_floor_us"])},
+                     "attainable_frac": attainable(attn_bytes, floor["launch_floor_us"]),
+                     "read_reference": ref,
+                     "frac_of_same_bytes_read": round(achieved / ref["same_bytes_warm_gbs"], 4)},
     }
     if not args.no_cpu_baseline:
         log("[bench] cpu baseline (oracle)")

@@ -402,6 +402,17 @@ void mlkv_profile_disable(void);
  * timed this way can go below.  Errors: MLKV_ERR_INVALID_ARG, MLKV_ERR_HIP. */
 mlkv_status mlkv_profile_launch_floor(int workgroups, int threads, int reps, hipStream_t stream,
                                       double* median_ms);
+/* The achievable read rate the attention kernels are compared with: `reps`
+ * back-to-back launches of a plain streaming read (every 16-byte piece of
+ * the first bytes - 16 bytes of `buffer` loaded once, eight loads in flight
+ * per thread, 8 workgroups of 256 per compute unit), each timed by an event
+ * pair recorded with its dispatch; returns the median and the best rate in
+ * GB/s.  buffer: caller-owned device memory, 16-byte aligned, at least 16 KiB;
+ * its contents are not changed except, for one impossible data pattern, the
+ * last 16 bytes.  A buffer several times the 256 MB Infinity Cache measures
+ * HBM.  Errors: MLKV_ERR_INVALID_ARG, MLKV_ERR_ALIGNMENT, MLKV_ERR_HIP. */
+mlkv_status mlkv_profile_read_bandwidth(const void* buffer, size_t bytes, int reps,
+                                        hipStream_t stream, double* median_gbs, double* best_gbs);
 
 #ifdef __cplusplus
 }

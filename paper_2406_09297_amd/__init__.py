@@ -38,6 +38,7 @@ EXPORTS = [
     "mlkv_workspace_bytes", "mlkv_cache_append", "mlkv_decode_attention", "mlkv_decode_step",
     "mlkv_plan", "mlkv_workspace_init", "mlkv_profile_enable", "mlkv_profile_read",
     "mlkv_profile_durations", "mlkv_profile_disable", "mlkv_profile_launch_floor",
+    "mlkv_profile_read_bandwidth",
     "mlkv_decode_step_rope",
     "mlkv_cache_append_rows", "mlkv_prefill_attention", "mlkv_prefill_step",
     "mlkv_model_create", "mlkv_model_destroy", "mlkv_model_workspace_bytes",
@@ -105,6 +106,9 @@ def lib():
             "mlkv_profile_disable": ([], None),
             "mlkv_profile_launch_floor": ([I, I, I, ctypes.c_void_p,
                                            ctypes.POINTER(ctypes.c_double)], S),
+            "mlkv_profile_read_bandwidth": ([ctypes.c_void_p, ctypes.c_size_t, I, ctypes.c_void_p,
+                                             ctypes.POINTER(ctypes.c_double),
+                                             ctypes.POINTER(ctypes.c_double)], S),
         }
         for name, (args, res) in sig.items():
             f = getattr(L, name)
@@ -457,6 +461,16 @@ def profile_durations(capacity: int) -> np.ndarray:
 
 def profile_disable():
     lib().mlkv_profile_disable()
+
+
+def profile_read_bandwidth(buffer: torch.Tensor, reps: int = 10, stream=None):
+    """(median, best) GB/s of a plain streaming read of `buffer`
+    (mlkv_profile_read_bandwidth)."""
+    med, best = ctypes.c_double(), ctypes.c_double()
+    _check(lib().mlkv_profile_read_bandwidth(buffer.data_ptr(), buffer.numel() * buffer.element_size(),
+                                             reps, _stream(stream), ctypes.byref(med),
+                                             ctypes.byref(best)))
+    return med.value, best.value
 
 
 def profile_launch_floor(workgroups: int, threads: int = 256, reps: int = 100,

@@ -153,5 +153,9 @@ hipError_t launch_fill(uint32_t* dst, size_t n_words, uint32_t value, hipStream_
 // An empty kernel bracketed by start/stop (launch-overhead reference).
 hipError_t launch_empty_timed(int workgroups, int threads, hipStream_t stream, hipEvent_t start,
                               hipEvent_t stop);
+// A streaming read of `bytes` (a multiple of 16) at src bracketed by
+// start/stop; sink receives one word only for an impossible data pattern.
+hipError_t launch_stream_read_timed(const void* src, size_t bytes, uint32_t* sink, int workgroups,
+                                    hipStream_t stream, hipEvent_t start, hipEvent_t stop);
 
 }  // namespace mlkv

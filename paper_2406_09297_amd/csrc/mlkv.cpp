@@ -1237,6 +1237,44 @@ mlkv_status mlkv_profile_launch_floor(int workgroups, int threads, int reps, hip
   return ok();
 }
 
+mlkv_status mlkv_profile_read_bandwidth(const void* buffer, size_t bytes, int reps,
+                                        hipStream_t stream, double* median_gbs, double* best_gbs) {
+  if (!buffer || bytes < 16 * 1024 || reps <= 0 || !median_gbs || !best_gbs)
+    return fail(MLKV_ERR_INVALID_ARG, "buffer, bytes (>= 16 KiB), reps and outputs required");
+  if (!aligned16(buffer)) return fail(MLKV_ERR_ALIGNMENT, "buffer must be 16-byte aligned");
+  const size_t body = bytes / 16 * 16 - 16;  // the last 16 bytes hold the sink word
+  uint32_t* sink = reinterpret_cast<uint32_t*>(static_cast<char*>(const_cast<void*>(buffer)) + body);
+  long cus = mlkv::compute_units();
+  if (cus <= 0) cus = kFallbackResident / 3;
+  const int workgroups = static_cast<int>(8 * cus);
+  std::vector<hipEvent_t> ev(2 * static_cast<size_t>(reps), nullptr);
+  mlkv_status s = MLKV_OK;
+  for (auto& e : ev)
+    if (hipEventCreateWithFlags(&e, hipEventDisableSystemFence) != hipSuccess) {
+      s = fail(MLKV_ERR_HIP, "hipEventCreate failed");
+      break;
+    }
+  for (int i = 0; s == MLKV_OK && i < reps; ++i)
+    if (mlkv::launch_stream_read_timed(buffer, body, sink, workgroups, stream, ev[2 * i],
+                                       ev[2 * i + 1]) != hipSuccess)
+      s = fail(MLKV_ERR_HIP, "stream read launch failed");
+  std::vector<double> gbs;
+  for (int i = 0; s == MLKV_OK && i < reps; ++i) {
+    float t = 0.f;
+    if (hipEventSynchronize(ev[2 * i + 1]) != hipSuccess ||
+        hipEventElapsedTime(&t, ev[2 * i], ev[2 * i + 1]) != hipSuccess)
+      s = fail(MLKV_ERR_HIP, "reading stream events failed");
+    gbs.push_back(static_cast<double>(body) / (t * 1e-3) / 1e9);
+  }
+  for (hipEvent_t e : ev)
+    if (e) (void)hipEventDestroy(e);
+  if (s != MLKV_OK) return s;
+  std::sort(gbs.begin(), gbs.end());
+  *median_gbs = gbs[gbs.size() / 2];
+  *best_gbs = gbs.back();
+  return ok();
+}
+
 void mlkv_profile_disable(void) {
   Profile& prof = g_profile;
   for (hipEvent_t e : prof.start)
