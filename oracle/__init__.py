@@ -71,6 +71,8 @@ def _load():
         lib.oracle_append_rows.restype = I
         lib.oracle_prefill_step.argtypes = [I, I, I, I, I, I, I, P, P, P, P, P, P, P, P, P]
         lib.oracle_prefill_step.restype = None
+        lib.oracle_threads.argtypes = [I]
+        lib.oracle_threads.restype = I
         _lib = lib
     return _lib
 
@@ -269,3 +271,9 @@ def decode_step_rope(q_all, k_cache, v_cache, k_new, v_new, kv_of, owner_of, ctx
 def to_f32_rne(x: np.ndarray) -> np.ndarray:
     """fp64 -> fp32 rounding of oracle outputs (numpy rounds to nearest even)."""
     return np.asarray(x, dtype=np.float64).astype(np.float32)
+
+
+def threads(n: int = 0) -> int:
+    """Host threads of the oracle's OpenMP loops: n > 0 sets them; returns
+    the count in effect (timing only; results do not depend on it)."""
+    return int(_load().oracle_threads(n))

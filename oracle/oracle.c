@@ -49,6 +49,7 @@
  * appended at consecutive slots with nothing else touched.
  */
 #include <math.h>
+#include <omp.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -361,4 +362,11 @@ void oracle_decode_step_rope(int l, int B, int h, int n_kv, int S, int D, int rd
     }
   oracle_decode_step(l, B, h, n_kv, S, D, kv_of, owner_of, q_rot, Kc, Vc, k_rot, v_new, ctx,
                      lens_scratch, out_all);
+}
+
+/* Host threads the OpenMP loops above use (n > 0 sets them); returns the
+ * count in effect.  Timing only: the arithmetic does not depend on it. */
+int oracle_threads(int n) {
+  if (n > 0) omp_set_num_threads(n);
+  return omp_get_max_threads();
 }
