@@ -354,13 +354,17 @@ mlkv_status mlkv_model_decode_step(mlkv_model* model, float* x, const mlkv_cache
  * equally by `workgroups` workgroups (two per compute unit, or the device's
  * resident capacity if lower; capped at 128 per (sequence, KV head) and at
  * one per 4 tiles, at least one per (sequence, KV head); one workgroup for at
- * most 16 tiles); `max_parts` bounds the workgroups covering one sequence.
+ * most 16 tiles; with at least as many (sequence, KV head) pairs as the
+ * budget, exactly one workgroup per pair); `max_parts` bounds the workgroups
+ * covering one sequence.
  * Environment overrides, read on every call (tests and tuning):
  *   MLKV_WORKGROUPS=n   workgroup budget n instead of the device's;
  *   MLKV_COMBINE=kernel always merge split runs with the separate merge
  *                       kernel (by default the last run of each unit merges
  *                       them in place when they fit the kernel's staging
- *                       area without reducing the workgroup count);
+ *                       area, at the full workgroup count or, failing that,
+ *                       at a whole multiple of the compute units no smaller
+ *                       than one per unit);
  *   MLKV_COMBINE=fused  merge in place also when that costs up to half of
  *                       the workgroups;
  *   MLKV_WIDE=1         one run per unit on a wider workgroup (no partials,
