@@ -363,8 +363,8 @@ mlkv_status mlkv_model_decode_step(mlkv_model* model, float* x, const mlkv_cache
  *                       kernel (by default the last run of each unit merges
  *                       them in place when they fit the kernel's staging
  *                       area, at the full workgroup count or, failing that,
- *                       at a whole multiple of the compute units no smaller
- *                       than one per unit);
+ *                       on fewer workgroups, a whole multiple of the compute
+ *                       units and at least one per compute unit);
  *   MLKV_COMBINE=fused  merge in place also when that costs up to half of
  *                       the workgroups;
  *   MLKV_WIDE=1         one run per unit on a wider workgroup (no partials,
