@@ -124,6 +124,43 @@ struct ResidualParams {  // x += (a32 + b_o) + (m32 + b_2)
   const uint16_t *b_o, *b_2;
   int rows, d;
 };
+// Fused model-step products (B operand = batch rows, padded to 16 per tile).
+// Weights are packed at model creation into MFMA A-operand tiles: tile
+// (nt, kb) of a matrix with KB k-blocks holds output columns 16 nt .. +15 and
+// inputs 32 kb .. +31 at element offset (nt * KB + kb) * 512; inside it,
+// element (n, k) sits at ((k % 32) / 8) * 128 + (n % 16) * 8 + k % 8, so lane
+// l of a wave reads elements 8 l .. 8 l + 7 (16 contiguous bytes).
+constexpr int kPackTile = 512;  // bf16 elements per packed tile
+constexpr int kFusedMaxBatch = 64;  // rows of a model step on the fused path
+struct PackParams {  // source W[k_rows][n_cols] row-major -> tiles (nt0 + nt, kb0 + kb)
+  const uint16_t* src;
+  uint16_t* dst;
+  int k_rows, n_cols, kb_total, kb0, nt0, nt_count;  // k_rows % 32 == 0
+};
+struct LayerInParams {  // LN1/LN2 of x -> [q | k | v | fc1] products and their epilogues
+  const float* x;                        // [rows][d] residual stream
+  const uint16_t *ln1_w, *ln1_b, *ln2_w, *ln2_b;
+  const uint16_t* w;                     // packed, column blocks of D: h q, owned k, owned v, fc1
+  const uint16_t *b_q, *b_k, *b_v, *b_fc1;
+  uint16_t* q16;                         // [rows][h*D]
+  uint16_t *k16, *v16;                   // [rows][kv_stride], owned block at kv_offset
+  uint16_t* f16;                         // [rows][ff], bf16(GELU(h2 W_1 + b_1))
+  const int32_t* pos;                    // [rows] rotation position
+  int rows, d, h, owned, ff, kv_stride, kv_offset, dims;
+  float eps;
+  double inv_freq[kMaxRopePairs];
+};
+struct LayerOutParams {  // x += (o W_o + b_o) + (f W_2 + b_2)
+  const uint16_t *o16, *f16;  // [rows][hD], [rows][ff] bf16
+  const uint16_t* w;          // packed, K = hD + ff (W_o rows, then W_2 rows), N = d
+  const uint16_t *b_o, *b_2;
+  float* x;
+  int rows, d, hD, ff;
+};
+hipError_t launch_pack(const PackParams& p, hipStream_t stream);
+hipError_t launch_layer_in(const LayerInParams& p, int head_dim, hipStream_t stream);
+hipError_t launch_layer_out(const LayerOutParams& p, hipStream_t stream);
+
 hipError_t launch_norm2(const NormParams& p, hipStream_t stream);
 hipError_t launch_qkv_epilogue(const QkvEpilogueParams& p, hipStream_t stream);
 hipError_t launch_gelu(const GeluParams& p, hipStream_t stream);

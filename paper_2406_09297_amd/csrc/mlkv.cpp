@@ -34,6 +34,11 @@ struct mlkv_model {
   double inv_freq[mlkv::kMaxRopePairs] = {};
   std::vector<mlkv_layer_weights> layers;
   rocblas_handle blas = nullptr;
+  // Packed weights of the fused path (NULL when d_ff % 32 != 0): per layer
+  // the layer-in matrix [W_q | W_k | W_v | W_1] and the layer-out matrix
+  // [W_o ; W_2], element offsets into `packed`.
+  uint16_t* packed = nullptr;
+  std::vector<size_t> in_off, out_off;
 };
 
 namespace {
@@ -988,6 +993,60 @@ mlkv_status hip_ok(hipError_t e, const char* what) {
   return MLKV_OK;
 }
 
+// Copies every layer's matrices into the fused path's MFMA tiles (one device
+// allocation; the null stream, finished before returning).
+mlkv_status pack_weights(mlkv_model* m) {
+  const mlkv_map* map = m->map;
+  const int D = m->D, NT = D / 16, d = m->d, ff = m->d_ff, h = map->h, hD = h * D;
+  const int KB = d / 32, ff_blocks = (ff + D - 1) / D;
+  size_t total = 0;
+  for (int n = 0; n < map->l; ++n) {
+    const int owned = map->own_count[n];
+    m->in_off.push_back(total);
+    total += static_cast<size_t>(h + 2 * owned + ff_blocks) * NT * KB * mlkv::kPackTile;
+    m->out_off.push_back(total);
+    total += static_cast<size_t>(d) * (hD + ff);
+  }
+  void* mem = nullptr;
+  if (hipMalloc(&mem, total * sizeof(uint16_t)) != hipSuccess)
+    return fail(MLKV_ERR_HIP, "hipMalloc of %zu bytes of packed weights failed", total * 2);
+  m->packed = static_cast<uint16_t*>(mem);
+  auto u16 = [](const void* p) { return static_cast<const uint16_t*>(p); };
+  auto pack = [&](const void* src, int k_rows, int n_cols, uint16_t* dst, int kb_total, int kb0,
+                  int nt0, int nt_count) {
+    const mlkv::PackParams pp{u16(src), dst, k_rows, n_cols, kb_total, kb0, nt0, nt_count};
+    return hip_ok(mlkv::launch_pack(pp, nullptr), "weight packing");
+  };
+  mlkv_status s;
+  for (int n = 0; n < map->l; ++n) {
+    const mlkv_layer_weights& lw = m->layers[n];
+    const int owned = map->own_count[n];
+    uint16_t* win = m->packed + m->in_off[n];
+    uint16_t* wout = m->packed + m->out_off[n];
+    if ((s = pack(lw.w_q, d, hD, win, KB, 0, 0, h * NT)) != MLKV_OK) return s;
+    if (owned > 0 &&
+        ((s = pack(lw.w_k, d, owned * D, win, KB, 0, h * NT, owned * NT)) != MLKV_OK ||
+         (s = pack(lw.w_v, d, owned * D, win, KB, 0, (h + owned) * NT, owned * NT)) != MLKV_OK))
+      return s;
+    if ((s = pack(lw.w_fc1, d, ff, win, KB, 0, (h + 2 * owned) * NT, ff_blocks * NT)) != MLKV_OK ||
+        (s = pack(lw.w_o, hD, d, wout, (hD + ff) / 32, 0, 0, d / 16)) != MLKV_OK ||
+        (s = pack(lw.w_fc2, ff, d, wout, (hD + ff) / 32, hD / 32, 0, d / 16)) != MLKV_OK)
+      return s;
+  }
+  const hipError_t e = hipStreamSynchronize(nullptr);
+  if (e != hipSuccess) return fail(MLKV_ERR_HIP, "weight packing: %s", hipGetErrorString(e));
+  return MLKV_OK;
+}
+
+// The fused path serves batches up to kFusedMaxBatch rows (its products
+// re-read the weights once per 16 rows); MLKV_MODEL_GEMM=library forces the
+// library GEMMs.
+bool use_fused(const mlkv_model* m, int B) {
+  if (!m->packed || B > mlkv::kFusedMaxBatch) return false;
+  const char* env = std::getenv("MLKV_MODEL_GEMM");
+  return !(env && std::strcmp(env, "library") == 0);
+}
+
 }  // namespace
 
 mlkv_status mlkv_model_create(const mlkv_map* map, int d_model, int d_ff, int head_dim,
@@ -1035,6 +1094,10 @@ mlkv_status mlkv_model_create(const mlkv_map* map, int d_model, int d_ff, int he
     delete m;
     return fail(MLKV_ERR_HIP, "rocblas_create_handle failed");
   }
+  if (d_ff % 32 == 0 && (s = pack_weights(m)) != MLKV_OK) {
+    mlkv_model_destroy(m);
+    return s;
+  }
   *out = m;
   return ok();
 }
@@ -1042,6 +1105,7 @@ mlkv_status mlkv_model_create(const mlkv_map* map, int d_model, int d_ff, int he
 void mlkv_model_destroy(mlkv_model* model) {
   if (!model) return;
   if (model->blas) (void)rocblas_destroy_handle(model->blas);
+  if (model->packed) (void)hipFree(model->packed);
   delete model;
 }
 
@@ -1084,16 +1148,76 @@ mlkv_status mlkv_model_decode_step(mlkv_model* model, float* x, const mlkv_cache
   auto f32 = [&](size_t off) { return reinterpret_cast<float*>(base + off); };
   const int hD = h * D, kvD = n_kv * D, d = model->d, ff = model->d_ff;
   auto u16 = [](const void* p) { return static_cast<const uint16_t*>(p); };
+  // Attention of layer n with the owner's append (inside the attention launch
+  // when the layer reads every head it owns).  The schedule is planned again
+  // only when the number of KV heads read changes.
+  auto layer_attention = [&](int n, int& planned_key) -> mlkv_status {
+    mlkv_status st;
+    const int owned = map->own_count[n];
+    const int own0 = owned ? map->own_begin[n] * D : 0;
+    const bool fused_append = owned > 0 && map->own_begin[n] >= map->kv_begin[n] &&
+                              map->own_begin[n] + owned <= map->kv_begin[n] + map->kv_count[n];
+    if (owned > 0 && !fused_append &&
+        (st = append_impl(n, map, cache, bf(w.k16) + own0, bf(w.v16) + own0, kvD, ctx_lens,
+                          stream)) != MLKV_OK)
+      return st;
+    const int key = map->kv_count[n];
+    const int mode = key == planned_key ? 2 : 1;
+    if ((st = attention_impl(n, bf(w.q16), cache, map, ctx_lens, 1, bf(w.o16), MLKV_OUT_BF16,
+                             max_len_hint, base + w.attn, w.attn_bytes, stream, mode,
+                             fused_append ? bf(w.k16) : nullptr,
+                             fused_append ? bf(w.v16) : nullptr)) != MLKV_OK)
+      return st;
+    planned_key = key;
+    return MLKV_OK;
+  };
+  const bool fused = use_fused(model, B);
   int planned_key = -1;
   for (int n = 0; n < map->l; ++n) {
     const mlkv_layer_weights& lw = model->layers[n];
+    const int owned = map->own_count[n];
+    const int own0 = owned ? map->own_begin[n] * D : 0;
+    if (fused) {
+      mlkv::LayerInParams ip{};
+      ip.x = x;
+      ip.ln1_w = u16(lw.ln1_w);
+      ip.ln1_b = u16(lw.ln1_b);
+      ip.ln2_w = u16(lw.ln2_w);
+      ip.ln2_b = u16(lw.ln2_b);
+      ip.w = model->packed + model->in_off[n];
+      ip.b_q = u16(lw.b_q);
+      ip.b_k = u16(lw.b_k);
+      ip.b_v = u16(lw.b_v);
+      ip.b_fc1 = u16(lw.b_fc1);
+      ip.q16 = bf(w.q16);
+      ip.k16 = bf(w.k16);
+      ip.v16 = bf(w.v16);
+      ip.f16 = bf(w.f16);
+      ip.pos = ctx_lens;
+      ip.rows = B;
+      ip.d = d;
+      ip.h = h;
+      ip.owned = owned;
+      ip.ff = ff;
+      ip.kv_stride = kvD;
+      ip.kv_offset = own0;
+      ip.dims = model->dims;
+      ip.eps = model->eps;
+      std::memcpy(ip.inv_freq, model->inv_freq, sizeof ip.inv_freq);
+      if ((s = hip_ok(mlkv::launch_layer_in(ip, D, stream), "layer-in product")) != MLKV_OK)
+        return s;
+      if ((s = layer_attention(n, planned_key)) != MLKV_OK) return s;
+      const mlkv::LayerOutParams op{bf(w.o16), bf(w.f16), model->packed + model->out_off[n],
+                                    u16(lw.b_o), u16(lw.b_fc2), x, B, d, hD, ff};
+      if ((s = hip_ok(mlkv::launch_layer_out(op, stream), "layer-out product")) != MLKV_OK)
+        return s;
+      continue;
+    }
     mlkv::NormParams np{x, u16(lw.ln1_w), u16(lw.ln1_b), u16(lw.ln2_w), u16(lw.ln2_b),
                         bf(w.h1), bf(w.h2), B, d, model->eps};
     if ((s = hip_ok(mlkv::launch_norm2(np, stream), "layer norm")) != MLKV_OK) return s;
     if ((s = gemm(model->blas, B, hD, d, bf(w.h1), d, lw.w_q, f32(w.q32), hD)) != MLKV_OK)
       return s;
-    const int owned = map->own_count[n];
-    const int own0 = owned ? map->own_begin[n] * D : 0;
     if (owned) {
       if ((s = gemm(model->blas, B, owned * D, d, bf(w.h1), d, lw.w_k, f32(w.k32) + own0,
                     kvD)) != MLKV_OK ||
@@ -1122,21 +1246,7 @@ mlkv_status mlkv_model_decode_step(mlkv_model* model, float* x, const mlkv_cache
     std::memcpy(qp.inv_freq, model->inv_freq, sizeof qp.inv_freq);
     if ((s = hip_ok(mlkv::launch_qkv_epilogue(qp, stream), "q/k/v epilogue")) != MLKV_OK)
       return s;
-    // Attention with the owner's append (fused when the layer reads all it owns).
-    const bool fused_append = owned > 0 && map->own_begin[n] >= map->kv_begin[n] &&
-                              map->own_begin[n] + owned <= map->kv_begin[n] + map->kv_count[n];
-    if (owned > 0 && !fused_append &&
-        (s = append_impl(n, map, cache, bf(w.k16) + own0, bf(w.v16) + own0, kvD, ctx_lens,
-                         stream)) != MLKV_OK)
-      return s;
-    const int key = map->kv_count[n];
-    const int mode = key == planned_key ? 2 : 1;
-    if ((s = attention_impl(n, bf(w.q16), cache, map, ctx_lens, 1, bf(w.o16), MLKV_OUT_BF16,
-                            max_len_hint, base + w.attn, w.attn_bytes, stream, mode,
-                            fused_append ? bf(w.k16) : nullptr,
-                            fused_append ? bf(w.v16) : nullptr)) != MLKV_OK)
-      return s;
-    planned_key = key;
+    if ((s = layer_attention(n, planned_key)) != MLKV_OK) return s;
     if ((s = gemm(model->blas, B, d, hD, bf(w.o16), hD, lw.w_o, f32(w.a32), d)) != MLKV_OK ||
         (s = gemm(model->blas, B, ff, d, bf(w.h2), d, lw.w_fc1, f32(w.f32), ff)) != MLKV_OK)
       return s;

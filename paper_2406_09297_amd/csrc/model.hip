@@ -1,21 +1,32 @@
 // HIP kernels around attention in a GPT-NeoX decode step (the architecture of
-// the paper's Pythia models, Section 4.2), for CDNA4 (gfx950):
+// the paper's Pythia models, Section 4.2), for CDNA4 (gfx950).
 //
-//   norm2_kernel        both layer norms of the residual stream x (fp32) ->
-//                       h1, h2 (bf16); one workgroup per row
+// Fused path (batches up to kFusedMaxBatch rows; two launches around each
+// layer's attention):
+//   pack_kernel         once, at model creation: weights into MFMA A-operand
+//                       tiles (layout in kernels.h)
+//   layer_in_kernel     both layer norms of the residual stream x computed in
+//                       the prologue, then [q | k | v | fc1] = LN(x) W on the
+//                       matrix cores; epilogue: bias, rotary embedding at the
+//                       token's position, exact GELU for fc1, bf16 rounding
+//   layer_out_kernel    x += (o W_o + b_o) + (f W_2 + b_2) on the matrix cores
+//
+// Library path (larger batches): plain library GEMMs between
+//   norm2_kernel        both layer norms of x (fp32) -> h1, h2 (bf16)
 //   qkv_epilogue_kernel bias, rotary embedding at the token's position and
 //                       bf16 rounding of the query (every head) and the
 //                       owner's key; bias and rounding of the owner's value
 //   gelu_kernel         bias + exact GELU of the first MLP product, bf16
 //   residual_kernel     x += (o W_o + b_o) + (MLP out + b_2)
 //
-// The matrix products between them are plain library GEMMs (bf16 operands,
-// fp32 results); these kernels carry the elementwise work and the rounding
-// points.  Small, bandwidth-light passes over [batch][width] rows.
+// Both paths round at the same points: the layer-norm outputs, the rotated
+// q and k, v, the attention output and the GELU output are bf16; products
+// accumulate in fp32; the residual stream is fp32.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
 #include "kernels.h"
+#include "tile.h"
 
 namespace mlkv {
 namespace {
@@ -132,12 +143,238 @@ __global__ __launch_bounds__(kModelThreads) void residual_kernel(ResidualParams 
   }
 }
 
+// ---------------------------------------------------------------------------
+// Fused path.  B operand of every product: batch rows b0 .. b0+15 (lane l
+// supplies row b0 + l % 16, inputs 8 (l / 16) .. +7 of the k-block); rows at
+// or beyond `rows` supply zeros and their results are never stored.  Eight
+// waves split the k-blocks (wave w takes w, w + 8, ...) and their partial
+// tiles are summed in LDS in wave order, so a launch is deterministic.
+// ---------------------------------------------------------------------------
+constexpr int kFusedWaves = 8;
+constexpr int kFusedThreads = kFusedWaves * 64;
+
+__global__ __launch_bounds__(256) void pack_kernel(PackParams p) {
+  const int kbs = p.k_rows / 32;
+  const size_t chunks = static_cast<size_t>(p.nt_count) * kbs * 64;
+  for (size_t i = blockIdx.x * 256ull + threadIdx.x; i < chunks;
+       i += static_cast<size_t>(gridDim.x) * 256) {
+    const int lane = static_cast<int>(i % 64);
+    const size_t rest = i / 64;
+    const int kb = static_cast<int>(rest % kbs);
+    const int nt = static_cast<int>(rest / kbs);
+    const int n = nt * 16 + lane % 16;
+    const int k = kb * 32 + 8 * (lane / 16);
+    u16x8 v;
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+      v[j] = n < p.n_cols ? p.src[static_cast<size_t>(k + j) * p.n_cols + n] : uint16_t(0);
+    *reinterpret_cast<u16x8*>(
+        p.dst + (static_cast<size_t>(p.nt0 + nt) * p.kb_total + p.kb0 + kb) * kPackTile +
+        lane * 8) = v;
+  }
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
+  return v;
+}
+
+// Column block blk of the layer-in product: q head blk (blk < h), then the
+// owned key heads, the owned value heads and the fc1 blocks, each D wide.
+template <int D>
+__global__ __launch_bounds__(kFusedThreads) void layer_in_kernel(LayerInParams p) {
+  constexpr int NT = D / 16;
+  __shared__ f32x4 part[kFusedWaves][NT][64];
+  __shared__ float y[16][D + 1];
+  __shared__ float stats[16][2];
+  const int blk = blockIdx.x, b0 = blockIdx.y * 16;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const bool mlp = blk >= p.h + 2 * p.owned;
+  const uint16_t* lnw = mlp ? p.ln2_w : p.ln1_w;
+  const uint16_t* lnb = mlp ? p.ln2_b : p.ln1_b;
+  const int d = p.d;
+
+  // Layer-norm statistics of the tile's rows (wave w: rows w and w + 8).
+  for (int r = wave; r < 16; r += kFusedWaves) {
+    float mean = 0.f, rstd = 0.f;
+    if (b0 + r < p.rows) {
+      const float* xr = p.x + static_cast<size_t>(b0 + r) * d;
+      float s = 0.f;
+      for (int i = lane; i < d; i += 64) s += xr[i];
+      mean = wave_sum(s) / d;
+      float s2 = 0.f;
+      for (int i = lane; i < d; i += 64) {
+        const float c = xr[i] - mean;
+        s2 += c * c;
+      }
+      rstd = 1.f / sqrtf(wave_sum(s2) / d + p.eps);
+    }
+    if (lane == 0) {
+      stats[r][0] = mean;
+      stats[r][1] = rstd;
+    }
+  }
+  __syncthreads();
+
+  const int r = lane & 15, grp = lane >> 4;
+  const bool live = b0 + r < p.rows;
+  const float mean = stats[r][0], rstd = stats[r][1];
+  const float* xr = p.x + static_cast<size_t>(b0 + (live ? r : 0)) * d + 8 * grp;
+  const int KB = d / 32;
+  const uint16_t* wblk = p.w + static_cast<size_t>(blk) * NT * KB * kPackTile + lane * 8;
+  f32x4 acc[NT];
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll 2
+  for (int kb = wave; kb < KB; kb += kFusedWaves) {
+    u16x8 a[NT];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) a[nt] = load16(wblk + (static_cast<size_t>(nt) * KB + kb) * kPackTile);
+    // LN(x) for 8 consecutive inputs of row b0 + r, rounded to bf16.
+    u16x8 hb = {0, 0, 0, 0, 0, 0, 0, 0};
+    if (live) {
+      const int k = kb * 32;
+      const float4 x0 = *reinterpret_cast<const float4*>(xr + k);
+      const float4 x1 = *reinterpret_cast<const float4*>(xr + k + 4);
+      const u16x8 gw = load16(lnw + k + 8 * grp), gb = load16(lnb + k + 8 * grp);
+      const float xv[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const float z = (xv[j] - mean) * rstd;
+        hb[j] = f32_to_bf16_rne(z * bf16_to_f32(gw[j]) + bf16_to_f32(gb[j]));
+      }
+    }
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) acc[nt] = mfma_bf16(as_bf16(a[nt]), as_bf16(hb), acc[nt]);
+  }
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) part[wave][nt][lane] = acc[nt];
+  __syncthreads();
+  // Result lane l of tile nt: column b = l % 16, outputs 16 nt + 4 (l / 16) + i.
+  if (threadIdx.x < NT * 64) {
+    const int nt = threadIdx.x >> 6, l = threadIdx.x & 63;
+    f32x4 s = part[0][nt][l];
+#pragma unroll
+    for (int w = 1; w < kFusedWaves; ++w) s += part[w][nt][l];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) y[l & 15][nt * 16 + 4 * (l >> 4) + i] = s[i];
+  }
+  __syncthreads();
+
+  // Epilogue, in double as the library path's: bias, rotation (q and k),
+  // GELU (fc1), one rounding to bf16.
+  const int half = p.dims / 2;
+  const int role = blk < p.h ? 0 : blk < p.h + p.owned ? 1 : blk < p.h + 2 * p.owned ? 2 : 3;
+  for (int e = threadIdx.x; e < 16 * D; e += kFusedThreads) {
+    const int rr = e / D, c = e % D, b = b0 + rr;
+    if (b >= p.rows) continue;
+    const double u = y[rr][c];
+    if (role == 3) {
+      const int col = (blk - p.h - 2 * p.owned) * D + c;
+      if (col >= p.ff) continue;
+      const double z = u + static_cast<double>(bf16_to_f32(p.b_fc1[col]));
+      p.f16[static_cast<size_t>(b) * p.ff + col] =
+          f64_to_bf16_rne(0.5 * z * (1.0 + erf(z * 0.70710678118654752440)));
+      continue;
+    }
+    const int j = role == 0 ? blk : role == 1 ? blk - p.h : blk - p.h - p.owned;
+    const uint16_t* bias = role == 0 ? p.b_q : role == 1 ? p.b_k : p.b_v;
+    const double ub = u + static_cast<double>(bf16_to_f32(bias[j * D + c]));
+    uint16_t out;
+    if (role == 2 || c >= p.dims) {
+      out = f64_to_bf16_rne(ub);
+    } else {
+      const int partner = c < half ? c + half : c - half;
+      const double w =
+          static_cast<double>(y[rr][partner]) + static_cast<double>(bf16_to_f32(bias[j * D + partner]));
+      double sn, cs;
+      sincos(static_cast<double>(p.pos[b]) * p.inv_freq[c < half ? c : c - half], &sn, &cs);
+      out = f64_to_bf16_rne(c < half ? ub * cs - w * sn : ub * cs + w * sn);
+    }
+    if (role == 0)
+      p.q16[static_cast<size_t>(b) * p.h * D + j * D + c] = out;
+    else
+      (role == 1 ? p.k16 : p.v16)[static_cast<size_t>(b) * p.kv_stride + p.kv_offset + j * D + c] = out;
+  }
+}
+
+// Column block blk (16 outputs) of x += (o W_o + b_o) + (f W_2 + b_2); the two
+// products keep separate accumulators, as the library path's two GEMMs do.
+__global__ __launch_bounds__(kFusedThreads) void layer_out_kernel(LayerOutParams p) {
+  __shared__ f32x4 part[kFusedWaves][2][64];
+  const int blk = blockIdx.x, b0 = blockIdx.y * 16;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int r = lane & 15, grp = lane >> 4;
+  const bool live = b0 + r < p.rows;
+  const int KA = p.hD / 32, KM = p.ff / 32;
+  const uint16_t* wblk = p.w + static_cast<size_t>(blk) * (KA + KM) * kPackTile + lane * 8;
+  const uint16_t* orow = p.o16 + static_cast<size_t>(b0 + (live ? r : 0)) * p.hD + 8 * grp;
+  const uint16_t* frow = p.f16 + static_cast<size_t>(b0 + (live ? r : 0)) * p.ff + 8 * grp;
+  const u16x8 zero = {0, 0, 0, 0, 0, 0, 0, 0};
+  f32x4 acc_a = {0.f, 0.f, 0.f, 0.f}, acc_m = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 4
+  for (int kb = wave; kb < KA; kb += kFusedWaves) {
+    const u16x8 a = load16(wblk + static_cast<size_t>(kb) * kPackTile);
+    const u16x8 v = live ? load16(orow + kb * 32) : zero;
+    acc_a = mfma_bf16(as_bf16(a), as_bf16(v), acc_a);
+  }
+#pragma unroll 4
+  for (int kb = wave; kb < KM; kb += kFusedWaves) {
+    const u16x8 a = load16(wblk + static_cast<size_t>(KA + kb) * kPackTile);
+    const u16x8 v = live ? load16(frow + kb * 32) : zero;
+    acc_m = mfma_bf16(as_bf16(a), as_bf16(v), acc_m);
+  }
+  part[wave][0][lane] = acc_a;
+  part[wave][1][lane] = acc_m;
+  __syncthreads();
+  if (threadIdx.x < 64) {
+    const int l = threadIdx.x;
+    f32x4 sa = part[0][0][l], sm = part[0][1][l];
+#pragma unroll
+    for (int w = 1; w < kFusedWaves; ++w) {
+      sa += part[w][0][l];
+      sm += part[w][1][l];
+    }
+    const int b = b0 + (l & 15);
+    if (b < p.rows) {
+      float* xr = p.x + static_cast<size_t>(b) * p.d;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int n = blk * 16 + 4 * (l >> 4) + i;
+        xr[n] += (sa[i] + bf16_to_f32(p.b_o[n])) + (sm[i] + bf16_to_f32(p.b_2[n]));
+      }
+    }
+  }
+}
+
 unsigned grid_for(size_t n) {
   const size_t blocks = (n + kModelThreads - 1) / kModelThreads;
   return static_cast<unsigned>(blocks < 2048 ? (blocks > 0 ? blocks : 1) : 2048);
 }
 
 }  // namespace
+
+hipError_t launch_pack(const PackParams& p, hipStream_t stream) {
+  const size_t chunks = static_cast<size_t>(p.nt_count) * (p.k_rows / 32) * 64;
+  hipLaunchKernelGGL(pack_kernel, dim3(grid_for(chunks)), dim3(256), 0, stream, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_layer_in(const LayerInParams& p, int head_dim, hipStream_t stream) {
+  const dim3 grid(p.h + 2 * p.owned + (p.ff + head_dim - 1) / head_dim, (p.rows + 15) / 16);
+  if (head_dim == 64)
+    hipLaunchKernelGGL(layer_in_kernel<64>, grid, dim3(kFusedThreads), 0, stream, p);
+  else
+    hipLaunchKernelGGL(layer_in_kernel<128>, grid, dim3(kFusedThreads), 0, stream, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_layer_out(const LayerOutParams& p, hipStream_t stream) {
+  hipLaunchKernelGGL(layer_out_kernel, dim3(p.d / 16, (p.rows + 15) / 16), dim3(kFusedThreads), 0,
+                     stream, p);
+  return hipGetLastError();
+}
 
 hipError_t launch_norm2(const NormParams& p, hipStream_t stream) {
   hipLaunchKernelGGL(norm2_kernel, dim3(p.rows), dim3(kModelThreads), 0, stream, p);

@@ -1,7 +1,7 @@
 // Device helpers shared by the decode and prefill kernels (gfx950, wave64):
 // vector types, MFMA and conversion wrappers, and the wave-level tile
 // arithmetic of attention (one 32-token tile of keys/values against 16 query
-// columns).  Included by kernels.hip and prefill.hip only.
+// columns).  Included by kernels.hip, prefill.hip and model.hip only.
 #pragma once
 
 #include <hip/hip_runtime.h>

@@ -122,6 +122,28 @@ def test_model_step_head_dim_128_and_full_rotation():
     _run_case(2, 4, 128, 640, 2, 2, B=2, ctx=[31, 96], seed=93, rd=128, label="D128 rd128")
 
 
+def test_model_step_library_gemm_path(monkeypatch):
+    """The library-GEMM path (forced here; taken by itself above 64 rows or
+    when d_ff is not a multiple of 32) against the same oracle."""
+    monkeypatch.setenv("MLKV_MODEL_GEMM", "library")
+    _run_case(12, 12, 64, 3072, 4, 1, B=4, ctx=[0, 33, 100, 257], seed=91, label="library MLKV-4")
+    _run_case(2, 4, 128, 640, 2, 2, B=2, ctx=[31, 96], seed=93, rd=128, label="library D128")
+
+
+def test_model_step_batch_tiles_ragged():
+    """Fused path over two 16-row batch tiles, the second with 4 rows."""
+    ctx = [int(c) for c in np.random.default_rng(96).integers(0, 200, 20)]
+    _run_case(3, 4, 64, 256, 3, 2, B=20, ctx=ctx, seed=96, label="B20")
+
+
+def test_model_step_large_batch_and_ragged_ff_take_the_library_path():
+    """65 rows (above the fused path's 64) and d_ff = 400 (not a multiple of
+    32, so no packed weights): both run on library GEMMs."""
+    ctx = [int(c) for c in np.random.default_rng(97).integers(0, 90, 65)]
+    _run_case(2, 4, 64, 256, 2, 1, B=65, ctx=ctx, seed=97, label="B65")
+    _run_case(2, 4, 64, 400, 1, 1, B=3, ctx=[3, 40, 77], seed=98, label="ff400")
+
+
 def test_model_step_general_map_owner_not_reading_its_head():
     """Layer 0 owns KV heads 0 and 1 but reads only head 0 (its append runs
     separately); layer 1 reads head 1."""
