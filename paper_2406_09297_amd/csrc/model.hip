@@ -182,71 +182,139 @@ __device__ __forceinline__ float wave_sum(float v) {
 
 // Column block blk of the layer-in product: q head blk (blk < h), then the
 // owned key heads, the owned value heads and the fc1 blocks, each D wide.
+// Each wave takes its k-blocks in chunks of PRE and issues every load of a
+// chunk (weights, the x rows, the layer-norm scale and shift) before the
+// first product, so a chunk costs one memory round trip; the first chunk's
+// loads are in flight while the layer-norm statistics are taken.
 template <int D>
 __global__ __launch_bounds__(kFusedThreads) void layer_in_kernel(LayerInParams p) {
   constexpr int NT = D / 16;
+  constexpr int PRE = 16 / NT;  // k-blocks per chunk: 4 (D = 64) or 2 (D = 128)
   __shared__ f32x4 part[kFusedWaves][NT][64];
   __shared__ float y[16][D + 1];
   __shared__ float stats[16][2];
+  __shared__ double sc[16][kMaxRopePairs][2];
   const int blk = blockIdx.x, b0 = blockIdx.y * 16;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const bool mlp = blk >= p.h + 2 * p.owned;
   const uint16_t* lnw = mlp ? p.ln2_w : p.ln1_w;
   const uint16_t* lnb = mlp ? p.ln2_b : p.ln1_b;
-  const int d = p.d;
+  const int d = p.d, KB = d / 32;
+  const int r = lane & 15, grp = lane >> 4;
+  const bool live = b0 + r < p.rows;
+  const float* xr = p.x + static_cast<size_t>(b0 + (live ? r : 0)) * d + 8 * grp;
+  const uint16_t* wblk = p.w + static_cast<size_t>(blk) * NT * KB * kPackTile + lane * 8;
 
-  // Layer-norm statistics of the tile's rows (wave w: rows w and w + 8).
-  for (int r = wave; r < 16; r += kFusedWaves) {
-    float mean = 0.f, rstd = 0.f;
-    if (b0 + r < p.rows) {
-      const float* xr = p.x + static_cast<size_t>(b0 + r) * d;
-      float s = 0.f;
-      for (int i = lane; i < d; i += 64) s += xr[i];
-      mean = wave_sum(s) / d;
-      float s2 = 0.f;
-      for (int i = lane; i < d; i += 64) {
-        const float c = xr[i] - mean;
-        s2 += c * c;
+  u16x8 a[PRE][NT], gw[PRE], gb[PRE];
+  float4 x0[PRE], x1[PRE];
+  auto issue = [&](int base) {
+#pragma unroll
+    for (int i = 0; i < PRE; ++i) {
+      const int kb = base + i * kFusedWaves;
+      if (kb < KB) {
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt)
+          a[i][nt] = load16(wblk + (static_cast<size_t>(nt) * KB + kb) * kPackTile);
+        if (live) {
+          x0[i] = *reinterpret_cast<const float4*>(xr + kb * 32);
+          x1[i] = *reinterpret_cast<const float4*>(xr + kb * 32 + 4);
+          gw[i] = load16(lnw + kb * 32 + 8 * grp);
+          gb[i] = load16(lnb + kb * 32 + 8 * grp);
+        }
       }
-      rstd = 1.f / sqrtf(wave_sum(s2) / d + p.eps);
     }
-    if (lane == 0) {
-      stats[r][0] = mean;
-      stats[r][1] = rstd;
+  };
+  issue(wave);
+
+  // Rotation angles of the tile's rows (q and k blocks), in double, while the
+  // loads are in flight: sc[row][j] = (sin, cos) of pos[row] * inv_freq[j].
+  const int half = p.dims / 2;
+  const int role = blk < p.h ? 0 : blk < p.h + p.owned ? 1 : blk < p.h + 2 * p.owned ? 2 : 3;
+  if (role < 2) {
+    for (int e = threadIdx.x; e < 16 * half; e += kFusedThreads) {
+      const int row = e / half, jj = e % half;
+      if (b0 + row < p.rows)
+        sincos(static_cast<double>(p.pos[b0 + row]) * p.inv_freq[jj], &sc[row][jj][0],
+               &sc[row][jj][1]);
+    }
+  }
+
+  // Layer-norm statistics: 32 threads per row, each holding up to kStatRegs
+  // float4 of it, so the centred second pass reads registers (wider rows
+  // read the rest again, from cache).
+  {
+    constexpr int kStatRegs = 8;
+    const int row = threadIdx.x >> 5, j = threadIdx.x & 31;
+    float mean = 0.f, rstd = 0.f;
+    if (b0 + row < p.rows) {
+      const float* xs = p.x + static_cast<size_t>(b0 + row) * d;
+      float4 xv[kStatRegs];
+      float s = 0.f;
+#pragma unroll
+      for (int i = 0; i < kStatRegs; ++i) {
+        const int c = 4 * j + 128 * i;
+        xv[i] = c < d ? *reinterpret_cast<const float4*>(xs + c) : float4{0.f, 0.f, 0.f, 0.f};
+      }
+#pragma unroll
+      for (int i = 0; i < kStatRegs; ++i) s += (xv[i].x + xv[i].y) + (xv[i].z + xv[i].w);
+      for (int c = 4 * j + 128 * kStatRegs; c < d; c += 128) {
+        const float4 v = *reinterpret_cast<const float4*>(xs + c);
+        s += (v.x + v.y) + (v.z + v.w);
+      }
+#pragma unroll
+      for (int off = 16; off >= 1; off >>= 1) s += __shfl_xor(s, off);
+      mean = s / d;
+      float s2 = 0.f;
+#pragma unroll
+      for (int i = 0; i < kStatRegs; ++i) {
+        if (4 * j + 128 * i < d) {
+          const float c0 = xv[i].x - mean, c1 = xv[i].y - mean, c2 = xv[i].z - mean,
+                      c3 = xv[i].w - mean;
+          s2 += (c0 * c0 + c1 * c1) + (c2 * c2 + c3 * c3);
+        }
+      }
+      for (int c = 4 * j + 128 * kStatRegs; c < d; c += 128) {
+        const float4 v = *reinterpret_cast<const float4*>(xs + c);
+        const float c0 = v.x - mean, c1 = v.y - mean, c2 = v.z - mean, c3 = v.w - mean;
+        s2 += (c0 * c0 + c1 * c1) + (c2 * c2 + c3 * c3);
+      }
+#pragma unroll
+      for (int off = 16; off >= 1; off >>= 1) s2 += __shfl_xor(s2, off);
+      rstd = 1.f / sqrtf(s2 / d + p.eps);
+    }
+    if (j == 0) {
+      stats[row][0] = mean;
+      stats[row][1] = rstd;
     }
   }
   __syncthreads();
-
-  const int r = lane & 15, grp = lane >> 4;
-  const bool live = b0 + r < p.rows;
   const float mean = stats[r][0], rstd = stats[r][1];
-  const float* xr = p.x + static_cast<size_t>(b0 + (live ? r : 0)) * d + 8 * grp;
-  const int KB = d / 32;
-  const uint16_t* wblk = p.w + static_cast<size_t>(blk) * NT * KB * kPackTile + lane * 8;
+
   f32x4 acc[NT];
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll 2
-  for (int kb = wave; kb < KB; kb += kFusedWaves) {
-    u16x8 a[NT];
+  for (int base = wave;;) {
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) a[nt] = load16(wblk + (static_cast<size_t>(nt) * KB + kb) * kPackTile);
-    // LN(x) for 8 consecutive inputs of row b0 + r, rounded to bf16.
-    u16x8 hb = {0, 0, 0, 0, 0, 0, 0, 0};
-    if (live) {
-      const int k = kb * 32;
-      const float4 x0 = *reinterpret_cast<const float4*>(xr + k);
-      const float4 x1 = *reinterpret_cast<const float4*>(xr + k + 4);
-      const u16x8 gw = load16(lnw + k + 8 * grp), gb = load16(lnb + k + 8 * grp);
-      const float xv[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+    for (int i = 0; i < PRE; ++i) {
+      if (base + i * kFusedWaves < KB) {
+        // LN(x) for 8 consecutive inputs of row b0 + r, rounded to bf16.
+        u16x8 hb = {0, 0, 0, 0, 0, 0, 0, 0};
+        if (live) {
+          const float xv[8] = {x0[i].x, x0[i].y, x0[i].z, x0[i].w,
+                               x1[i].x, x1[i].y, x1[i].z, x1[i].w};
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const float z = (xv[j] - mean) * rstd;
-        hb[j] = f32_to_bf16_rne(z * bf16_to_f32(gw[j]) + bf16_to_f32(gb[j]));
+          for (int jj = 0; jj < 8; ++jj) {
+            const float z = (xv[jj] - mean) * rstd;
+            hb[jj] = f32_to_bf16_rne(z * bf16_to_f32(gw[i][jj]) + bf16_to_f32(gb[i][jj]));
+          }
+        }
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) acc[nt] = mfma_bf16(as_bf16(a[i][nt]), as_bf16(hb), acc[nt]);
       }
     }
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) acc[nt] = mfma_bf16(as_bf16(a[nt]), as_bf16(hb), acc[nt]);
+    base += PRE * kFusedWaves;
+    if (base >= KB) break;
+    issue(base);
   }
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) part[wave][nt][lane] = acc[nt];
@@ -264,8 +332,6 @@ __global__ __launch_bounds__(kFusedThreads) void layer_in_kernel(LayerInParams p
 
   // Epilogue, in double as the library path's: bias, rotation (q and k),
   // GELU (fc1), one rounding to bf16.
-  const int half = p.dims / 2;
-  const int role = blk < p.h ? 0 : blk < p.h + p.owned ? 1 : blk < p.h + 2 * p.owned ? 2 : 3;
   for (int e = threadIdx.x; e < 16 * D; e += kFusedThreads) {
     const int rr = e / D, c = e % D, b = b0 + rr;
     if (b >= p.rows) continue;
@@ -288,8 +354,8 @@ __global__ __launch_bounds__(kFusedThreads) void layer_in_kernel(LayerInParams p
       const int partner = c < half ? c + half : c - half;
       const double w =
           static_cast<double>(y[rr][partner]) + static_cast<double>(bf16_to_f32(bias[j * D + partner]));
-      double sn, cs;
-      sincos(static_cast<double>(p.pos[b]) * p.inv_freq[c < half ? c : c - half], &sn, &cs);
+      const int jj = c < half ? c : c - half;
+      const double sn = sc[rr][jj][0], cs = sc[rr][jj][1];
       out = f64_to_bf16_rne(c < half ? ub * cs - w * sn : ub * cs + w * sn);
     }
     if (role == 0)
@@ -301,29 +367,40 @@ __global__ __launch_bounds__(kFusedThreads) void layer_in_kernel(LayerInParams p
 
 // Column block blk (16 outputs) of x += (o W_o + b_o) + (f W_2 + b_2); the two
 // products keep separate accumulators, as the library path's two GEMMs do.
+// K-blocks 0 .. KA-1 are W_o's (input o), KA .. KA+KM-1 W_2's (input f); each
+// wave takes every eighth one, in chunks of PRE whose loads are all issued
+// before the chunk's products.
 __global__ __launch_bounds__(kFusedThreads) void layer_out_kernel(LayerOutParams p) {
+  constexpr int PRE = 16;
   __shared__ f32x4 part[kFusedWaves][2][64];
   const int blk = blockIdx.x, b0 = blockIdx.y * 16;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int r = lane & 15, grp = lane >> 4;
   const bool live = b0 + r < p.rows;
-  const int KA = p.hD / 32, KM = p.ff / 32;
-  const uint16_t* wblk = p.w + static_cast<size_t>(blk) * (KA + KM) * kPackTile + lane * 8;
+  const int KA = p.hD / 32, KM = p.ff / 32, KT = KA + KM;
+  const uint16_t* wblk = p.w + static_cast<size_t>(blk) * KT * kPackTile + lane * 8;
   const uint16_t* orow = p.o16 + static_cast<size_t>(b0 + (live ? r : 0)) * p.hD + 8 * grp;
   const uint16_t* frow = p.f16 + static_cast<size_t>(b0 + (live ? r : 0)) * p.ff + 8 * grp;
   const u16x8 zero = {0, 0, 0, 0, 0, 0, 0, 0};
   f32x4 acc_a = {0.f, 0.f, 0.f, 0.f}, acc_m = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll 4
-  for (int kb = wave; kb < KA; kb += kFusedWaves) {
-    const u16x8 a = load16(wblk + static_cast<size_t>(kb) * kPackTile);
-    const u16x8 v = live ? load16(orow + kb * 32) : zero;
-    acc_a = mfma_bf16(as_bf16(a), as_bf16(v), acc_a);
-  }
-#pragma unroll 4
-  for (int kb = wave; kb < KM; kb += kFusedWaves) {
-    const u16x8 a = load16(wblk + static_cast<size_t>(KA + kb) * kPackTile);
-    const u16x8 v = live ? load16(frow + kb * 32) : zero;
-    acc_m = mfma_bf16(as_bf16(a), as_bf16(v), acc_m);
+  for (int base = wave; base < KT; base += PRE * kFusedWaves) {
+    u16x8 a[PRE], v[PRE];
+#pragma unroll
+    for (int i = 0; i < PRE; ++i) {
+      const int kb = base + i * kFusedWaves;
+      if (kb < KT) {
+        a[i] = load16(wblk + static_cast<size_t>(kb) * kPackTile);
+        v[i] = !live ? zero : kb < KA ? load16(orow + kb * 32) : load16(frow + (kb - KA) * 32);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < PRE; ++i) {
+      const int kb = base + i * kFusedWaves;
+      if (kb < KA)
+        acc_a = mfma_bf16(as_bf16(a[i]), as_bf16(v[i]), acc_a);
+      else if (kb < KT)
+        acc_m = mfma_bf16(as_bf16(a[i]), as_bf16(v[i]), acc_m);
+    }
   }
   part[wave][0][lane] = acc_a;
   part[wave][1][lane] = acc_m;
