@@ -300,16 +300,23 @@ mlkv_status mlkv_prefill_step(const void* q_all, const void* k_new_all, const vo
  *   ctx_lens[b] + 1 positions of its KV head (as mlkv_decode_step)
  *   x += (o W_o + b_o) + (GELU(h2 W_1 + b_1) W_2 + b_2)  (exact GELU; the
  *   parallel residual)
- * The matrix products are library GEMMs (rocBLAS; bf16 operands, fp32
- * results); layer norms, bias, rotation, GELU and residual run in the
- * library's kernels.  Stored in bf16: h1, h2, the rotated q and k, v, the
+ * Matrix products take bf16 operands and accumulate in fp32.  Up to 64
+ * sequences (and d_ff a multiple of 32) they run in two fused kernels per
+ * layer around the attention: layer norms, the q/k/v and fc1 products, bias,
+ * rotation and GELU in one; the output and fc2 products, biases and the
+ * residual in the other (weights packed at creation into the matrix cores'
+ * operand tiles).  Otherwise the products are library GEMMs (rocBLAS)
+ * between the library's layer-norm, epilogue and residual kernels; the
+ * environment variable MLKV_MODEL_GEMM=library selects that path for any
+ * batch.  Either way stored in bf16: h1, h2, the rotated q and k, v, the
  * attention output and the GELU output (nearest, ties to even); x stays fp32.
  */
 typedef struct mlkv_model mlkv_model; /* opaque, owned by the library */
 
 /* Device pointers of one layer's weights, bf16, matrices row-major [in][out].
- * The library keeps the pointers (not copies); the caller keeps the memory
- * alive and unchanged while the model exists. */
+ * mlkv_model_create copies the matrices into packed tiles (the fused path)
+ * and keeps the pointers for the library-GEMM path and the vectors: the
+ * caller keeps the memory alive and unchanged while the model exists. */
 typedef struct {
   const void* ln1_w; const void* ln1_b;   /* [d_model] */
   const void* ln2_w; const void* ln2_b;   /* [d_model] */
@@ -324,8 +331,10 @@ typedef struct {
 /* d_model must equal h * head_dim (head_dim 64 or 128); rotary_dims even, in
  * [0, head_dim]; rotary_base > 0; ln_eps >= 0; layers[l] with the key/value
  * pointers set exactly in the layers that own KV heads.  Creates the GEMM
- * library handle (allocates).  Errors: MLKV_ERR_INVALID_ARG,
- * MLKV_ERR_UNSUPPORTED, MLKV_ERR_HIP. */
+ * library handle and, when d_ff % 32 == 0, allocates device memory for the
+ * packed matrices (2 bytes per weight, every layer) and fills it on the null
+ * stream, finished before returning.  mlkv_model_destroy frees both.
+ * Errors: MLKV_ERR_INVALID_ARG, MLKV_ERR_UNSUPPORTED, MLKV_ERR_HIP. */
 mlkv_status mlkv_model_create(const mlkv_map* map, int d_model, int d_ff, int head_dim,
                               int rotary_dims, double rotary_base, double ln_eps,
                               const mlkv_layer_weights* layers, mlkv_model** out);
