@@ -301,11 +301,11 @@ mlkv_status mlkv_prefill_step(const void* q_all, const void* k_new_all, const vo
  *   x += (o W_o + b_o) + (GELU(h2 W_1 + b_1) W_2 + b_2)  (exact GELU; the
  *   parallel residual)
  * Matrix products take bf16 operands and accumulate in fp32.  Up to 64
- * sequences (and d_ff a multiple of 32) they run in two fused kernels per
- * layer around the attention: layer norms, the q/k/v and fc1 products, bias,
- * rotation and GELU in one; the output and fc2 products, biases and the
- * residual in the other (weights packed at creation into the matrix cores'
- * operand tiles).  Otherwise the products are library GEMMs (rocBLAS)
+ * sequences, when the model holds packed weights (mlkv_model_create), they
+ * run in two fused kernels per layer around the attention: layer norms, the
+ * q/k/v and fc1 products, bias, rotation and GELU in one; the output and fc2
+ * products, biases and the residual in the other (weights packed into the
+ * matrix cores' operand tiles).  Otherwise the products are library GEMMs (rocBLAS)
  * between the library's layer-norm, epilogue and residual kernels; the
  * environment variable MLKV_MODEL_GEMM=library selects that path for any
  * batch.  Either way stored in bf16: h1, h2, the rotated q and k, v, the
@@ -331,9 +331,11 @@ typedef struct {
 /* d_model must equal h * head_dim (head_dim 64 or 128); rotary_dims even, in
  * [0, head_dim]; rotary_base > 0; ln_eps >= 0; layers[l] with the key/value
  * pointers set exactly in the layers that own KV heads.  Creates the GEMM
- * library handle and, when d_ff % 32 == 0, allocates device memory for the
- * packed matrices (2 bytes per weight, every layer) and fills it on the null
- * stream, finished before returning.  mlkv_model_destroy frees both.
+ * library handle and, when d_ff % 32 == 0 and the layer-norm vectors are
+ * 16-byte aligned, allocates device memory for the packed matrices (2 bytes
+ * per weight, every layer) and fills it after synchronizing the device (so
+ * the caller's writes of the weights on any stream are complete), finished
+ * before returning.  mlkv_model_destroy frees both.
  * Errors: MLKV_ERR_INVALID_ARG, MLKV_ERR_UNSUPPORTED, MLKV_ERR_HIP. */
 mlkv_status mlkv_model_create(const mlkv_map* map, int d_model, int d_ff, int head_dim,
                               int rotary_dims, double rotary_base, double ln_eps,
@@ -357,6 +359,11 @@ mlkv_status mlkv_model_decode_step(mlkv_model* model, float* x, const mlkv_cache
 /* ----------------------------------------------------------------------- */
 /* Introspection (tests and benchmarks)                                      */
 /* ----------------------------------------------------------------------- */
+
+/* 1 when mlkv_model_decode_step runs `batch` sequences on the fused kernels
+ * (packed weights, batch <= 64, MLKV_MODEL_GEMM not "library"), 0 when on
+ * library GEMMs or for invalid arguments. */
+int mlkv_model_fused_path(const mlkv_model* model, int batch);
 
 /* Work plan mlkv_decode_attention uses for `layer` at this max length: the
  * 32-token tiles of all (sequence, KV head) pairs form one flat list shared

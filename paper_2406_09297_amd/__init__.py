@@ -42,6 +42,7 @@ EXPORTS = [
     "mlkv_decode_step_rope",
     "mlkv_cache_append_rows", "mlkv_prefill_attention", "mlkv_prefill_step",
     "mlkv_model_create", "mlkv_model_destroy", "mlkv_model_workspace_bytes",
+    "mlkv_model_fused_path",
     "mlkv_model_decode_step",
 ]
 
@@ -97,6 +98,7 @@ def lib():
             "mlkv_model_create": ([P, I, I, I, I, ctypes.c_double, ctypes.c_double, P, P], S),
             "mlkv_model_destroy": ([P], None),
             "mlkv_model_workspace_bytes": ([P, I, I], Z),
+            "mlkv_model_fused_path": ([P, I], I),
             "mlkv_model_decode_step": ([P, P, P, P, I, P, Z, P], S),
             "mlkv_plan": ([P, I, I, I, I, I, ctypes.POINTER(I), ctypes.POINTER(I)], S),
             "mlkv_workspace_init": ([P, Z, P], S),
@@ -417,6 +419,10 @@ class Model:
         if getattr(self, "_h", None) and self._h.value and _lib is not None:
             _lib.mlkv_model_destroy(self._h)
             self._h = ctypes.c_void_p()
+
+    def fused_path(self, batch: int) -> bool:
+        """mlkv_model_fused_path: whether `batch` sequences run on the fused kernels."""
+        return bool(lib().mlkv_model_fused_path(self._h, batch))
 
     def workspace(self, batch: int, capacity: int, device="cuda", stream=None) -> torch.Tensor:
         n = lib().mlkv_model_workspace_bytes(self._h, batch, capacity)

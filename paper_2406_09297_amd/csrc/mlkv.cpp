@@ -994,8 +994,11 @@ mlkv_status hip_ok(hipError_t e, const char* what) {
 }
 
 // Copies every layer's matrices into the fused path's MFMA tiles (one device
-// allocation; the null stream, finished before returning).
+// allocation; after all work already queued on the device, on the null
+// stream, finished before returning).
 mlkv_status pack_weights(mlkv_model* m) {
+  const hipError_t e0 = hipDeviceSynchronize();  // the caller's writes of the weights
+  if (e0 != hipSuccess) return fail(MLKV_ERR_HIP, "weight packing: %s", hipGetErrorString(e0));
   const mlkv_map* map = m->map;
   const int D = m->D, NT = D / 16, d = m->d, ff = m->d_ff, h = map->h, hD = h * D;
   const int KB = d / 32, ff_blocks = (ff + D - 1) / D;
@@ -1094,7 +1097,12 @@ mlkv_status mlkv_model_create(const mlkv_map* map, int d_model, int d_ff, int he
     delete m;
     return fail(MLKV_ERR_HIP, "rocblas_create_handle failed");
   }
-  if (d_ff % 32 == 0 && (s = pack_weights(m)) != MLKV_OK) {
+  // The fused path reads the layer-norm vectors 16 bytes at a time.
+  bool ln_aligned = true;
+  for (const mlkv_layer_weights& w : m->layers)
+    ln_aligned = ln_aligned && aligned16(w.ln1_w) && aligned16(w.ln1_b) && aligned16(w.ln2_w) &&
+                 aligned16(w.ln2_b);
+  if (d_ff % 32 == 0 && ln_aligned && (s = pack_weights(m)) != MLKV_OK) {
     mlkv_model_destroy(m);
     return s;
   }
@@ -1107,6 +1115,10 @@ void mlkv_model_destroy(mlkv_model* model) {
   if (model->blas) (void)rocblas_destroy_handle(model->blas);
   if (model->packed) (void)hipFree(model->packed);
   delete model;
+}
+
+int mlkv_model_fused_path(const mlkv_model* model, int batch) {
+  return model && batch > 0 && use_fused(model, batch) ? 1 : 0;
 }
 
 size_t mlkv_model_workspace_bytes(const mlkv_model* model, int batch, int capacity) {

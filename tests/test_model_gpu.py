@@ -41,7 +41,15 @@ def _gpu():
     yield
 
 
-def _run_case(l, h, D, d_ff, m, g, B, ctx, seed, rd=16, kv_of=None, owner_of=None, label=""):
+def _offset_view(t):
+    """The same values at a 2-byte offset (not 16-byte aligned)."""
+    buf = torch.empty(t.numel() + 1, dtype=t.dtype, device=t.device)
+    buf[1:].copy_(t.reshape(-1))
+    return buf[1:].view(t.shape)
+
+
+def _run_case(l, h, D, d_ff, m, g, B, ctx, seed, rd=16, kv_of=None, owner_of=None, label="",
+              misalign_ln=False, fused=True):
     ctx = np.asarray(ctx, dtype=np.int32)
     if kv_of is None:
         kv_of, owner_of = oracle.map_uniform(l, h, m, g)
@@ -53,8 +61,13 @@ def _run_case(l, h, D, d_ff, m, g, B, ctx, seed, rd=16, kv_of=None, owner_of=Non
     weights = synth.model_weights(seed, l, h, D, d_ff, owned)
     dev = [{k: (None if v is None else mlkv.bf16_tensor(v, "cuda")) for k, v in lw.items()}
            for lw in weights]
+    if misalign_ln:
+        for lw in dev:
+            for k in ("ln1_w", "ln1_b", "ln2_w", "ln2_b"):
+                lw[k] = _offset_view(lw[k])
     d = h * D
     model = mlkv.Model(mp, d, d_ff, D, dev, rotary_dims=rd)
+    assert model.fused_path(B) == fused, f"{label}: fused path expected {fused}"
     S = (int(ctx.max()) + 1 + 63) // 64 * 64
     lens = np.tile(ctx, n_kv)
     kc = synth.rows_bf16(seed, 1, n_kv * B, S, D, lens, fill=synth.BF16_NAN).reshape(n_kv, B, S, D)
@@ -126,8 +139,10 @@ def test_model_step_library_gemm_path(monkeypatch):
     """The library-GEMM path (forced here; taken by itself above 64 rows or
     when d_ff is not a multiple of 32) against the same oracle."""
     monkeypatch.setenv("MLKV_MODEL_GEMM", "library")
-    _run_case(12, 12, 64, 3072, 4, 1, B=4, ctx=[0, 33, 100, 257], seed=91, label="library MLKV-4")
-    _run_case(2, 4, 128, 640, 2, 2, B=2, ctx=[31, 96], seed=93, rd=128, label="library D128")
+    _run_case(12, 12, 64, 3072, 4, 1, B=4, ctx=[0, 33, 100, 257], seed=91, label="library MLKV-4",
+              fused=False)
+    _run_case(2, 4, 128, 640, 2, 2, B=2, ctx=[31, 96], seed=93, rd=128, label="library D128",
+              fused=False)
 
 
 def test_model_step_batch_tiles_ragged():
@@ -140,8 +155,16 @@ def test_model_step_large_batch_and_ragged_ff_take_the_library_path():
     """65 rows (above the fused path's 64) and d_ff = 400 (not a multiple of
     32, so no packed weights): both run on library GEMMs."""
     ctx = [int(c) for c in np.random.default_rng(97).integers(0, 90, 65)]
-    _run_case(2, 4, 64, 256, 2, 1, B=65, ctx=ctx, seed=97, label="B65")
-    _run_case(2, 4, 64, 400, 1, 1, B=3, ctx=[3, 40, 77], seed=98, label="ff400")
+    _run_case(2, 4, 64, 256, 2, 1, B=65, ctx=ctx, seed=97, label="B65", fused=False)
+    _run_case(2, 4, 64, 400, 1, 1, B=3, ctx=[3, 40, 77], seed=98, label="ff400", fused=False)
+
+
+def test_model_step_unaligned_layer_norm_vectors_take_the_library_path():
+    """The fused kernels read the layer-norm vectors 16 bytes at a time; a
+    model whose vectors are not 16-byte aligned keeps no packed weights and
+    runs on library GEMMs."""
+    _run_case(2, 4, 64, 256, 2, 1, B=3, ctx=[3, 40, 77], seed=99, label="unaligned ln",
+              misalign_ln=True, fused=False)
 
 
 def test_model_step_general_map_owner_not_reading_its_head():
