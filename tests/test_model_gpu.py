@@ -135,6 +135,12 @@ def test_model_step_head_dim_128_and_full_rotation():
     _run_case(2, 4, 128, 640, 2, 2, B=2, ctx=[31, 96], seed=93, rd=128, label="D128 rd128")
 
 
+def test_model_step_full_size_benchmark_configuration():
+    """The whole-model benchmark's configuration: Pythia-160M shapes, MLKV-4,
+    batch 8, 2000 cached tokens per sequence (capacity 2048)."""
+    _run_case(12, 12, 64, 3072, 4, 1, B=8, ctx=[2000] * 8, seed=90, label="model_b8 full size")
+
+
 def test_model_step_library_gemm_path(monkeypatch):
     """The library-GEMM path (forced here; taken by itself above 64 rows or
     when d_ff is not a multiple of 32) against the same oracle."""
