@@ -119,12 +119,16 @@ def test_prefill_long_prompt_empty_cache():
     _check_case(PrefillCase(w), "prefill T=300")
 
 
-def test_prefill_peaked_scores():
-    """Keys x3 before rounding (peaked softmax, as in the long decode case)."""
-    w = synth.Workload("prefill_peaked", l=2, h=12, m=2, g=1, D=64, B=2, ctx=64, T=80,
-                       k_scale=3.0, seed=84)
-    say("prefill peaked")
-    _check_case(PrefillCase(w), "prefill peaked")
+@pytest.mark.parametrize("ctx,T,D,seed", [(64, 80, 64, 84), (0, 160, 64, 85), (100, 300, 64, 86),
+                                          (31, 33, 64, 87), (64, 80, 128, 88), (500, 257, 64, 89)])
+def test_prefill_peaked_scores(ctx, T, D, seed):
+    """Keys x3 before rounding (peaked softmax, as in the long decode case),
+    over prompt lengths and contexts that put the causal edge at different
+    tile and block offsets."""
+    w = synth.Workload("prefill_peaked", l=2, h=12, m=2, g=1, D=D, B=2, ctx=ctx, T=T,
+                       k_scale=3.0, seed=seed)
+    say(f"prefill peaked ctx={ctx} T={T} D={D}")
+    _check_case(PrefillCase(w), f"prefill peaked ctx={ctx} T={T} D={D}")
 
 
 def test_prefill_general_map_owner_not_reading_its_head():
