@@ -43,24 +43,31 @@ KERNEL_SOURCES = [os.path.join(ROOT, "paper_2406_09297_amd", "csrc", f)
                   for f in ("kernels.hip", "tile.h")]
 
 
-def kernel_source_sha256() -> str:
-    """SHA-256 over the decode kernels' sources (kernels.hip then tile.h)."""
+def kernel_code_sha256() -> str:
+    """SHA-256 over the decode kernels' code (kernels.hip then tile.h) with
+    comments removed and whitespace collapsed, so that editing a comment does
+    not void a counter record taken from the same code."""
     import hashlib
+    import re
 
     h = hashlib.sha256()
     for f in KERNEL_SOURCES:
-        with open(f, "rb") as fh:
-            h.update(fh.read())
+        with open(f) as fh:
+            text = fh.read()
+        text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", " ", text)
+        h.update(re.sub(r"\s+", " ", text).strip().encode())
     return h.hexdigest()
 
 
 def measured_traffic(workload: str):
-    """HBM bytes per attention launch from the committed rocprofv3 counter
-    summary, or None if it does not cover this workload or the kernel source
+    """HBM bytes per timed attention launch (the attention kernel plus, where
+    one follows it, the merge kernel) from the committed rocprofv3 counter
+    summary, or None if it does not cover this workload or the kernels' code
     changed since the counters were taken."""
     try:
         text = open(TRAFFIC_FILE).read()
-        sha = kernel_source_sha256()
+        sha = kernel_code_sha256()
     except OSError:
         return None
     fields = {}
@@ -69,7 +76,7 @@ def measured_traffic(workload: str):
         if "=" in line and not line.startswith("#"):
             k, v = line.split("=", 1)
             fields[k.strip()] = v.strip()
-    if fields.get("kernel_source_sha256") != sha:
+    if fields.get("kernel_code_sha256") != sha:
         return None
     v = fields.get(f"traffic_bytes_per_launch[{workload}]")
     return int(v) if v else None
@@ -274,14 +281,12 @@ def run_model(args, w):
     """Whole-model decode step (mlkv_model_decode_step): tokens/s at batch B."""
     import torch
     import synth
-    import oracle
     import paper_2406_09297_amd as mlkv
 
     dev = "cuda:0"
     log(f"[bench] model workload {w.name}: generating weights and cache")
     mp = mlkv.Map.uniform(w.l, w.h, w.m, w.g)
-    kv_of, owner_of = oracle.map_uniform(w.l, w.h, w.m, w.g)
-    owned = [int((owner_of == n).sum()) for n in range(w.l)]
+    owned = [mp.layer_owned(n)[1] for n in range(w.l)]
     weights = synth.model_weights(w.seed, w.l, w.h, w.D, w.d_ff, owned)
     dev_w = [{k: (None if v is None else mlkv.bf16_tensor(v, dev)) for k, v in lw.items()}
              for lw in weights]
@@ -379,7 +384,10 @@ def run_model(args, w):
     }
     if not args.no_cpu_baseline:
         log("[bench] cpu baseline (oracle)")
+        import oracle
         import oracle.model as om
+
+        kv_of, owner_of = oracle.map_uniform(w.l, w.h, w.m, w.g)
 
         kc, vc = om._f64(inp["k_cache"]), om._f64(inp["v_cache"])
         threads = int(os.environ.get("OMP_NUM_THREADS", len(os.sched_getaffinity(0))))
@@ -442,7 +450,6 @@ def run_capacity(args, w):
     timed at that batch."""
     import torch
     import synth
-    import oracle
     import paper_2406_09297_amd as mlkv
 
     dev = "cuda:0"
@@ -528,6 +535,8 @@ def run_capacity(args, w):
             mlkv.bf16_bits(cache.v.index_select(1, sel)).reshape(w.n_kv, 4, S // 32, w.D, 32)
             .transpose(0, 1, 2, 4, 3)).reshape(w.n_kv, 4, S, w.D)
         ctx_h = np.full(4, w.ctx, dtype=np.int32)
+        import oracle
+
         kv_of, owner_of = oracle.map_uniform(w.l, w.h, w.m, w.g)
         threads = int(os.environ.get("OMP_NUM_THREADS", len(os.sched_getaffinity(0))))
         runs, spent = 0, 0.0
@@ -593,8 +602,8 @@ def main():
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--map", default=None,
                     help="m,g of a map-sweep workload (default: its last point)")
-    ap.add_argument("--no-cold", action="store_true",
-                    help="skip timing attention launches after a 1 GiB read evicts the caches")
+    ap.add_argument("--long-context", default="mlkv4_b8_long",
+                    help="second decode workload reported in the same line ('none' to skip)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--rotary-dims", type=int, default=0,
                     help="rotate the newest token's queries and keys inside the step "
@@ -644,6 +653,32 @@ def main():
     elif w.sweep:
         m, g = w.sweep[-1]
         w = w.with_map(m, g)
+    result = measure_decode(args, w, dev, headline=True)
+    if result is None:  # counter pass
+        return
+    extra = args.long_context
+    if extra and extra != "none" and extra != w.name and not args.map:
+        wl = synth.get_workload(extra)
+        sub = measure_decode(args, wl, dev, headline=False)
+        result["long_context"] = sub
+    print(json.dumps(result), flush=True)
+
+
+def flush_caches(flush, sink):
+    """Evict the 256 MB Infinity Cache: a 1 GiB read (clean lines, no
+    write-back) through a plain reduction on the current stream."""
+    sink += flush.sum()
+
+
+def measure_decode(args, w, dev, headline: bool):
+    """The decode step of workload w: timed cold-start steps (value), warm
+    back-to-back steps, and the attention launches (with their merge kernel
+    when one follows) timed per launch by the library's event pairs, cold and
+    in the warm step order.  Returns the JSON object (None for a counter pass)."""
+    import torch
+    import synth
+    import paper_2406_09297_amd as mlkv
+
     log(f"[bench] workload {w.name}: generating inputs")
     inp = synth.step_inputs(w, fill=0)
     S = inp["capacity"]
@@ -657,7 +692,8 @@ def main():
     vn = mlkv.bf16_tensor(inp["v_new"], dev)
     ctx = torch.from_numpy(inp["ctx"]).to(dev)
     out = torch.empty((w.l, w.B, w.h, w.D), dtype=torch.float32, device=dev)
-    ws = mlkv.workspace(mp, w.B, S, w.D, dev)
+    ws = mlkv.workspace(mp, w.B, S, w.D, dev, rotary_dims=args.rotary_dims)
+    ws_attn = mlkv.workspace(mp, w.B, S, w.D, dev)  # for single-layer calls
     max_len = int(inp["ctx"].max()) + 1
     stream = torch.cuda.current_stream()
 
@@ -666,6 +702,7 @@ def main():
     per_layer = step_bytes(w, inp["ctx"], kv_count, owned)
     step_total = sum(sum(x.values()) for x in per_layer)
     kv_total = sum(x["kv"] for x in per_layer)
+    attn_bytes = float(np.mean([x["kv"] + x["q"] + x["out"] for x in per_layer]))
 
     def one_step():
         mlkv.decode_step(q, kn, vn, cache, mp, ctx, out, max_len_hint=max_len, ws=ws,
@@ -685,13 +722,38 @@ def main():
             one_step()
         torch.cuda.synchronize()
         log("[bench] pmc pass done")
-        return
+        return None
 
     log(f"[bench] warmup {args.warmup}")
     for _ in range(args.warmup):
         one_step()
     torch.cuda.synchronize()
-    log(f"[bench] timing {args.steps} steps")
+
+    flush = torch.ones(1 << 28, dtype=torch.float32, device=dev)
+    sink = torch.zeros((), device=dev)
+
+    # (1) Cold-start steps (value): the Infinity Cache is flushed before each
+    # step, so every step starts with its inputs in HBM only; inside a step
+    # the layers sharing a KV head meet it where the previous layer left it,
+    # as they would in a model.  An event pair per step; the flushes are
+    # outside the pairs.  The host enqueues all of it behind a GPU sleep.
+    log(f"[bench] timing {args.steps} cold-start steps")
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    torch.cuda._sleep(SLEEP_CYCLES)
+    for e0, e1 in evs:
+        flush_caches(flush, sink)
+        e0.record(stream)
+        one_step()
+        e1.record(stream)
+    torch.cuda.synchronize()
+    step_ms = np.array([e0.elapsed_time(e1) for e0, e1 in evs])
+    ms_step = float(step_ms.mean())
+
+    # (2) Warm back-to-back steps: the whole cache of this workload may stay
+    # in the Infinity Cache between steps (effective bandwidth, not HBM).
+    log(f"[bench] timing {args.steps} warm back-to-back steps")
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     e0.record(stream)
@@ -699,77 +761,95 @@ def main():
         one_step()
     e1.record(stream)
     torch.cuda.synchronize()
-    ms_step = e0.elapsed_time(e1) / args.steps
+    ms_warm = e0.elapsed_time(e1) / args.steps
 
-    # Per-launch duration of the dominant kernel (split-K attention), from HIP
-    # event pairs the library records on the launch stream around each
-    # attention kernel, over a second timed region of the same steps.
-    # The host enqueues each chunk of steps while a sleep kernel holds the
-    # GPU, so the GPU runs the chunk back to back and no event interval
-    # contains host launch latency.
-    log("[bench] timing attention kernels (event pairs)")
+    # (3) Per launch, cold: a flush before every layer's attention
+    # (mlkv_decode_attention; the pair brackets the merge kernel too when
+    # one follows).  This is the roofline's figure.
+    log("[bench] cold attention launches")
+    lens_attn = (ctx + 1).to(torch.int32)
+    out_l = torch.empty((w.B, w.h, w.D), dtype=torch.float32, device=dev)
+    reps = max(3 * w.l, min(args.steps, 10 * w.l))
+    mlkv.profile_enable(reps)
+    for i in range(reps):
+        n = i % w.l
+        flush_caches(flush, sink)
+        mlkv.decode_attention(n, q[n], cache, mp, lens_attn, out_l, max_len_hint=max_len,
+                              ws=ws_attn)
+    torch.cuda.synchronize()
+    c_n, _, c_min, c_max = mlkv.profile_read()
+    c_dur = mlkv.profile_durations(c_n)
+    mlkv.profile_disable()
+    del flush
+    torch.cuda.empty_cache()
+    c_avg = float(c_dur.mean()) * 1e-3
+    achieved = attn_bytes / c_avg / 1e9
+
+    # (4) Per launch, warm: the library's pairs around each layer's attention
+    # inside back-to-back steps (chunks of ten steps enqueued behind a GPU
+    # sleep, so no interval holds host launch latency).
+    log("[bench] warm attention launches (event pairs)")
     mlkv.profile_enable(args.steps * w.l)
     torch.cuda.synchronize()
-    chunk = 10
-    prof_ms = 0.0
     done = 0
     while done < args.steps:
-        n = min(chunk, args.steps - done)
-        e2, e3 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        n = min(10, args.steps - done)
         torch.cuda._sleep(SLEEP_CYCLES)
-        e2.record(stream)
         for _ in range(n):
             one_step()
-        e3.record(stream)
         torch.cuda.synchronize()
-        prof_ms += e2.elapsed_time(e3)
         done += n
-    n_launch, tot_ms, min_ms, max_ms = mlkv.profile_read()
-    durations = mlkv.profile_durations(n_launch)
+    n_launch, w_tot, _, _ = mlkv.profile_read()
     mlkv.profile_disable()
-    ms_step_profiled = prof_ms / args.steps
-    p10, p50, p90 = (float(np.percentile(durations, q)) for q in (10, 50, 90))
-    avg = tot_ms * 1e-3 / n_launch
-    attn_bytes = float(np.mean([x["kv"] + x["q"] + x["out"] for x in per_layer]))
-    achieved = attn_bytes / avg / 1e9
-    cold = None
-    if not args.no_cold:
-        # Cold-cache attention launches: a 1 GiB read evicts the 256 MB
-        # Infinity Cache (clean lines, no write-back) before each launch.
-        log("[bench] cold attention launches")
-        flush = torch.ones(1 << 28, dtype=torch.float32, device=dev)
-        lens_attn = (ctx + 1).to(torch.int32)
-        out_l = torch.empty((w.B, w.h, w.D), dtype=torch.float32, device=dev)
-        reps = 3 * w.l
-        mlkv.profile_enable(reps)
-        sink = torch.zeros((), device=dev)
-        for i in range(reps):
-            n = i % w.l
-            sink += flush.sum()
-            mlkv.decode_attention(n, q[n], cache, mp, lens_attn, out_l, max_len_hint=max_len,
-                                  ws=ws)
-        torch.cuda.synchronize()
-        c_n, c_tot, c_min, c_max = mlkv.profile_read()
-        mlkv.profile_disable()
-        c_avg = c_tot * 1e-3 / c_n
-        cold = {"avg_launch_us": round(c_avg * 1e6, 3),
-                "achieved": round(attn_bytes / c_avg / 1e9, 1),
-                "frac": round(attn_bytes / c_avg / 1e9 / HBM_PEAK_GBS, 4)}
+    w_avg = w_tot * 1e-3 / n_launch
+
     workgroups, max_parts = mp.plan(0, w.B, S, w.D, max_len)
     floor = launch_floor(workgroups)
     ref = read_reference(int(attn_bytes))
-
+    p10, p50, p90 = (float(np.percentile(c_dur, pq)) for pq in (10, 50, 90))
+    gbs = step_total / (ms_step * 1e-3) / 1e9
+    warm_gbs = step_total / (ms_warm * 1e-3) / 1e9
+    merge_kernel = mp.plan_merge_kernel(0, w.B, S, w.D, max_len)
+    kernel = "attention_kernel" + (" + combine_kernel" if merge_kernel else "")
+    roofline = {
+        "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+        "frac": round(achieved / HBM_PEAK_GBS, 4),
+        "traffic": measured_traffic(w.name) if not args.rotary_dims else None,
+        "kernel": kernel,
+        "avg_launch_us": round(c_avg * 1e6, 3),
+        "min_launch_us": round(c_min * 1e3, 3), "max_launch_us": round(c_max * 1e3, 3),
+        "p10_p50_p90_launch_us": [round(p10 * 1e3, 3), round(p50 * 1e3, 3), round(p90 * 1e3, 3)],
+        "launches": c_n, "bytes_per_launch": int(attn_bytes),
+        "cache_state": "Infinity Cache flushed (1 GiB read) before each launch: K/V from HBM",
+        "warm": {"avg_launch_us": round(w_avg * 1e6, 3),
+                 "achieved": round(attn_bytes / w_avg / 1e9, 1),
+                 "frac": round(attn_bytes / w_avg / 1e9 / HBM_PEAK_GBS, 4),
+                 "launches": n_launch,
+                 "cache_state": "natural layer order, back-to-back steps (Infinity Cache "
+                                "serves re-read heads: effective bandwidth, not HBM)"},
+        **floor,
+        "attainable_frac": attainable(attn_bytes, floor["launch_floor_us"]),
+        "read_reference": ref,
+        "frac_of_hbm_read": round(achieved / ref["hbm_2GiB_gbs"], 4),
+    }
     result = {
         "metric": "decode-attention HBM GB/s (% of peak) + decode steps/s, MLKV Pythia-160M shape",
-        "value": round(step_total / (ms_step * 1e-3) / 1e9, 2),
+        "value": round(gbs, 2),
         "unit": "GB/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms_step, 5),
         "steps_per_s": round(1e3 / ms_step, 1),
-        "pct_of_hbm_peak": round(100 * step_total / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 2),
+        "pct_of_hbm_peak": round(100 * achieved / HBM_PEAK_GBS, 2),
+        "step_pct_of_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 2),
         "kv_gbs": round(kv_total / (ms_step * 1e-3) / 1e9, 2),
+        "step_timing": "cold start: Infinity Cache flushed before each step (outside the "
+                       "timed pairs); K/V of each step from HBM",
+        "warm_steps": {"ms_per_step": round(ms_warm, 5), "steps_per_s": round(1e3 / ms_warm, 1),
+                       "gbs": round(warm_gbs, 2),
+                       "note": "back-to-back steps: this workload's cache may stay in the "
+                               "256 MB Infinity Cache between steps (effective bandwidth)"},
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -780,33 +860,20 @@ def main():
                    "ctx_sum": int(inp["ctx"].sum()), "capacity": S,
                    "bytes_per_step": int(step_total), "kv_bytes_per_step": int(kv_total),
                    "workgroups_layer0": workgroups, "rotary_dims": args.rotary_dims},
-        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                     "traffic": measured_traffic(w.name) if not args.rotary_dims else None,
-                     "kernel": "attention_kernel",
-                     "avg_launch_us": round(avg * 1e6, 3),
-                     "min_launch_us": round(min_ms * 1e3, 3),
-                     "max_launch_us": round(max_ms * 1e3, 3),
-                     "p10_p50_p90_launch_us": [round(p10 * 1e3, 3), round(p50 * 1e3, 3),
-                                               round(p90 * 1e3, 3)],
-
-                     "launches": n_launch,
-                     "bytes_per_launch": int(attn_bytes),
-                     "cache_state": "natural layer order, back-to-back steps",
-                     "ms_per_step_while_timed": round(ms_step_profiled, 5),
-                     "cold": cold, **floor,
-                     "attainable_frac": attainable(attn_bytes, floor["launch_floor_us"]),
-                     "read_reference": ref,
-                     "frac_of_same_bytes_read": round(achieved / ref["same_bytes_warm_gbs"], 4)},
+        "roofline": roofline,
     }
-    if not args.no_cpu_baseline:
+    if headline and not args.no_cpu_baseline:
         log("[bench] cpu baseline (oracle)")
         import oracle
 
         kv_of, owner_of = oracle.map_uniform(w.l, w.h, w.m, w.g)
         result["cpu_baseline"] = cpu_baseline(w, inp, kv_of, owner_of, step_total,
                                               rotary=(args.rotary_dims, args.rotary_base))
-    print(json.dumps(result), flush=True)
+    if not headline:
+        for k in ("metric", "n_gpus", "steps", "warmup", "higher_is_better", "scaling",
+                  "vs_baseline", "dtype", "data"):
+            result.pop(k, None)
+    return result
 
 
 if __name__ == "__main__":

@@ -129,6 +129,29 @@ typedef struct {
  * Returns 0 for invalid arguments. */
 size_t mlkv_cache_bytes(const mlkv_map* map, int batch, int capacity, int head_dim);
 
+/*
+ * Fill cache planes from plain rows, on the device (for a cache filled from
+ * outside the decode path, e.g. by a prefill elsewhere, or a migration):
+ *   k_rows, v_rows: device bf16 [kv_count][batch][capacity][head_dim], token
+ *                   rows in plain row-major order (element (c, b, t, d) at
+ *                   ((c*batch + b)*capacity + t)*head_dim + d), 16-byte aligned.
+ * KV heads [kv_begin, kv_begin + kv_count) of the cache receive them: the key
+ * plane as is, the value plane in its 32-token channel-major blocks (layout
+ * above).  Every slot of those heads is written, nothing else.  kv_count 0
+ * does nothing.  Errors: MLKV_ERR_INVALID_ARG (NULL pointers, a head range
+ * outside [0, n_kv)), MLKV_ERR_ALIGNMENT, MLKV_ERR_CAPACITY (capacity not a
+ * multiple of 32, or more than 2^31 - 1 blocks of 32 tokens), MLKV_ERR_UNSUPPORTED
+ * (head_dim), MLKV_ERR_HIP.  Enqueued on `stream`; the rows must not overlap
+ * the planes.
+ */
+mlkv_status mlkv_cache_write_rows(const mlkv_cache* cache, int kv_begin, int kv_count,
+                                  const void* k_rows, const void* v_rows, hipStream_t stream);
+/* The reverse: KV heads [kv_begin, kv_begin + kv_count) of the cache planes
+ * out to plain rows in the same [kv_count][batch][capacity][head_dim] order.
+ * Same arguments and errors. */
+mlkv_status mlkv_cache_read_rows(const mlkv_cache* cache, int kv_begin, int kv_count,
+                                 void* k_rows, void* v_rows, hipStream_t stream);
+
 /* Device workspace needed by mlkv_decode_attention / mlkv_decode_step for any
  * max_len_hint <= capacity (split-K partial results and per-sequence split
  * counters), sized for the current device.  0 for invalid args, and 0 when
@@ -205,27 +228,41 @@ mlkv_status mlkv_decode_step(const void* q_all, const void* k_new_all, const voi
 
 /*
  * mlkv_decode_step with the rotary position embedding of the GPT-NeoX
- * architecture that the paper's Pythia models use (Section 4.2) applied
- * first to the newest token, IN PLACE: on return q_all (every layer and head)
- * and k_new_all (every KV head) hold their vectors rotated at position
- * ctx_lens[b], and the cache holds the rotated keys.  Calling it twice on
- * the same buffers rotates twice.
+ * architecture that the paper's Pythia models use (Section 4.2) applied to
+ * the newest token inside the step: each attention launch rotates the
+ * queries it loads and each owning layer rotates the new keys before storing
+ * them, so the cache holds rotated keys.  q_all and k_new_all are read only
+ * (never written): repeating a call on the same buffers, or replaying it
+ * from a captured graph, gives the same outputs and cache.
  * Rotation: channel pairs (j, j + rotary_dims/2), j < rotary_dims/2, of each
- * head vector turn by ctx_lens[b] * rotary_base^(-2j/rotary_dims) radians
- * (angle, sine, cosine and rotation in double, rounded once to bf16,
- * nearest even); channels at or past rotary_dims and the values are
- * unchanged.  Pythia-160M: rotary_dims 16, rotary_base 10000.
+ * head vector turn by ctx_lens[b] * rotary_base^(-2j/rotary_dims) radians;
+ * the cosine and sine are tabulated once per step in double (in the first
+ * mlkv_workspace_bytes_rope - mlkv_workspace_bytes bytes of the workspace),
+ * each rotated value is computed in double (products and sum each rounded)
+ * and rounded once to bf16, nearest even; channels at or past rotary_dims
+ * and the values are not rotated.  Pythia-160M: rotary_dims 16, rotary_base
+ * 10000.
  *   rotary_dims: a multiple of 16 in [0, head_dim] (else
  *                MLKV_ERR_UNSUPPORTED); 0 is mlkv_decode_step.
  *   rotary_base: positive and finite (else MLKV_ERR_INVALID_ARG).
+ *   workspace:   at least mlkv_workspace_bytes_rope(...) bytes, 16-byte
+ *                aligned, initialised once by mlkv_workspace_init (else
+ *                MLKV_ERR_WORKSPACE / MLKV_ERR_ALIGNMENT).
  * Other arguments and errors as mlkv_decode_step; every check is made before
- * anything is rotated or launched.
+ * anything is launched.
  */
-mlkv_status mlkv_decode_step_rope(void* q_all, void* k_new_all, const void* v_new_all,
+mlkv_status mlkv_decode_step_rope(const void* q_all, const void* k_new_all, const void* v_new_all,
                                   const mlkv_cache* cache, const mlkv_map* map,
                                   const int32_t* ctx_lens, int rotary_dims, double rotary_base,
                                   void* out_all, mlkv_out_dtype out_dtype, int max_len_hint,
                                   void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Workspace of mlkv_decode_step_rope: the rotary table (batch *
+ * rotary_dims/2 (cos, sin) pairs in double, rounded up to 256 bytes) followed
+ * by a decode workspace of mlkv_workspace_bytes(map, batch, capacity,
+ * head_dim) bytes.  0 for invalid arguments (rotary_dims as above). */
+size_t mlkv_workspace_bytes_rope(const mlkv_map* map, int batch, int capacity, int head_dim,
+                                 int rotary_dims);
 
 /* ----------------------------------------------------------------------- */
 /* Prefill: T new tokens per sequence (a prompt, or a chunk of one)          */
@@ -391,6 +428,12 @@ int mlkv_model_fused_path(const mlkv_model* model, int batch);
  * Returns MLKV_ERR_* on invalid arguments. */
 mlkv_status mlkv_plan(const mlkv_map* map, int layer, int batch, int capacity, int head_dim,
                       int max_len, int* workgroups, int* max_parts);
+/* 1 when that plan finishes split runs with the separate merge kernel after
+ * the attention kernel, 0 when the attention launch finishes every
+ * (sequence, KV head) itself, -1 for invalid arguments (same arguments and
+ * environment overrides as mlkv_plan). */
+int mlkv_plan_merge_kernel(const mlkv_map* map, int layer, int batch, int capacity, int head_dim,
+                           int max_len);
 
 /* ----------------------------------------------------------------------- */
 /* Kernel timing (benchmarks)                                                */
@@ -399,8 +442,11 @@ mlkv_status mlkv_plan(const mlkv_map* map, int layer, int batch, int capacity, i
 /* While enabled (on the calling thread), every split-K attention kernel that
  * mlkv_decode_attention / mlkv_decode_step launches, and every prefill
  * attention kernel of mlkv_prefill_attention / mlkv_prefill_step, is
- * bracketed by a pair of HIP events recorded on its launch stream (the merge
- * kernel, when one runs, and the append kernels are outside the pair).  Up to max_launches launches
+ * bracketed by a pair of HIP events recorded on its launch stream; when a
+ * separate merge kernel finishes the split runs of that attention launch, the
+ * pair brackets both kernels (start with the attention dispatch, stop when
+ * the merge completes), so one timed launch is a layer's whole attention.
+ * Separate append kernels are outside the pair.  Up to max_launches launches
  * are recorded; later ones are not timed.  Creates the events (host call, not
  * for capture).  Errors: MLKV_ERR_INVALID_ARG (max_launches <= 0),
  * MLKV_ERR_HIP. */

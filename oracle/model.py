@@ -78,7 +78,7 @@ def attend(q: np.ndarray, K: np.ndarray, V: np.ndarray) -> np.ndarray:
 
 def decode_step_model(x, layers, kv_of, owner_of, k_cache, v_cache, ctx, h: int, D: int,
                       rd: int, base: float = 10000.0, eps: float = 1e-5,
-                      round_bf16: bool = True) -> np.ndarray:
+                      round_bf16: bool = True, updates: list | None = None) -> np.ndarray:
     """One decode step through every layer.
 
     x        [B][d] float64, the newest token's residual stream
@@ -86,6 +86,8 @@ def decode_step_model(x, layers, kv_of, owner_of, k_cache, v_cache, ctx, h: int,
              slot ctx[b]); positions 0 .. ctx[b]-1 hold the cached tokens
     ctx      [B] tokens cached before the step
     Returns the residual stream after the last layer, [B][d] float64.
+    updates: if a list, each layer appends its two residual updates (a, m),
+    each [B][d] (for error estimates in the tests; nothing else changes).
     """
     rb = to_bf16 if round_bf16 else (lambda a: a)
     x = np.array(x, dtype=np.float64)
@@ -119,5 +121,7 @@ def decode_step_model(x, layers, kv_of, owner_of, k_cache, v_cache, ctx, h: int,
         a = o.reshape(B, h * D) @ g["w_o"] + g["b_o"]
         f = rb(gelu(h2 @ g["w_fc1"] + g["b_fc1"]))
         m = f @ g["w_fc2"] + g["b_fc2"]
+        if updates is not None:
+            updates.append((a, m))
         x = x + a + m
     return x

@@ -19,8 +19,7 @@ import numpy as np
 import torch  # loaded first: the library then binds to torch's HIP runtime
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-# MLKV_LIBRARY may name another build of the same library (e.g. for A/B timing).
-LIB_PATH = os.environ.get("MLKV_LIBRARY") or os.path.join(_HERE, "libmlkv.so")
+LIB_PATH = os.path.join(_HERE, "libmlkv.so")
 
 MLKV_OK = 0
 STATUS_NAMES = ["MLKV_OK", "MLKV_ERR_INVALID_ARG", "MLKV_ERR_BAD_MAP", "MLKV_ERR_ALIGNMENT",
@@ -36,11 +35,12 @@ EXPORTS = [
     "mlkv_map_kv_head", "mlkv_map_owner_layer", "mlkv_map_layer_kv_count",
     "mlkv_map_layer_owned_count", "mlkv_map_layer_owned_begin", "mlkv_cache_bytes",
     "mlkv_workspace_bytes", "mlkv_cache_append", "mlkv_decode_attention", "mlkv_decode_step",
-    "mlkv_plan", "mlkv_workspace_init", "mlkv_profile_enable", "mlkv_profile_read",
+    "mlkv_plan", "mlkv_plan_merge_kernel", "mlkv_workspace_init", "mlkv_profile_enable", "mlkv_profile_read",
     "mlkv_profile_durations", "mlkv_profile_disable", "mlkv_profile_launch_floor",
     "mlkv_profile_read_bandwidth",
-    "mlkv_decode_step_rope",
+    "mlkv_decode_step_rope", "mlkv_workspace_bytes_rope",
     "mlkv_cache_append_rows", "mlkv_prefill_attention", "mlkv_prefill_step",
+    "mlkv_cache_write_rows", "mlkv_cache_read_rows",
     "mlkv_model_create", "mlkv_model_destroy", "mlkv_model_workspace_bytes",
     "mlkv_model_fused_path",
     "mlkv_model_decode_step",
@@ -92,7 +92,10 @@ def lib():
             "mlkv_decode_attention": ([I, P, P, P, P, P, I, I, P, Z, P], S),
             "mlkv_decode_step": ([P, P, P, P, P, P, P, I, I, P, Z, P], S),
             "mlkv_decode_step_rope": ([P, P, P, P, P, P, I, ctypes.c_double, P, I, I, P, Z, P], S),
+            "mlkv_workspace_bytes_rope": ([P, I, I, I, I], Z),
             "mlkv_cache_append_rows": ([I, P, P, P, P, I, I, P, P], S),
+            "mlkv_cache_write_rows": ([P, I, I, P, P, P], S),
+            "mlkv_cache_read_rows": ([P, I, I, P, P, P], S),
             "mlkv_prefill_attention": ([I, P, P, P, P, I, P, I, P], S),
             "mlkv_prefill_step": ([P, P, P, P, P, P, I, P, I, P], S),
             "mlkv_model_create": ([P, I, I, I, I, ctypes.c_double, ctypes.c_double, P, P], S),
@@ -101,6 +104,7 @@ def lib():
             "mlkv_model_fused_path": ([P, I], I),
             "mlkv_model_decode_step": ([P, P, P, P, I, P, Z, P], S),
             "mlkv_plan": ([P, I, I, I, I, I, ctypes.POINTER(I), ctypes.POINTER(I)], S),
+            "mlkv_plan_merge_kernel": ([P, I, I, I, I, I], I),
             "mlkv_workspace_init": ([P, Z, P], S),
             "mlkv_profile_enable": ([I], S),
             "mlkv_profile_read": ([ctypes.POINTER(I)] + [ctypes.POINTER(ctypes.c_double)] * 3, S),
@@ -212,7 +216,11 @@ class Map:
     def cache_bytes(self, batch: int, capacity: int, head_dim: int) -> int:
         return lib().mlkv_cache_bytes(self._h, batch, capacity, head_dim)
 
-    def workspace_bytes(self, batch: int, capacity: int, head_dim: int) -> int:
+    def workspace_bytes(self, batch: int, capacity: int, head_dim: int,
+                        rotary_dims: int = 0) -> int:
+        """mlkv_workspace_bytes, or mlkv_workspace_bytes_rope when rotary_dims > 0."""
+        if rotary_dims:
+            return lib().mlkv_workspace_bytes_rope(self._h, batch, capacity, head_dim, rotary_dims)
         return lib().mlkv_workspace_bytes(self._h, batch, capacity, head_dim)
 
     def plan(self, layer: int, batch: int, capacity: int, head_dim: int, max_len: int = 0):
@@ -221,6 +229,15 @@ class Map:
         _check(lib().mlkv_plan(self._h, layer, batch, capacity, head_dim, max_len,
                                ctypes.byref(wg), ctypes.byref(mp)))
         return wg.value, mp.value
+
+    def plan_merge_kernel(self, layer: int, batch: int, capacity: int, head_dim: int,
+                          max_len: int = 0) -> bool:
+        """mlkv_plan_merge_kernel: whether a separate merge kernel follows the
+        attention launch of that plan."""
+        r = lib().mlkv_plan_merge_kernel(self._h, layer, batch, capacity, head_dim, max_len)
+        if r < 0:
+            raise ValueError("invalid plan arguments")
+        return bool(r)
 
 
 # ------------------------------------------------------------------- cache ---
@@ -251,22 +268,39 @@ class Cache:
     def struct(self):
         return ctypes.byref(self._c)
 
+    def write_rows(self, k_rows: torch.Tensor, v_rows: torch.Tensor, kv_begin: int = 0,
+                   stream=None):
+        """mlkv_cache_write_rows: device rows [n][B][S][D] bf16 (plain row-major
+        token rows) into the planes of KV heads kv_begin .. kv_begin + n - 1."""
+        n = k_rows.shape[0]
+        shape = (n, self.batch, self.capacity, self.head_dim)
+        if tuple(k_rows.shape) != shape or tuple(v_rows.shape) != shape:
+            raise ValueError(f"rows must be {shape}")
+        _check(lib().mlkv_cache_write_rows(self.struct, kv_begin, n,
+                                           _dev_ptr(k_rows, torch.bfloat16, "k_rows"),
+                                           _dev_ptr(v_rows, torch.bfloat16, "v_rows"),
+                                           _stream(stream)))
+
+    def read_rows(self, kv_begin: int = 0, kv_count: int | None = None, stream=None):
+        """mlkv_cache_read_rows: the planes of KV heads kv_begin .. +kv_count-1
+        as device rows (k, v), each [kv_count][B][S][D] bf16."""
+        n = self.n_kv - kv_begin if kv_count is None else kv_count
+        shape = (n, self.batch, self.capacity, self.head_dim)
+        k = torch.empty(shape, dtype=torch.bfloat16, device=self.k.device)
+        v = torch.empty(shape, dtype=torch.bfloat16, device=self.k.device)
+        _check(lib().mlkv_cache_read_rows(self.struct, kv_begin, n, _dev_ptr(k, torch.bfloat16, "k"),
+                                          _dev_ptr(v, torch.bfloat16, "v"), _stream(stream)))
+        return k, v
+
     def load_rows(self, k_rows: np.ndarray, v_rows: np.ndarray, kv_range=None):
-        """Copy logical host rows ([n][B][S][D] bf16 bit patterns, uint16) for the
-        KV heads kv_range (default: all) into the device planes."""
+        """Upload logical host rows ([n][B][S][D] bf16 bit patterns, uint16) for
+        the KV heads kv_range (default: all) and write them into the planes
+        on the device (mlkv_cache_write_rows)."""
         lo, hi = kv_range if kv_range is not None else (0, self.n_kv)
         assert k_rows.shape == (hi - lo, self.batch, self.capacity, self.head_dim)
         assert v_rows.shape == k_rows.shape
-        self.k[lo:hi].copy_(bf16_tensor(k_rows))
-        self.v[lo:hi].copy_(bf16_tensor(pack_value_rows(v_rows)))
-
-
-def pack_value_rows(v_rows: np.ndarray) -> np.ndarray:
-    """Host-side conversion of logical value rows [..., S, D] into the value
-    plane's blocked layout [..., S/32, D, 32]."""
-    *lead, S, D = v_rows.shape
-    blk = v_rows.reshape(*lead, S // V_BLOCK, V_BLOCK, D)
-    return np.ascontiguousarray(np.swapaxes(blk, -1, -2))
+        dev = self.k.device
+        self.write_rows(bf16_tensor(k_rows, dev), bf16_tensor(v_rows, dev), lo)
 
 
 def bf16_tensor(a: np.ndarray, device=None) -> torch.Tensor:
@@ -281,9 +315,10 @@ def bf16_bits(t: torch.Tensor) -> np.ndarray:
 
 
 def workspace(map_: Map, batch: int, capacity: int, head_dim: int, device="cuda",
-              stream=None) -> torch.Tensor:
-    """Allocate and initialise (mlkv_workspace_init) a decode workspace."""
-    n = map_.workspace_bytes(batch, capacity, head_dim)
+              stream=None, rotary_dims: int = 0) -> torch.Tensor:
+    """Allocate and initialise (mlkv_workspace_init) a decode workspace (with
+    room for the rotary table of mlkv_decode_step_rope when rotary_dims > 0)."""
+    n = map_.workspace_bytes(batch, capacity, head_dim, rotary_dims)
     ws = torch.empty(max(n, 16), dtype=torch.uint8, device=device)
     _check(lib().mlkv_workspace_init(ws.data_ptr(), ws.numel(), _stream(stream)))
     return ws
@@ -322,8 +357,9 @@ def decode_step(q_all: torch.Tensor, k_new_all: torch.Tensor, v_new_all: torch.T
                 rotary_dims: int = 0, rotary_base: float = 10000.0):
     """mlkv_decode_step over all layers: q_all [l][B][h][D], k/v_new_all [B][n_kv][D].
     rotary_dims > 0 calls mlkv_decode_step_rope: the newest token's queries
-    and keys are first rotated IN PLACE (q_all and k_new_all) at position
-    ctx_lens[b]."""
+    and keys are rotated at position ctx_lens[b] inside the step (q_all and
+    k_new_all are not written); ws must then come from
+    workspace(..., rotary_dims=rotary_dims)."""
     out_dt = OUT_BF16 if out_all.dtype == torch.bfloat16 else OUT_F32
     if out_all.dtype not in (torch.float32, torch.bfloat16):
         raise ValueError("out_all must be float32 or bfloat16")

@@ -7,15 +7,16 @@
 namespace mlkv {
 
 // Rotary position embedding of the newest token (GPT-NeoX: rotate-half pairs
-// (j, j + dims/2) of the first `dims` channels of every head vector), applied
-// in place to its queries of every layer and its keys of every KV head.
-// inv_freq[j] = base^(-2j/dims): radians pair j turns by per position.
+// (j, j + half) of the first 2*half channels of every head vector).  Once per
+// step the cosine and sine of each pair's angle at the token's position are
+// tabulated in double, cs[(b*half + j)*2 + {0, 1}]; the attention launches
+// rotate their queries and the owners' appends their keys from that table.
+// inv_freq[j] = base^(-2j/(2*half)): radians pair j turns by per position.
 constexpr int kMaxRopePairs = 64;
-struct RopeParams {
-  uint16_t* q;               // [l][B][h][D]
-  uint16_t* k;               // [B][n_kv][D]
+struct RopeTableParams {
   const int32_t* pos;        // [B] position of sequence b's newest token
-  int l, B, h, n_kv, D, dims;
+  double* cs;                // [B][half][2] out: cos, sin
+  int B, half;
   double inv_freq[kMaxRopePairs];
 };
 
@@ -26,6 +27,20 @@ struct AppendParams {
   uint16_t* k;               // key plane
   uint16_t* v;               // value plane
   int B, S, kv_begin, row_stride;
+  const double* rope_cs;     // null, or the step's rotary table: keys rotated before they are stored
+  int rope_half;
+};
+
+// Whole-plane conversion between logical rows [kv][B][S][D] (row-major) and
+// the cache planes (K identical, V in channel-major 32-token blocks), for the
+// KV heads [kv_begin, kv_begin + kv_count): to_cache 1 writes the planes from
+// the rows, 0 the rows from the planes.
+struct CacheRowsParams {
+  uint16_t* k_plane;
+  uint16_t* v_plane;
+  uint16_t* k_rows;          // [kv_count][B][S][D]
+  uint16_t* v_rows;
+  int B, S, kv_begin, kv_count, to_cache;
 };
 
 // Owners' rows of a prompt: row (b, t) at k_new + (b*T + t)*row_stride,
@@ -91,6 +106,10 @@ struct AttnParams {
   const uint16_t* k_new;
   const uint16_t* v_new;
   int new_stride, own_begin, own_count;
+  // Rotary embedding of the step's newest token (null: none): queries are
+  // rotated as they are loaded, the owner's new key before it is stored.
+  const double* rope_cs;     // [B][rope_half][2] cos, sin at the token's position
+  int rope_half;
 };
 
 // ---- GPT-NeoX layer pieces around attention (model.hip) ----
@@ -168,7 +187,8 @@ hipError_t launch_residual(const ResidualParams& p, hipStream_t stream);
 
 hipError_t launch_append(const AppendParams& p, int head_dim, int owned_count,
                          hipStream_t stream);
-hipError_t launch_rope(const RopeParams& p, hipStream_t stream);
+hipError_t launch_rope_table(const RopeTableParams& p, hipStream_t stream);
+hipError_t launch_cache_rows(const CacheRowsParams& p, int head_dim, hipStream_t stream);
 hipError_t launch_append_rows(const AppendRowsParams& p, int head_dim, int owned_count,
                               hipStream_t stream);
 // start/stop: optional events recorded around the prefill dispatch.
@@ -179,7 +199,9 @@ hipError_t launch_prefill(const PrefillParams& p, int head_dim, hipStream_t stre
 // start/stop: optional events recorded around the attention dispatch.
 hipError_t launch_attention_main(const AttnParams& p, int head_dim, hipStream_t stream,
                                  hipEvent_t start, hipEvent_t stop);
-hipError_t launch_attention_merge(const AttnParams& p, int head_dim, hipStream_t stream);
+// stop: optional event recorded when the merge kernel completes.
+hipError_t launch_attention_merge(const AttnParams& p, int head_dim, hipStream_t stream,
+                                  hipEvent_t stop);
 int max_batch();
 int stage_floats();  // partial-output floats one workgroup can merge in place
 int resident_workgroups(int head_dim); // attention workgroups the device holds at once (0: none)

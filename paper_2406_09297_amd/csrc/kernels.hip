@@ -61,36 +61,27 @@ __device__ __forceinline__ int attended_len(const AttnParams& p, int b) {
 __device__ __forceinline__ int tiles_of(int L) { return (L + kTile - 1) / kTile; }
 
 // ---------------------------------------------------------------------------
-// Cache append (Section 2.4): one workgroup per (sequence b, owned head c),
-// one thread per 8 channels.
-// ---------------------------------------------------------------------------
-template <int D>
-__global__ __launch_bounds__(D / 8) void append_kernel(AppendParams p) {
-  const int b = blockIdx.x;
-  const int c = blockIdx.y;
-  const int pos = p.positions[b];
-  if (pos < 0 || pos >= p.S) return;
-  const int d0 = threadIdx.x * 8;
-  const size_t src = static_cast<size_t>(b) * p.row_stride + static_cast<size_t>(c) * D + d0;
-  const u16x8 kv_k = load16(p.k_new + src);
-  const u16x8 kv_v = load16(p.v_new + src);
-  const size_t seq = static_cast<size_t>(p.kv_begin + c) * p.B + b;
-  *reinterpret_cast<u16x8*>(p.k + (seq * p.S + pos) * D + d0) = kv_k;
-  uint16_t* vdst = p.v + (seq * p.S + (pos & ~(kTile - 1))) * D + (pos & (kTile - 1));
-#pragma unroll
-  for (int e = 0; e < 8; ++e) vdst[(d0 + e) * kTile] = kv_v[e];
-}
-
-// ---------------------------------------------------------------------------
 // Rotary position embedding of the GPT-NeoX architecture (the paper's Pythia
-// models, Section 4.2), for the newest token of each sequence, in place.
-// Workgroup (x, b): the cosine and sine of every channel pair's angle at
-// position pos[b] are taken in double, one pair per thread, into LDS; then
-// each thread rotates eight pairs (channels j0..j0+7 with their partners
-// j0+dims/2..) of one head vector: a query of some layer, or a key.  The
-// rotation is evaluated in double and rounded once to bf16, nearest even.
+// models, Section 4.2) for the newest token of each sequence.  Pair
+// (j, j + half) of a head vector's first 2*half channels turns by the angle
+// pos * base^(-2j/(2*half)):
+//   y_j = x_j cos - x_{j+half} sin,   y_{j+half} = x_{j+half} cos + x_j sin.
+// rope_table_kernel tabulates cos and sin in double once per step, one
+// (sequence, pair) per thread; the attention and append kernels rotate the
+// 8-channel chunks they load from that table.  Each product and the sum are
+// rounded in double (no fused multiply-add) and the result once to bf16,
+// nearest even.
 // ---------------------------------------------------------------------------
 constexpr int kRopeThreads = 256;
+
+__global__ __launch_bounds__(kRopeThreads) void rope_table_kernel(RopeTableParams p) {
+  const int i = blockIdx.x * kRopeThreads + threadIdx.x;
+  if (i >= p.B * p.half) return;
+  const int b = i / p.half, j = i - b * p.half;
+  double s, c;
+  sincos(static_cast<double>(p.pos[b]) * p.inv_freq[j], &s, &c);
+  reinterpret_cast<double2*>(p.cs)[i] = make_double2(c, s);
+}
 
 __device__ __forceinline__ uint16_t f64_to_bf16_bits(double v) {
   // Round to odd into fp32 (24 bits: no double rounding), then to nearest
@@ -101,38 +92,120 @@ __device__ __forceinline__ uint16_t f64_to_bf16_bits(double v) {
   return f32_to_bf16_bits(__builtin_bit_cast(float, u));
 }
 
-__global__ __launch_bounds__(kRopeThreads) void rope_kernel(RopeParams p) {
-  __shared__ double cos_t[kMaxRopePairs], sin_t[kMaxRopePairs];
-  const int b = blockIdx.y;
-  const int half = p.dims / 2;
-  const double pos = static_cast<double>(p.pos[b]);
-  for (int t = threadIdx.x; t < half; t += kRopeThreads)
-    sincos(pos * p.inv_freq[t], &sin_t[t], &cos_t[t]);
-  __syncthreads();
-  const int chunks = p.dims / 16;  // eight-pair chunks per head vector
-  const int rows = p.l * p.h + p.n_kv;
-  const int item = blockIdx.x * kRopeThreads + threadIdx.x;
-  if (item >= rows * chunks) return;
-  const int row = item / chunks;
-  const int j0 = (item - row * chunks) * 8;
-  uint16_t* x;
-  if (row < p.l * p.h) {
-    const int n = row / p.h, i = row - n * p.h;
-    x = p.q + ((static_cast<size_t>(n) * p.B + b) * p.h + i) * p.D;
-  } else {
-    x = p.k + (static_cast<size_t>(b) * p.n_kv + (row - p.l * p.h)) * p.D;
-  }
-  const u16x8 a = load16(x + j0), c = load16(x + half + j0);
-  u16x8 ya, yc;
+__device__ __forceinline__ double bf16_to_f64(uint16_t x) {
+  return __builtin_bit_cast(float, static_cast<uint32_t>(x) << 16);
+}
+
+// y = own cos -/+ partner sin with both products and the sum rounded.
+template <bool HI>
+__device__ __forceinline__ double rotate_one(double own, double partner, double c, double s) {
+#pragma clang fp contract(off)
+  return HI ? own * c + partner * s : own * c - partner * s;
+}
+
+// The rotated chunk of channels c0 .. c0+7 (c0 a multiple of 8): `own` holds
+// them, `partner` channels c0 + half (c0 < half) or c0 - half (half <= c0 <
+// 2*half); cs = the table entries (cos, sin) of pairs c0 % half ... Chunks at
+// or past 2*half are returned unchanged.
+template <typename CS>
+__device__ __forceinline__ u16x8 rotate_chunk(u16x8 own, u16x8 partner, int c0, int half, CS cs) {
+  if (c0 >= 2 * half) return own;
+  const bool hi = c0 >= half;
+  const int j0 = hi ? c0 - half : c0;
+  u16x8 y;
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
-    const double u = __builtin_bit_cast(float, static_cast<uint32_t>(a[e]) << 16);
-    const double w = __builtin_bit_cast(float, static_cast<uint32_t>(c[e]) << 16);
-    ya[e] = f64_to_bf16_bits(u * cos_t[j0 + e] - w * sin_t[j0 + e]);
-    yc[e] = f64_to_bf16_bits(w * cos_t[j0 + e] + u * sin_t[j0 + e]);
+    const double2 t = cs(j0 + e);
+    const double u = bf16_to_f64(own[e]), w = bf16_to_f64(partner[e]);
+    y[e] = f64_to_bf16_bits(hi ? rotate_one<true>(u, w, t.x, t.y) : rotate_one<false>(u, w, t.x, t.y));
   }
-  *reinterpret_cast<u16x8*>(x + j0) = ya;
-  *reinterpret_cast<u16x8*>(x + half + j0) = yc;
+  return y;
+}
+
+// Offset of the channel chunk paired with chunk c0 (see rotate_chunk).
+__device__ __forceinline__ int partner_chunk(int c0, int half) {
+  return c0 < half ? c0 + half : c0 - half;
+}
+
+// ---------------------------------------------------------------------------
+// Cache append (Section 2.4): one workgroup per (sequence b, owned head c),
+// one thread per 8 channels.  With a rotary table the key is rotated first.
+// ---------------------------------------------------------------------------
+template <int D>
+__global__ __launch_bounds__(D / 8) void append_kernel(AppendParams p) {
+  const int b = blockIdx.x;
+  const int c = blockIdx.y;
+  const int pos = p.positions[b];
+  if (pos < 0 || pos >= p.S) return;
+  const int d0 = threadIdx.x * 8;
+  const size_t row = static_cast<size_t>(b) * p.row_stride + static_cast<size_t>(c) * D;
+  u16x8 kv_k = load16(p.k_new + row + d0);
+  const u16x8 kv_v = load16(p.v_new + row + d0);
+  if (p.rope_cs && d0 < 2 * p.rope_half) {
+    const u16x8 partner = load16(p.k_new + row + partner_chunk(d0, p.rope_half));
+    const double2* cs = reinterpret_cast<const double2*>(p.rope_cs) + static_cast<size_t>(b) * p.rope_half;
+    kv_k = rotate_chunk(kv_k, partner, d0, p.rope_half, [&](int j) { return cs[j]; });
+  }
+  const size_t seq = static_cast<size_t>(p.kv_begin + c) * p.B + b;
+  *reinterpret_cast<u16x8*>(p.k + (seq * p.S + pos) * D + d0) = kv_k;
+  uint16_t* vdst = p.v + (seq * p.S + (pos & ~(kTile - 1))) * D + (pos & (kTile - 1));
+#pragma unroll
+  for (int e = 0; e < 8; ++e) vdst[(d0 + e) * kTile] = kv_v[e];
+}
+
+// ---------------------------------------------------------------------------
+// Cache planes <-> logical rows, one workgroup per 32-token block of one
+// (KV head, sequence): the block's K rows are copied as they are; its V rows
+// go through LDS, where the [32][D] tile is transposed to [D][32], so both
+// the row side and the plane side move in 16-byte pieces.
+// ---------------------------------------------------------------------------
+constexpr int kRowsThreads = 256;
+
+template <int D>
+__global__ __launch_bounds__(kRowsThreads) void cache_rows_kernel(CacheRowsParams p) {
+  constexpr int kChunks = kTile * D / 8;      // 16-byte pieces per block and plane
+  constexpr int kPad = 8;                     // LDS row padding (elements)
+  __shared__ alignas(16) uint16_t tile[kTile][D + kPad];
+  const size_t blocks_per_seq = static_cast<size_t>(p.S / kTile);
+  const size_t blk = blockIdx.x;              // (c, b, t-block), c-major
+  const size_t seq = blk / blocks_per_seq;    // c * B + b
+  const size_t tb = blk - seq * blocks_per_seq;
+  const size_t row_off = (seq * p.S + tb * kTile) * D;  // in the rows
+  const size_t plane_off = (static_cast<size_t>(p.kv_begin) * p.B * p.S) * D + row_off;
+  for (int i = threadIdx.x; i < kChunks; i += kRowsThreads) {
+    const size_t e = static_cast<size_t>(i) * 8;
+    if (p.to_cache)
+      *reinterpret_cast<u16x8*>(p.k_plane + plane_off + e) = load16(p.k_rows + row_off + e);
+    else
+      *reinterpret_cast<u16x8*>(p.k_rows + row_off + e) = load16(p.k_plane + plane_off + e);
+  }
+  if (p.to_cache) {
+    for (int i = threadIdx.x; i < kChunks; i += kRowsThreads) {  // token i / (D/8), channels
+      const int t = i / (D / 8), c = (i - t * (D / 8)) * 8;
+      *reinterpret_cast<u16x8*>(&tile[t][c]) = load16(p.v_rows + row_off + t * D + c);
+    }
+    __syncthreads();
+    for (int i = threadIdx.x; i < kChunks; i += kRowsThreads) {  // channel i / 4, tokens
+      const int d = i / (kTile / 8), t0 = (i - d * (kTile / 8)) * 8;
+      u16x8 v;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] = tile[t0 + e][d];
+      *reinterpret_cast<u16x8*>(p.v_plane + plane_off + d * kTile + t0) = v;
+    }
+  } else {
+    for (int i = threadIdx.x; i < kChunks; i += kRowsThreads) {
+      const int d = i / (kTile / 8), t0 = (i - d * (kTile / 8)) * 8;
+      const u16x8 v = load16(p.v_plane + plane_off + d * kTile + t0);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) tile[t0 + e][d] = v[e];
+    }
+    __syncthreads();
+    for (int i = threadIdx.x; i < kChunks; i += kRowsThreads) {
+      const int t = i / (D / 8), c = (i - t * (D / 8)) * 8;
+      *reinterpret_cast<u16x8*>(p.v_rows + row_off + t * D + c) =
+          *reinterpret_cast<const u16x8*>(&tile[t][c]);
+    }
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -180,6 +253,7 @@ struct alignas(16) AttnShared {
   };
   float stage_ml[kStageMl];
   alignas(16) uint16_t new_row[2 * D];  // newest token's key and value (fused append)
+  double2 rope[kMaxRopePairs];          // the sequence's rotary (cos, sin) pairs
   // QK_VALU: the group's queries (16 heads, zero-padded) and each wave's
   // score block [16 heads][32 tokens].
   alignas(16) uint16_t q_lds[QK_VALU ? 16 * D : 8];
@@ -362,6 +436,10 @@ void attention_kernel(AttnParams p) {
     k0 = j * R;
     k1 = k0 + R < tiles_b ? k0 + R : tiles_b;
     if (plan_out && threadIdx.x == 0) plan_out[g] = RunItem{b, r, j, nb, L, k0, k1, z};
+    // The schedule tables share LDS with the waves' merge area: every wave
+    // has read them (the run is in registers) before any wave, possibly one
+    // with no tiles of its own, writes its partial there.
+    __syncthreads();
   }
 
   const int kv = p.kv_begin + r;
@@ -370,30 +448,24 @@ void attention_kernel(AttnParams p) {
   const uint16_t* kbase = p.k + seq * p.S * D;
   const uint16_t* vbase = p.v + seq * p.S * D;
 
-  if (QK_VALU) {  // stage the group's queries (padded heads zero) and zero padded score rows
-    for (int idx = threadIdx.x; idx < 16 * D / 8; idx += NT) {
-      const int hh = idx / (D / 8);
-      const int c = (idx - hh * (D / 8)) * 8;
-      u16x8 v = {0, 0, 0, 0, 0, 0, 0, 0};
-      if (hh < p.G) v = load16(p.q + (static_cast<size_t>(b) * p.h + head0 + hh) * D + c);
-      *reinterpret_cast<u16x8*>(&sm.q_lds[hh * D + c]) = v;
-    }
-    for (int idx = threadIdx.x; idx < W * 16 * kTile; idx += NT)
-      if ((idx / kTile) % 16 >= p.G) sm.s_lds[idx] = 0.f;
-    __syncthreads();
-  }
-  bf16x8 qf[KK];
-  {
-    const bool valid = col < p.G;
-    const uint16_t* qrow =
-        p.q + (static_cast<size_t>(b) * p.h + head0 + (valid ? col : p.G - 1)) * D + grp * 8;
+  // This lane's query chunks (channels grp*8 + kk*32 .. +7 of its head; a
+  // padded head reads the group's last one and scores zero).  With rotation,
+  // also the partner chunks and this sequence's table entries, all in flight
+  // together with the first tile.
+  const int rope_half = p.rope_cs ? p.rope_half : 0;
+  const bool valid = col < p.G;
+  const uint16_t* qrow = p.q + (static_cast<size_t>(b) * p.h + head0 + (valid ? col : p.G - 1)) * D;
+  u16x8 qraw[KK], qpart[KK];
 #pragma unroll
-    for (int kk = 0; kk < KK; ++kk) {
-      const u16x8 v = load16(qrow + kk * 32);
-      const u16x8 zero = {0, 0, 0, 0, 0, 0, 0, 0};
-      qf[kk] = as_bf16(valid ? v : zero);  // padded heads score zero
-    }
+  for (int kk = 0; kk < KK; ++kk) {
+    const int c0 = grp * 8 + kk * 32;
+    qraw[kk] = load16(qrow + c0);
+    qpart[kk] = c0 < 2 * rope_half ? load16(qrow + partner_chunk(c0, rope_half)) : qraw[kk];
   }
+  double2 cs_mine = make_double2(0.0, 0.0);
+  if (threadIdx.x < rope_half)
+    cs_mine = reinterpret_cast<const double2*>(p.rope_cs)[static_cast<size_t>(b) * rope_half + threadIdx.x];
+
   Tile<D> ta, tb;
   int it = k0 + wave;
   WaveState<D> st;
@@ -411,6 +483,37 @@ void attention_kernel(AttnParams p) {
       return;
     }
   }
+  auto cs_lds = [&](int jj) { return sm.rope[jj]; };
+  if (rope_half) {  // the table to LDS, then the queries rotated in registers
+    if (threadIdx.x < rope_half) sm.rope[threadIdx.x] = cs_mine;
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk)
+      qraw[kk] = rotate_chunk(qraw[kk], qpart[kk], grp * 8 + kk * 32, rope_half, cs_lds);
+  }
+  if (QK_VALU) {  // stage the group's queries (padded heads zero) and zero padded score rows
+    for (int idx = threadIdx.x; idx < 16 * D / 8; idx += NT) {
+      const int hh = idx / (D / 8);
+      const int c = (idx - hh * (D / 8)) * 8;
+      u16x8 v = {0, 0, 0, 0, 0, 0, 0, 0};
+      if (hh < p.G) {
+        const uint16_t* row = p.q + (static_cast<size_t>(b) * p.h + head0 + hh) * D;
+        v = load16(row + c);
+        if (c < 2 * rope_half)
+          v = rotate_chunk(v, load16(row + partner_chunk(c, rope_half)), c, rope_half, cs_lds);
+      }
+      *reinterpret_cast<u16x8*>(&sm.q_lds[hh * D + c]) = v;
+    }
+    for (int idx = threadIdx.x; idx < W * 16 * kTile; idx += NT)
+      if ((idx / kTile) % 16 >= p.G) sm.s_lds[idx] = 0.f;
+    __syncthreads();
+  }
+  bf16x8 qf[KK];
+#pragma unroll
+  for (int kk = 0; kk < KK; ++kk) {
+    const u16x8 zero = {0, 0, 0, 0, 0, 0, 0, 0};
+    qf[kk] = as_bf16(valid ? qraw[kk] : zero);  // padded heads score zero
+  }
   const bool has_tiles = it < k1;
   float* const s_wave = sm.s_lds + (QK_VALU ? wave * 16 * kTile : 0);
 
@@ -425,8 +528,11 @@ void attention_kernel(AttnParams p) {
       if (threadIdx.x < D / 8) {
         const int d0 = threadIdx.x * 8;
         const size_t src = static_cast<size_t>(b) * p.new_stride + static_cast<size_t>(kv) * D + d0;
-        const u16x8 nk = load16(p.k_new + src);
+        u16x8 nk = load16(p.k_new + src);
         const u16x8 nv = load16(p.v_new + src);
+        if (d0 < 2 * rope_half)
+          nk = rotate_chunk(nk, load16(p.k_new + src - d0 + partner_chunk(d0, rope_half)), d0,
+                            rope_half, cs_lds);
         uint16_t* kc = const_cast<uint16_t*>(kbase);  // the caller's cache, written here only
         uint16_t* vc = const_cast<uint16_t*>(vbase);
         *reinterpret_cast<u16x8*>(kc + static_cast<size_t>(pos) * D + d0) = nk;
@@ -775,14 +881,16 @@ hipError_t launch_attention_main(const AttnParams& p, int head_dim, hipStream_t 
   return hipGetLastError();
 }
 
-hipError_t launch_attention_merge(const AttnParams& p, int head_dim, hipStream_t stream) {
+hipError_t launch_attention_merge(const AttnParams& p, int head_dim, hipStream_t stream,
+                                  hipEvent_t stop) {
   if (p.n_blocks == 1) return hipSuccess;  // every unit is finished in place
   const int rows_per_block = kWaves / p.merge_waves;
   const dim3 cgrid((p.B * p.h + rows_per_block - 1) / rows_per_block);
-  if (head_dim == 64)
-    hipLaunchKernelGGL(combine_kernel<64>, cgrid, dim3(kThreads), 0, stream, p);
+  auto kernel = head_dim == 64 ? combine_kernel<64> : combine_kernel<128>;
+  if (stop)
+    hipExtLaunchKernelGGL(kernel, cgrid, dim3(kThreads), 0, stream, nullptr, stop, 0, p);
   else
-    hipLaunchKernelGGL(combine_kernel<128>, cgrid, dim3(kThreads), 0, stream, p);
+    hipLaunchKernelGGL(kernel, cgrid, dim3(kThreads), 0, stream, p);
   return hipGetLastError();
 }
 
@@ -823,11 +931,22 @@ int resident_workgroups(int head_dim) {
   return v;
 }
 
-hipError_t launch_rope(const RopeParams& p, hipStream_t stream) {
-  const int items = (p.l * p.h + p.n_kv) * (p.dims / 16);
-  if (items == 0 || p.B == 0) return hipSuccess;
-  const dim3 grid((items + kRopeThreads - 1) / kRopeThreads, p.B);
-  hipLaunchKernelGGL(rope_kernel, grid, dim3(kRopeThreads), 0, stream, p);
+hipError_t launch_rope_table(const RopeTableParams& p, hipStream_t stream) {
+  const int items = p.B * p.half;
+  if (items == 0) return hipSuccess;
+  hipLaunchKernelGGL(rope_table_kernel, dim3((items + kRopeThreads - 1) / kRopeThreads),
+                     dim3(kRopeThreads), 0, stream, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_cache_rows(const CacheRowsParams& p, int head_dim, hipStream_t stream) {
+  const size_t blocks = static_cast<size_t>(p.kv_count) * p.B * (p.S / kTile);
+  if (blocks == 0) return hipSuccess;
+  const dim3 grid(static_cast<unsigned>(blocks));
+  if (head_dim == 64)
+    hipLaunchKernelGGL(cache_rows_kernel<64>, grid, dim3(kRowsThreads), 0, stream, p);
+  else
+    hipLaunchKernelGGL(cache_rows_kernel<128>, grid, dim3(kRowsThreads), 0, stream, p);
   return hipGetLastError();
 }
 

@@ -256,6 +256,13 @@ Plan plan(const mlkv_map* map, int layer, int batch, int max_len, int head_dim) 
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
+// Workspace bytes of the rotary table of mlkv_decode_step_rope: (cos, sin)
+// in double for each sequence and channel pair.
+size_t rope_table_bytes(int batch, int rotary_dims) {
+  if (rotary_dims <= 0) return 0;
+  return align_up(static_cast<size_t>(batch) * (rotary_dims / 2) * 2 * sizeof(double), 256);
+}
+
 // Plans that schedule runs inside the kernel keep per-sequence tables in LDS,
 // which bounds the batch; direct plans (a workgroup per unit) have no bound.
 mlkv_status check_plan_batch(const Plan& pl, int batch) {
@@ -328,7 +335,8 @@ mlkv_status attention_impl(int layer, const void* q, const mlkv_cache* cache, co
                            const int32_t* lens, int len_offset, void* out, mlkv_out_dtype dt,
                            int max_len_hint, void* ws, size_t ws_bytes, hipStream_t stream,
                            int plan_mode = 0, const uint16_t* k_new = nullptr,
-                           const uint16_t* v_new = nullptr) {
+                           const uint16_t* v_new = nullptr, const double* rope_cs = nullptr,
+                           int rope_half = 0) {
   const int B = cache->batch, S = cache->capacity, D = cache->head_dim;
   const int max_len = max_len_hint <= 0 ? S : max_len_hint;
   const Plan pl = plan(map, layer, B, max_len, D);
@@ -383,21 +391,27 @@ mlkv_status attention_impl(int layer, const void* q, const mlkv_cache* cache, co
     p.own_begin = map->own_begin[layer];
     p.own_count = map->own_count[layer];
   }
+  p.rope_cs = rope_half > 0 ? rope_cs : nullptr;
+  p.rope_half = rope_half > 0 ? rope_half : 0;
   hipError_t err = hipSuccess;
   Profile& prof = g_profile;
   const bool timed = prof.on && prof.used < static_cast<int>(prof.start.size());
-  err = mlkv::launch_attention_main(p, D, stream, timed ? prof.start[prof.used] : nullptr,
-                                               timed ? prof.stop[prof.used] : nullptr);
-  if (err == hipSuccess && timed) ++prof.used;
+  // A layer's attention is one launch, or two when split runs are merged by
+  // the separate merge kernel: the timing pair then brackets both.
   const bool single_runs = pl.n_blocks == B * map->kv_count[layer];
-  if (err == hipSuccess && !pl.fused && !single_runs) err = mlkv::launch_attention_merge(p, D, stream);
+  const bool merge_kernel = !pl.fused && !single_runs && pl.n_blocks > 1;
+  hipEvent_t t0 = timed ? prof.start[prof.used] : nullptr;
+  hipEvent_t t1 = timed ? prof.stop[prof.used] : nullptr;
+  err = mlkv::launch_attention_main(p, D, stream, t0, merge_kernel ? nullptr : t1);
+  if (err == hipSuccess && merge_kernel) err = mlkv::launch_attention_merge(p, D, stream, t1);
+  if (err == hipSuccess && timed) ++prof.used;
   if (err != hipSuccess) return fail(MLKV_ERR_HIP, "attention launch: %s", hipGetErrorString(err));
   return MLKV_OK;
 }
 
 mlkv_status append_impl(int layer, const mlkv_map* map, const mlkv_cache* cache, const void* k_new,
                         const void* v_new, int row_stride, const int32_t* positions,
-                        hipStream_t stream) {
+                        hipStream_t stream, const double* rope_cs = nullptr, int rope_half = 0) {
   const int owned = map->own_count[layer];
   if (owned == 0) return MLKV_OK;
   mlkv::AppendParams p{};
@@ -410,6 +424,8 @@ mlkv_status append_impl(int layer, const mlkv_map* map, const mlkv_cache* cache,
   p.S = cache->capacity;
   p.kv_begin = map->own_begin[layer];
   p.row_stride = row_stride;
+  p.rope_cs = rope_half > 0 ? rope_cs : nullptr;
+  p.rope_half = rope_half > 0 ? rope_half : 0;
   const hipError_t err = mlkv::launch_append(p, cache->head_dim, owned, stream);
   if (err != hipSuccess) return fail(MLKV_ERR_HIP, "append launch: %s", hipGetErrorString(err));
   return MLKV_OK;
@@ -640,6 +656,15 @@ size_t mlkv_workspace_bytes(const mlkv_map* map, int batch, int capacity, int he
   return best;
 }
 
+size_t mlkv_workspace_bytes_rope(const mlkv_map* map, int batch, int capacity, int head_dim,
+                                 int rotary_dims) {
+  if (!map || batch <= 0 || capacity <= 0 || (head_dim != 64 && head_dim != 128) ||
+      rotary_dims < 0 || rotary_dims > head_dim || rotary_dims % 16 != 0)
+    return 0;
+  return rope_table_bytes(batch, rotary_dims) +
+         mlkv_workspace_bytes(map, batch, capacity, head_dim);
+}
+
 mlkv_status mlkv_workspace_init(void* workspace, size_t workspace_bytes, hipStream_t stream) {
   if (!workspace && workspace_bytes > 0) return fail(MLKV_ERR_INVALID_ARG, "workspace is NULL");
   if (workspace_bytes == 0) return ok();
@@ -665,6 +690,17 @@ mlkv_status mlkv_plan(const mlkv_map* map, int layer, int batch, int capacity, i
   return ok();
 }
 
+int mlkv_plan_merge_kernel(const mlkv_map* map, int layer, int batch, int capacity, int head_dim,
+                           int max_len) {
+  if (!map || layer < 0 || layer >= map->l || batch <= 0 || capacity <= 0 ||
+      (head_dim != 64 && head_dim != 128) || max_len > capacity)
+    return -1;
+  if (max_len <= 0) max_len = capacity;
+  const Plan pl = plan(map, layer, batch, max_len, head_dim);
+  const bool single_runs = pl.n_blocks == batch * map->kv_count[layer];
+  return !pl.fused && !single_runs && pl.n_blocks > 1 ? 1 : 0;
+}
+
 mlkv_status mlkv_cache_append(int layer, const mlkv_map* map, const mlkv_cache* cache,
                               const void* k_new, const void* v_new, int new_row_stride,
                               const int32_t* positions, hipStream_t stream) {
@@ -686,6 +722,57 @@ mlkv_status mlkv_cache_append(int layer, const mlkv_map* map, const mlkv_cache* 
       MLKV_OK)
     return s;
   return ok();
+}
+
+namespace {
+
+mlkv_status cache_rows(const mlkv_cache* cache, int kv_begin, int kv_count, const void* k_rows,
+                       const void* v_rows, int to_cache, hipStream_t stream) {
+  if (!cache) return fail(MLKV_ERR_INVALID_ARG, "cache is NULL");
+  if (!cache->k || !cache->v) return fail(MLKV_ERR_INVALID_ARG, "cache planes must be non-NULL");
+  if (!aligned16(cache->k) || !aligned16(cache->v))
+    return fail(MLKV_ERR_ALIGNMENT, "cache planes must be 16-byte aligned");
+  if (cache->batch <= 0 || cache->capacity <= 0 || cache->n_kv <= 0)
+    return fail(MLKV_ERR_INVALID_ARG, "cache n_kv, batch and capacity must be positive");
+  if (cache->capacity % kTileTokens != 0)
+    return fail(MLKV_ERR_CAPACITY, "cache capacity %d is not a multiple of 32", cache->capacity);
+  if (cache->head_dim != 64 && cache->head_dim != 128)
+    return fail(MLKV_ERR_UNSUPPORTED, "head_dim %d not supported (64 or 128)", cache->head_dim);
+  if (kv_begin < 0 || kv_count < 0 || kv_begin + static_cast<long>(kv_count) > cache->n_kv)
+    return fail(MLKV_ERR_INVALID_ARG, "KV heads [%d, %d + %d) outside [0, %d)", kv_begin, kv_begin,
+                kv_count, cache->n_kv);
+  if (kv_count == 0) return ok();
+  if (!k_rows || !v_rows) return fail(MLKV_ERR_INVALID_ARG, "k_rows and v_rows must be non-NULL");
+  if (!aligned16(k_rows) || !aligned16(v_rows))
+    return fail(MLKV_ERR_ALIGNMENT, "k_rows and v_rows must be 16-byte aligned");
+  const double blocks = static_cast<double>(kv_count) * cache->batch * (cache->capacity / 32);
+  if (blocks >= 2147483647.0)
+    return fail(MLKV_ERR_CAPACITY, "more than 2^31 - 1 blocks of 32 tokens in one call");
+  mlkv::CacheRowsParams p{};
+  p.k_plane = static_cast<uint16_t*>(cache->k);
+  p.v_plane = static_cast<uint16_t*>(cache->v);
+  p.k_rows = static_cast<uint16_t*>(const_cast<void*>(k_rows));
+  p.v_rows = static_cast<uint16_t*>(const_cast<void*>(v_rows));
+  p.B = cache->batch;
+  p.S = cache->capacity;
+  p.kv_begin = kv_begin;
+  p.kv_count = kv_count;
+  p.to_cache = to_cache;
+  const hipError_t err = mlkv::launch_cache_rows(p, cache->head_dim, stream);
+  if (err != hipSuccess) return fail(MLKV_ERR_HIP, "cache rows launch: %s", hipGetErrorString(err));
+  return ok();
+}
+
+}  // namespace
+
+mlkv_status mlkv_cache_write_rows(const mlkv_cache* cache, int kv_begin, int kv_count,
+                                  const void* k_rows, const void* v_rows, hipStream_t stream) {
+  return cache_rows(cache, kv_begin, kv_count, k_rows, v_rows, 1, stream);
+}
+
+mlkv_status mlkv_cache_read_rows(const mlkv_cache* cache, int kv_begin, int kv_count,
+                                 void* k_rows, void* v_rows, hipStream_t stream) {
+  return cache_rows(cache, kv_begin, kv_count, k_rows, v_rows, 0, stream);
 }
 
 mlkv_status mlkv_decode_attention(int layer, const void* q, const mlkv_cache* cache,
@@ -762,7 +849,8 @@ mlkv_status decode_step_launch(const void* q_all, const void* k_new_all, const v
                                const mlkv_cache* cache, const mlkv_map* map,
                                const int32_t* ctx_lens, void* out_all, mlkv_out_dtype out_dtype,
                                int max_len_hint, void* workspace, size_t workspace_bytes,
-                               hipStream_t stream) {
+                               hipStream_t stream, const double* rope_cs = nullptr,
+                               int rope_half = 0) {
   mlkv_status s;
   const int B = cache->batch, h = map->h, D = cache->head_dim, n_kv = map->n_kv;
   const size_t layer_elems = static_cast<size_t>(B) * h * D;
@@ -778,8 +866,8 @@ mlkv_status decode_step_launch(const void* q_all, const void* k_new_all, const v
                                   map->kv_begin[n] + map->kv_count[n];
     if (map->own_count[n] > 0 && !fused_append) {
       const size_t col = static_cast<size_t>(map->own_begin[n]) * D;
-      if ((s = append_impl(n, map, cache, k_new + col, v_new + col, n_kv * D, ctx_lens, stream)) !=
-          MLKV_OK)
+      if ((s = append_impl(n, map, cache, k_new + col, v_new + col, n_kv * D, ctx_lens, stream,
+                           rope_cs, rope_half)) != MLKV_OK)
         return s;
     }
     const void* q = static_cast<const uint16_t*>(q_all) + layer_elems * n;
@@ -790,7 +878,7 @@ mlkv_status decode_step_launch(const void* q_all, const void* k_new_all, const v
     const int mode = key == planned_key ? 2 : 1;
     if ((s = attention_impl(n, q, cache, map, ctx_lens, 1, out, out_dtype, max_len_hint, workspace,
                             workspace_bytes, stream, mode, fused_append ? k_new : nullptr,
-                            fused_append ? v_new : nullptr)) != MLKV_OK)
+                            fused_append ? v_new : nullptr, rope_cs, rope_half)) != MLKV_OK)
       return s;
     planned_key = key;
   }
@@ -811,7 +899,7 @@ mlkv_status mlkv_decode_step(const void* q_all, const void* k_new_all, const voi
                             max_len_hint, workspace, workspace_bytes, stream);
 }
 
-mlkv_status mlkv_decode_step_rope(void* q_all, void* k_new_all, const void* v_new_all,
+mlkv_status mlkv_decode_step_rope(const void* q_all, const void* k_new_all, const void* v_new_all,
                                   const mlkv_cache* cache, const mlkv_map* map,
                                   const int32_t* ctx_lens, int rotary_dims, double rotary_base,
                                   void* out_all, mlkv_out_dtype out_dtype, int max_len_hint,
@@ -824,26 +912,32 @@ mlkv_status mlkv_decode_step_rope(void* q_all, void* k_new_all, const void* v_ne
                 rotary_dims);
   if (!(rotary_base > 0.0) || !std::isfinite(rotary_base))
     return fail(MLKV_ERR_INVALID_ARG, "rotary_base must be positive and finite");
+  // The rotary table heads the workspace; the decode workspace follows it.
+  const size_t table = rope_table_bytes(cache->batch, rotary_dims);
+  if (table > 0 && (!workspace || workspace_bytes < table))
+    return fail(MLKV_ERR_WORKSPACE, "workspace of at least %zu bytes needed for the rotary table, "
+                "%zu given", table, workspace ? workspace_bytes : 0);
+  if (table > 0 && !aligned16(workspace))
+    return fail(MLKV_ERR_ALIGNMENT, "workspace not 16-byte aligned");
+  void* ws = table > 0 ? static_cast<char*>(workspace) + table : workspace;
+  const size_t ws_bytes = table > 0 ? workspace_bytes - table : workspace_bytes;
   if ((s = decode_step_check(q_all, k_new_all, v_new_all, cache, map, ctx_lens, out_all, out_dtype,
-                             max_len_hint, workspace, workspace_bytes, stream)) != MLKV_OK)
+                             max_len_hint, ws, ws_bytes, stream)) != MLKV_OK)
     return s;
-  if (rotary_dims > 0) {
-    mlkv::RopeParams p{};
-    p.q = static_cast<uint16_t*>(q_all);
-    p.k = static_cast<uint16_t*>(k_new_all);
+  const int half = rotary_dims / 2;
+  double* cs = static_cast<double*>(workspace);
+  if (half > 0) {
+    mlkv::RopeTableParams p{};
     p.pos = ctx_lens;
-    p.l = map->l;
+    p.cs = cs;
     p.B = cache->batch;
-    p.h = map->h;
-    p.n_kv = map->n_kv;
-    p.D = cache->head_dim;
-    p.dims = rotary_dims;
-    for (int j = 0; j < rotary_dims / 2; ++j) p.inv_freq[j] = std::pow(rotary_base, -2.0 * j / rotary_dims);
-    const hipError_t err = mlkv::launch_rope(p, stream);
-    if (err != hipSuccess) return fail(MLKV_ERR_HIP, "rotary launch: %s", hipGetErrorString(err));
+    p.half = half;
+    for (int j = 0; j < half; ++j) p.inv_freq[j] = std::pow(rotary_base, -2.0 * j / rotary_dims);
+    const hipError_t err = mlkv::launch_rope_table(p, stream);
+    if (err != hipSuccess) return fail(MLKV_ERR_HIP, "rotary table launch: %s", hipGetErrorString(err));
   }
   return decode_step_launch(q_all, k_new_all, v_new_all, cache, map, ctx_lens, out_all, out_dtype,
-                            max_len_hint, workspace, workspace_bytes, stream);
+                            max_len_hint, ws, ws_bytes, stream, half > 0 ? cs : nullptr, half);
 }
 
 mlkv_status mlkv_cache_append_rows(int layer, const mlkv_map* map, const mlkv_cache* cache,

@@ -22,3 +22,10 @@ def unpack_v(v_plane_flat: np.ndarray, n_kv: int, B: int, S: int, D: int) -> np.
 
 def unpack_k(k_plane_flat: np.ndarray, n_kv: int, B: int, S: int, D: int) -> np.ndarray:
     return np.ascontiguousarray(k_plane_flat).reshape(n_kv, B, S, D)
+
+
+def pack_v(v_rows: np.ndarray) -> np.ndarray:
+    """Logical value rows [..., S, D] -> the plane's blocked order [..., S/32, D, 32]."""
+    *lead, S, D = v_rows.shape
+    blk = v_rows.reshape(*lead, S // 32, 32, D)
+    return np.ascontiguousarray(np.swapaxes(blk, -1, -2))

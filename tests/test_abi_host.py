@@ -138,6 +138,19 @@ def test_entry_points_reject_bad_arguments():
     # with valid rotary arguments the step's own checks apply (workspace here)
     assert names[L.mlkv_decode_step_rope(0x30000, 0x30000, 0x30000, ctypes.byref(big), mp.handle,
                                          0x40000, 16, 1e4, 0x50000, 0, 0, None, 0, None)] == "MLKV_ERR_WORKSPACE"
+    # the rotary workspace is the decode workspace plus B * rd/2 (cos, sin)
+    # doubles rounded up to 256 bytes; invalid rotary sizes give 0
+    for rd in (16, 32, 64):
+        assert (mp.workspace_bytes(2, 64, 64, rd) ==
+                mp.workspace_bytes(2, 64, 64) + (2 * rd // 2 * 16 + 255) // 256 * 256)
+    assert mp.workspace_bytes(2, 64, 64, 8) == 0 and mp.workspace_bytes(2, 64, 64, 80) == 0
+    # cache row conversion: NULL rows, a head range outside the cache, misalignment
+    assert names[L.mlkv_cache_write_rows(ref, 0, 4, None, 0x30000, None)] == "MLKV_ERR_INVALID_ARG"
+    assert names[L.mlkv_cache_read_rows(ref, 3, 2, 0x30000, 0x30000, None)] == "MLKV_ERR_INVALID_ARG"
+    assert names[L.mlkv_cache_write_rows(ref, -1, 1, 0x30000, 0x30000, None)] == "MLKV_ERR_INVALID_ARG"
+    assert names[L.mlkv_cache_write_rows(ref, 0, 1, 0x30008, 0x30000, None)] == "MLKV_ERR_ALIGNMENT"
+    assert names[L.mlkv_cache_write_rows(None, 0, 1, 0x30000, 0x30000, None)] == "MLKV_ERR_INVALID_ARG"
+    assert names[L.mlkv_cache_write_rows(ref, 2, 0, None, None, None)] == "MLKV_OK"
     # group size above 16 query heads per KV head is reported as unsupported
     mq = mlkv.Map.uniform(2, 32, 2, 1)
     c2 = mlkv._Cache(0x10000, 0x20000, 2, 2, 64, 64)
@@ -234,12 +247,14 @@ def test_large_batch_plans_one_workgroup_per_unit(monkeypatch):
                                     F, S, 0x60000, 1 << 30, None)] == "MLKV_ERR_UNSUPPORTED"
 
 
-def test_layout_reference_matches_binding_packer():
+def test_layout_reference_pack_and_unpack_agree():
+    """The tests' two statements of the value-plane layout (the index formula
+    and the block transpose) agree with each other."""
     rng = np.random.default_rng(0)
     n_kv, B, S, D = 2, 3, 64, 64
     rows = rng.integers(0, 65535, size=(n_kv, B, S, D), dtype=np.uint16)
     import layout_ref
-    packed = mlkv.pack_value_rows(rows)
+    packed = layout_ref.pack_v(rows)
     assert np.array_equal(layout_ref.unpack_v(packed, n_kv, B, S, D), rows)
     for _ in range(100):
         kv, b, t, d = rng.integers(n_kv), rng.integers(B), rng.integers(S), rng.integers(D)
@@ -251,8 +266,9 @@ def test_binding_fails_loudly_without_the_library(tmp_path):
     import subprocess
     import sys
     code = ("import paper_2406_09297_amd as m\n"
+            f"m.LIB_PATH = {str(tmp_path / 'absent.so')!r}\n"
             "try:\n    m.lib()\nexcept ImportError as e:\n    print('raised', e)\n")
-    env = dict(os.environ, MLKV_LIBRARY=str(tmp_path / "absent.so"))
+    env = dict(os.environ)
     r = subprocess.run([sys.executable, "-c", code], env=env, capture_output=True, text=True,
                        cwd=os.path.dirname(os.path.dirname(os.path.abspath(__file__))), timeout=120)
     assert "raised" in r.stdout and "no fallback" in r.stdout, r.stdout + r.stderr

@@ -84,6 +84,35 @@ def test_append_bit_exact(wname, kw):
     assert np.array_equal(v_gpu, v_ref)
 
 
+@pytest.mark.parametrize("n_kv,B,S,D", [(3, 2, 96, 64), (2, 3, 64, 128)])
+def test_cache_rows_through_the_library(n_kv, B, S, D):
+    """mlkv_cache_write_rows stores plain row-major rows in the documented
+    plane layout (checked against the tests' own statement of it), touching
+    only the named KV heads; mlkv_cache_read_rows returns them unchanged."""
+    import layout_ref
+
+    say(f"cache rows n_kv={n_kv} B={B} S={S} D={D}")
+    rng = np.random.default_rng(n_kv * 1000 + D)
+    rows_k = rng.integers(0, 0x7F00, size=(n_kv, B, S, D), dtype=np.uint16)
+    rows_v = rng.integers(0, 0x7F00, size=(n_kv, B, S, D), dtype=np.uint16)
+    cache = mlkv.Cache.empty(n_kv, B, S, D)
+    cache.k.fill_(float("nan"))
+    cache.v.fill_(float("nan"))
+    lo = 1  # heads 1.. written; head 0 stays as filled
+    cache.write_rows(mlkv.bf16_tensor(rows_k[lo:], "cuda"), mlkv.bf16_tensor(rows_v[lo:], "cuda"), lo)
+    torch.cuda.synchronize()
+    k_plane = mlkv.bf16_bits(cache.k).reshape(n_kv, B, S, D)
+    v_plane = mlkv.bf16_bits(cache.v).reshape(n_kv, B, S // 32, D, 32)
+    nan = mlkv.bf16_bits(torch.tensor([float("nan")], dtype=torch.bfloat16))[0]
+    assert np.all(k_plane[:lo] == nan) and np.all(v_plane[:lo] == nan), "other heads written"
+    assert np.array_equal(k_plane[lo:], rows_k[lo:])
+    assert np.array_equal(v_plane[lo:], layout_ref.pack_v(rows_v[lo:]))
+    k_back, v_back = cache.read_rows(lo)
+    torch.cuda.synchronize()
+    assert np.array_equal(mlkv.bf16_bits(k_back), rows_k[lo:])
+    assert np.array_equal(mlkv.bf16_bits(v_back), rows_v[lo:])
+
+
 # ----------------------------------------------------------- one layer ------
 
 @pytest.mark.parametrize("wname,kw,layers", [
@@ -137,6 +166,38 @@ def test_length_sweep_across_tile_boundaries(D, m, g):
                 ref = oracle.decode_attention(n, dw.host["q"][n], dw.host["k_cache"],
                                               dw.host["v_cache"], dw.kv_of, lens)
                 check_close(out.cpu().numpy(), ref, f"sweep D{D} g{g} L{n} wg{wg} {comb} {wide} {qk}")
+
+
+@pytest.mark.parametrize("workgroups", ["", "600", "1500"])
+def test_schedule_path_with_many_short_runs(workgroups):
+    """The in-kernel schedule (decode_attention, and the first layer of a
+    step) with short ragged sequences, so that many runs have fewer tiles
+    than the workgroup has waves: waves with no tile of their own reach the
+    LDS merge early while their siblings still read the schedule tables,
+    which share that LDS (the schedule is read into registers and a barrier
+    separates the two)."""
+    rng = np.random.default_rng(31)
+    lens = rng.integers(1, 130, size=300).astype(np.int32)
+    lens[:4] = [1, 32, 33, 96]
+    w = _sweep_workload(64, 4, 1, lens, h=12, l=4, seed=131)
+    dw = DeviceWorkload(w)
+    lens_d = torch.from_numpy(lens).cuda()
+    with plan_env(workgroups=workgroups):
+        for n in (0, 2):
+            say(f"short runs workgroups={workgroups or 'auto'} layer={n}")
+            out = torch.empty((w.B, w.h, w.D), dtype=torch.float32, device="cuda")
+            mlkv.decode_attention(n, dw.q[n], dw.cache, dw.map, lens_d, out, ws=dw.ws)
+            torch.cuda.synchronize()
+            ref = oracle.decode_attention(n, dw.host["q"][n], dw.host["k_cache"],
+                                          dw.host["v_cache"], dw.kv_of, lens)
+            check_close(out.cpu().numpy(), ref, f"short runs wg{workgroups} L{n}")
+        say(f"short runs workgroups={workgroups or 'auto'}: step")
+        _with_contexts(dw, lens - 1)
+        out = _run_step(dw).cpu().numpy()
+    k_gpu, v_gpu = dw.read_cache()
+    ref, k_ref, v_ref = _oracle_step(dw)
+    assert np.array_equal(k_gpu, k_ref) and np.array_equal(v_gpu, v_ref), "cache differs"
+    check_close(out, ref, f"short runs step wg{workgroups}")
 
 
 def test_split_count_invariance_and_determinism():
@@ -382,27 +443,33 @@ def test_step_owner_that_does_not_read_its_head():
 # ------------------------------------------------------ rotary embedding --
 
 def _check_rope_step(dw, rd, label, base=10000.0):
-    """The step with rotary embedding against the oracle: the newest token's
-    queries and keys are rotated in place bit for bit, the cache (rotated
-    keys) matches bit for bit, the outputs within tolerance."""
+    """The step with rotary embedding against the oracle: the cache (rotated
+    keys) matches bit for bit and the outputs within tolerance; the caller's
+    queries and new keys are left unchanged, so a second call on the same
+    buffers gives the same outputs and cache bit for bit."""
     w = dw.w
+    ws = mlkv.workspace(dw.map, w.B, dw.S, w.D, rotary_dims=rd)
+    q0, kn0 = dw.q.clone(), dw.k_new.clone()
     out = torch.empty((w.l, w.B, w.h, w.D), dtype=torch.float32, device="cuda")
-    mlkv.decode_step(dw.q, dw.k_new, dw.v_new, dw.cache, dw.map, dw.ctx, out, ws=dw.ws,
+    mlkv.decode_step(dw.q, dw.k_new, dw.v_new, dw.cache, dw.map, dw.ctx, out, ws=ws,
                      rotary_dims=rd, rotary_base=base)
     torch.cuda.synchronize()
-    out = out.cpu().numpy()
+    assert torch.equal(dw.q, q0) and torch.equal(dw.k_new, kn0), f"{label}: inputs written"
     k_gpu, v_gpu = dw.read_cache()
+    out2 = torch.full_like(out, float("nan"))
+    mlkv.decode_step(dw.q, dw.k_new, dw.v_new, dw.cache, dw.map, dw.ctx, out2, ws=ws,
+                     rotary_dims=rd, rotary_base=base)
+    torch.cuda.synchronize()
+    assert torch.equal(out, out2), f"{label}: a repeated call differs"
+    k2, v2 = dw.read_cache()
+    assert np.array_equal(k2, k_gpu) and np.array_equal(v2, v_gpu), f"{label}: cache changed"
+    out = out.cpu().numpy()
     k, v = dw.host["k_cache"].copy(), dw.host["v_cache"].copy()
-    ref, q_rot, k_rot = oracle.decode_step_rope(dw.host["q"], k, v, dw.host["k_new"],
-                                                dw.host["v_new"], dw.kv_of, dw.owner_of,
-                                                dw.host["ctx"], rd, base, return_rotated=True)
-    q_gpu = mlkv.bf16_bits(dw.q)
-    k_new_gpu = mlkv.bf16_bits(dw.k_new).reshape(k_rot.shape)
-    bad = np.argwhere(q_gpu != q_rot)
-    assert bad.size == 0, f"{label}: rotated queries differ at {bad[:4].tolist()}"
-    bad = np.argwhere(k_new_gpu != k_rot)
-    assert bad.size == 0, f"{label}: rotated keys differ at {bad[:4].tolist()}"
-    assert np.array_equal(v_gpu, v) and np.array_equal(k_gpu, k), f"{label}: cache differs"
+    ref = oracle.decode_step_rope(dw.host["q"], k, v, dw.host["k_new"], dw.host["v_new"],
+                                  dw.kv_of, dw.owner_of, dw.host["ctx"], rd, base)
+    bad = np.argwhere(k_gpu != k)
+    assert bad.size == 0, f"{label}: cached (rotated) keys differ at {bad[:4].tolist()}"
+    assert np.array_equal(v_gpu, v), f"{label}: cached values differ"
     check_close(out, ref, label)
 
 
@@ -412,9 +479,9 @@ def _check_rope_step(dw, rd, label, base=10000.0):
     (64, 4, 1, 16, "", "valu"), (128, 2, 4, 64, "", "valu")])
 def test_step_rope_across_tile_boundaries(D, m, g, rd, wide, qk):
     """Rotary embedding of the newest token inside the step: its queries are
-    rotated as each layer loads them and its keys as the owner appends them,
-    at every offset of a 32-token tile; the cache (rotated keys) matches the
-    oracle bit for bit and the outputs within tolerance."""
+    rotated as each layer's attention loads them and its keys as the owner
+    appends them, at every offset of a 32-token tile; the cache (rotated keys)
+    matches the oracle bit for bit and the outputs within tolerance."""
     w = synth.Workload("rope_sweep", l=4, h=12, m=m, g=g, D=D, B=len(APPEND_CTX),
                        ctx=max(APPEND_CTX), seed=78)
     dw = _with_contexts(DeviceWorkload(w), APPEND_CTX)

@@ -31,6 +31,24 @@ mlkv = pytest.importorskip("paper_2406_09297_amd")
 
 MAX_REL = 1e-2
 MEAN_REL = 1e-2
+# Bars against the plain float64 form, in units of the storage error scale E
+# (storage_error_scale): mean |diff| <= 2.5 E and max |diff| <= 12 E.
+PLAIN_MEAN_E = 2.5
+PLAIN_MAX_E = 12.0
+U_BF16 = 2.0 ** -9  # unit roundoff of bf16 (8 significant bits, nearest even)
+
+
+def storage_error_scale(updates) -> float:
+    """Expected rms deviation of the final residual stream from the plain
+    float64 form caused by bf16 storage at the path's rounding points: each
+    rounding is a relative error uniform in [-u, u] (rms u/sqrt 3) that a
+    following matrix product carries into the update it feeds at the same
+    relative size.  The attention update a of a layer sits behind five
+    roundings (h1, q, k or v, the softmax weights, o), the MLP update m
+    behind two (h2, the GELU output); layers add independently:
+        E = u/sqrt(3) * sqrt(sum_n 5 rms(a_n)^2 + 2 rms(m_n)^2)."""
+    tot = sum(5.0 * float(np.mean(a * a)) + 2.0 * float(np.mean(m * m)) for a, m in updates)
+    return U_BF16 / np.sqrt(3.0) * np.sqrt(tot)
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -88,12 +106,22 @@ def _run_case(l, h, D, d_ff, m, g, B, ctx, seed, rd=16, kv_of=None, owner_of=Non
     kr, vr = om._f64(kc), om._f64(vc)
     ref = om.decode_step_model(x0.astype(np.float64), weights, kv_of, owner_of, kr, vr, ctx, h, D,
                                rd)
+    # The plain float64 form (no bf16 storage; the form pinned against
+    # transformers' GPT-NeoX), with the storage error scale of this run.
+    updates = []
+    plain = om.decode_step_model(x0.astype(np.float64), weights, kv_of, owner_of, om._f64(kc),
+                                 om._f64(vc), ctx, h, D, rd, round_bf16=False, updates=updates)
+    E = storage_error_scale(updates)
     diff = np.abs(out - ref)
     scale = max(1.0, float(np.abs(ref).max()))
     mean_x = float(np.abs(ref).mean())
-    say(f"  {label}: max|d|={diff.max():.3e} mean|d|={diff.mean():.3e} max|x|={np.abs(ref).max():.3f} "
-        f"mean|x|={mean_x:.3f}")
+    dp = np.abs(out - plain)
+    say(f"  {label}: vs rounded form max|d|={diff.max():.3e} ({diff.max() / scale:.2e} of max|x|) "
+        f"mean|d|={diff.mean():.3e} ({diff.mean() / mean_x:.2e} of mean|x|); "
+        f"vs plain form max|d|={dp.max():.3e} ({dp.max() / E:.2f} E) mean|d|={dp.mean():.3e} "
+        f"({dp.mean() / E:.2f} E), E={E:.3e}; max|x|={np.abs(ref).max():.3f} mean|x|={mean_x:.3f}")
     assert np.all(np.isfinite(out))
+    assert dp.mean() <= PLAIN_MEAN_E * E and dp.max() <= PLAIN_MAX_E * E, f"{label}: vs plain form"
     assert diff.max() <= MAX_REL * scale and diff.mean() <= MEAN_REL * mean_x, label
     # cache: untouched slots bit-exact.  The rows appended by layer 0 come
     # from the step's input x: within one bf16 step of the oracle's.  Later
