@@ -162,8 +162,10 @@ size_t mlkv_workspace_bytes(const mlkv_map* map, int batch, int capacity, int he
 
 /* Zero-fill a workspace before its first use (a fill kernel enqueued on
  * `stream`, no memset, so it may be captured in a graph).  Every decode call
- * leaves the workspace's counters at zero again, so this is needed once per
- * allocation.  Calls that share one workspace must be ordered on one stream. */
+ * leaves the workspace's counters (its first 256 KiB, whatever the batch or
+ * map of the call) at zero again, so this is needed once per allocation, also
+ * when calls with different batches or maps share the workspace.  Calls that
+ * share one workspace must be ordered on one stream. */
 mlkv_status mlkv_workspace_init(void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*

@@ -157,6 +157,7 @@ struct Plan {
 };
 constexpr int kMinTiles = 4;
 constexpr int kMaxRunsPerUnit = 128;
+constexpr long kCounterSlots = 65536;  // arrival counters of a workspace (bounds the workgroups)
 constexpr int kFallbackResident = 768;  // 256 CUs x 3 when no device can be queried
 constexpr int kWorkgroupsPerCu = 2;
 
@@ -190,7 +191,7 @@ long workgroup_budget(int head_dim) {
     const long w = std::atol(env);
     if (w > 0) resident = w;
   }
-  return resident;
+  return resident < kCounterSlots ? resident : kCounterSlots;
 }
 
 Plan plan(const mlkv_map* map, int layer, int batch, int max_len, int head_dim) {
@@ -273,11 +274,16 @@ mlkv_status check_plan_batch(const Plan& pl, int batch) {
 }
 
 // Workspace layout of one call (nothing when one workgroup does all):
-//   counters  int32 [batch * h]  finished runs per unit, zero between calls
+//   counters  int32 [kCounterSlots]  finished runs per unit, zero between calls
 //   runs      int32 [batch]                          (256-byte aligned blocks)
 //   plan      32-byte run items [n_blocks]            (used by mlkv_decode_step)
 //   part_acc  fp32  [batch * h * max_parts][head_dim]
 //   part_ml   fp32  [batch * h * max_parts][2]
+// The counters are the only state a call leaves for the next one (all zero),
+// so their region has the same place and size in every call's layout: calls
+// with different batches or maps on one workspace never write anything else
+// there.  A split plan has fewer units than workgroups and at most
+// kCounterSlots workgroups, so every unit has its slot.
 constexpr size_t kRunItemBytes = 32;
 
 struct WsLayout {
@@ -289,7 +295,7 @@ WsLayout ws_layout(int batch, int h, int head_dim, const Plan& pl) {
   if (pl.n_blocks <= 1 || pl.direct) return w;
   const size_t rows = static_cast<size_t>(batch) * h * pl.max_parts;
   w.counters = 0;
-  w.runs = align_up(static_cast<size_t>(batch) * h * sizeof(int32_t), 256);
+  w.runs = static_cast<size_t>(kCounterSlots) * sizeof(int32_t);
   w.plan = w.runs + align_up(static_cast<size_t>(batch) * sizeof(int32_t), 256);
   w.acc = w.plan + align_up(static_cast<size_t>(pl.n_blocks) * kRunItemBytes, 256);
   w.ml = w.acc + align_up(rows * head_dim * sizeof(float), 256);

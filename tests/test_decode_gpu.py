@@ -379,6 +379,33 @@ def test_full_size_step_twice_on_one_workspace(merge):
     check_close(out, ref, f"step twice merge={merge or 'auto'}")
 
 
+def test_one_workspace_shared_by_steps_of_different_batches():
+    """A workspace sized for the largest of several steps serves them in
+    turn: a large batch, a smaller one with another map, then the large one
+    again.  The arrival counters keep one place in every call's layout, so
+    the smaller step's run list and partials never land where the larger
+    step's counters are (each step is checked against the oracle)."""
+    big = synth.Workload("ws_big", l=12, h=12, m=4, g=1, D=64, B=96, ctx_range=(200, 2000),
+                         seed=0x5C1)
+    small = synth.Workload("ws_small", l=4, h=12, m=2, g=3, D=64, B=9, ctx_range=(1, 300),
+                           seed=0x5C2)
+    need = 0
+    for w in (big, small):
+        mp = mlkv.Map.uniform(w.l, w.h, w.m, w.g)
+        need = max(need, mp.workspace_bytes(w.B, w.ctx_range[1] + 64, w.D))
+    ws = torch.empty(need, dtype=torch.uint8, device="cuda")
+    mlkv.lib().mlkv_workspace_init(ws.data_ptr(), need, torch.cuda.current_stream().cuda_stream)
+    for w in (big, small, big):
+        say(f"shared workspace {w.name} B={w.B}")
+        dw = DeviceWorkload(w)
+        dw.ws = ws
+        out = _run_step(dw).cpu().numpy()
+        k_gpu, v_gpu = dw.read_cache()
+        ref, k_ref, v_ref = _oracle_step(dw)
+        assert np.array_equal(k_gpu, k_ref) and np.array_equal(v_gpu, v_ref), "cache differs"
+        check_close(out, ref, f"shared workspace {w.name}")
+
+
 # ---------------------------------------------------- fused append in step --
 
 def _with_contexts(dw, ctx):

@@ -1,18 +1,21 @@
 """GPU parity of the model-level decode step (GPT-NeoX layers around the MLKV
-attention, mlkv_model_decode_step) against the float64 model oracle with the
-same bf16 rounding points (oracle/model.py).
+attention, mlkv_model_decode_step) against the float64 model oracle
+(oracle/model.py) in both its forms: the plain float64 form (the one pinned
+against transformers' GPT-NeoX), with a bar derived from bf16 storage at the
+path's rounding points (storage_error_scale), and the form that rounds to
+bf16 at those same points, with a tighter regression bar.
 
-Tolerance.  The attention kernels round the softmax weights to bf16 before
+Tolerance of the rounded form.  The attention kernels round the softmax weights to bf16 before
 the value product (relative error up to 2^-9 per weight, the decode path's
 documented arithmetic) where the oracle keeps them exact, so each layer's
 attention output differs from the oracle's by up to about one bf16 step in
 many elements; through W_o that adds a perturbation of order 2^-9 |a| to the
-residual stream per layer, and over the layers these add up (the GEMMs' fp32
-accumulation, which only occasionally flips a stored bf16 value, is far
-smaller).  Bars: max |diff| <= 1e-2 * max(1, max |x|) and mean |diff| <=
-1e-2 * mean |x| after the last layer; a cache row appended by layer 0
+residual stream per layer, and over the layers these add up; the fp32
+products also flip some stored bf16 values against the oracle's float64 ones.
+Bars: max |diff| <= 5e-3 * max(1, max |x|) and mean |diff| <= 5e-3 * mean |x|
+after the last layer; a cache row appended by layer 0
 (computed from the step's input, before any attention) within one bf16 step
-of the oracle's, later owners' rows within the same bar as the output.
+of the oracle's, later owners' rows within 1e-2 * max(1, max |row|).
 """
 import numpy as np
 import pytest
@@ -29,12 +32,19 @@ pytestmark = pytest.mark.gpu
 
 mlkv = pytest.importorskip("paper_2406_09297_amd")
 
-MAX_REL = 1e-2
-MEAN_REL = 1e-2
+# Regression bars against the form with the same bf16 storage points:
+# 0.5 % of max |x| and of mean |x| (measured up to 0.24 % after 12 layers).
+MAX_REL = 5e-3
+MEAN_REL = 5e-3
+ROW_REL = 1e-2  # later owners' appended rows (see above)
 # Bars against the plain float64 form, in units of the storage error scale E
-# (storage_error_scale): mean |diff| <= 2.5 E and max |diff| <= 12 E.
+# (storage_error_scale): mean |diff| <= 2.5 E (measured 0.7 - 1.5 E; the
+# model counts each rounding once, and errors carried through later layers'
+# layer norms add to it); max |diff| <= 13 E, the largest of the ~B*d
+# roughly normal deviations (about 4.2 sigma for 6144 of them) at that mean
+# bar (sigma = 1.25 mean): 4.2 * 1.25 * 2.5 E.  Measured max 3.5 - 8.2 E.
 PLAIN_MEAN_E = 2.5
-PLAIN_MAX_E = 12.0
+PLAIN_MAX_E = 13.0
 U_BF16 = 2.0 ** -9  # unit roundoff of bf16 (8 significant bits, nearest even)
 
 
@@ -141,7 +151,7 @@ def _run_case(l, h, D, d_ff, m, g, B, ctx, seed, rd=16, kv_of=None, owner_of=Non
                     f"{label}: layer-0 row of KV head {kv} off by more than one bf16 step"
                 assert np.mean(g64 != rr) <= 0.01, f"{label}: too many layer-0 values differ"
             else:
-                assert np.abs(g64 - rr).max() <= MAX_REL * max(1.0, float(np.abs(rr).max())), \
+                assert np.abs(g64 - rr).max() <= ROW_REL * max(1.0, float(np.abs(rr).max())), \
                     f"{label}: row of KV head {kv} outside the bar"
     return diff.max() / scale, diff.mean()
 
