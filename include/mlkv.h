@@ -229,6 +229,28 @@ mlkv_status mlkv_decode_step(const void* q_all, const void* k_new_all, const voi
                              hipStream_t stream);
 
 /*
+ * mlkv_decode_step for callers that cannot allocate device memory (code under
+ * HIP graph capture, serving loops or harnesses that forbid allocation): the
+ * same step, arguments and results, but with no workspace argument.  The
+ * split runs' counters, run list and partial results live in the library's
+ * own static device scratch of 16 MiB per device (allocated with the code
+ * object when the library is loaded on a device, held until the process
+ * ends); this call allocates nothing.  The first call on a device looks up
+ * the scratch's address and zero-fills it on `stream`.
+ * A step whose workspace need (that of mlkv_decode_step for these arguments;
+ * at most mlkv_workspace_bytes) exceeds 16 MiB is rejected with
+ * MLKV_ERR_WORKSPACE before anything is launched.  Every call on a device
+ * shares that device's scratch: calls that overlap on one device (on
+ * different streams, or from different threads without ordering) race and
+ * give wrong results; order them on one stream.
+ */
+mlkv_status mlkv_decode_step_noalloc(const void* q_all, const void* k_new_all,
+                                     const void* v_new_all, const mlkv_cache* cache,
+                                     const mlkv_map* map, const int32_t* ctx_lens, void* out_all,
+                                     mlkv_out_dtype out_dtype, int max_len_hint,
+                                     hipStream_t stream);
+
+/*
  * mlkv_decode_step with the rotary position embedding of the GPT-NeoX
  * architecture that the paper's Pythia models use (Section 4.2) applied to
  * the newest token inside the step: each attention launch rotates the

@@ -38,7 +38,7 @@ EXPORTS = [
     "mlkv_plan", "mlkv_plan_merge_kernel", "mlkv_workspace_init", "mlkv_profile_enable", "mlkv_profile_read",
     "mlkv_profile_durations", "mlkv_profile_disable", "mlkv_profile_launch_floor",
     "mlkv_profile_read_bandwidth",
-    "mlkv_decode_step_rope", "mlkv_workspace_bytes_rope",
+    "mlkv_decode_step_rope", "mlkv_workspace_bytes_rope", "mlkv_decode_step_noalloc",
     "mlkv_cache_append_rows", "mlkv_prefill_attention", "mlkv_prefill_step",
     "mlkv_cache_write_rows", "mlkv_cache_read_rows",
     "mlkv_model_create", "mlkv_model_destroy", "mlkv_model_workspace_bytes",
@@ -93,6 +93,7 @@ def lib():
             "mlkv_decode_step": ([P, P, P, P, P, P, P, I, I, P, Z, P], S),
             "mlkv_decode_step_rope": ([P, P, P, P, P, P, I, ctypes.c_double, P, I, I, P, Z, P], S),
             "mlkv_workspace_bytes_rope": ([P, I, I, I, I], Z),
+            "mlkv_decode_step_noalloc": ([P, P, P, P, P, P, P, I, I, P], S),
             "mlkv_cache_append_rows": ([I, P, P, P, P, I, I, P, P], S),
             "mlkv_cache_write_rows": ([P, I, I, P, P, P], S),
             "mlkv_cache_read_rows": ([P, I, I, P, P, P], S),

@@ -19,7 +19,7 @@ DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 
 
 def sources():
-    return [os.path.join(CSRC, f) for f in ("kernels.hip", "prefill.hip", "model.hip", "timing.hip", "mlkv.cpp")]
+    return [os.path.join(CSRC, f) for f in ("kernels.hip", "prefill.hip", "model.hip", "timing.hip", "scratch.hip", "mlkv.cpp")]
 
 
 def build(verbose: bool = False) -> str:

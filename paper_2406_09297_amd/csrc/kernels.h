@@ -209,6 +209,11 @@ int wide_waves();                      // waves per workgroup of the one-run-per
 int compute_units();                   // compute units of the current device (0: unknown)
 int default_waves();                   // waves per workgroup otherwise
 hipError_t launch_fill(uint32_t* dst, size_t n_words, uint32_t value, hipStream_t stream);
+// The library's static device scratch (scratch.hip): kScratchBytes per device.
+// Returns its device address on the current device, looked up (and zero
+// filled on `stream`) on the first call per device.
+constexpr size_t kScratchBytes = size_t(16) << 20;
+hipError_t scratch_for_current_device(hipStream_t stream, void** ptr);
 // An empty kernel bracketed by start/stop (launch-overhead reference).
 hipError_t launch_empty_timed(int workgroups, int threads, hipStream_t stream, hipEvent_t start,
                               hipEvent_t stop);

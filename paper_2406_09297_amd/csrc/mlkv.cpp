@@ -905,6 +905,34 @@ mlkv_status mlkv_decode_step(const void* q_all, const void* k_new_all, const voi
                             max_len_hint, workspace, workspace_bytes, stream);
 }
 
+mlkv_status mlkv_decode_step_noalloc(const void* q_all, const void* k_new_all,
+                                     const void* v_new_all, const mlkv_cache* cache,
+                                     const mlkv_map* map, const int32_t* ctx_lens, void* out_all,
+                                     mlkv_out_dtype out_dtype, int max_len_hint,
+                                     hipStream_t stream) {
+  // Every argument, and the step's need against the scratch's fixed size,
+  // is checked before the scratch is looked up or anything is launched.
+  // decode_step_check only compares pointers and sizes: the address below
+  // stands in for the scratch until its device address is known.
+  void* const stand_in = reinterpret_cast<void*>(uintptr_t(256));
+  mlkv_status s = decode_step_check(q_all, k_new_all, v_new_all, cache, map, ctx_lens, out_all,
+                                    out_dtype, max_len_hint, stand_in, mlkv::kScratchBytes,
+                                    stream);
+  if (s != MLKV_OK) {
+    if (s == MLKV_ERR_WORKSPACE)
+      return fail(MLKV_ERR_WORKSPACE, "this step needs more than the library's %zu-byte static "
+                  "scratch (%s); use mlkv_decode_step with a workspace",
+                  mlkv::kScratchBytes, g_last_error.c_str());
+    return s;
+  }
+  void* scratch = nullptr;
+  const hipError_t err = mlkv::scratch_for_current_device(stream, &scratch);
+  if (err != hipSuccess)
+    return fail(MLKV_ERR_HIP, "static scratch set-up: %s", hipGetErrorString(err));
+  return decode_step_launch(q_all, k_new_all, v_new_all, cache, map, ctx_lens, out_all, out_dtype,
+                            max_len_hint, scratch, mlkv::kScratchBytes, stream);
+}
+
 mlkv_status mlkv_decode_step_rope(const void* q_all, const void* k_new_all, const void* v_new_all,
                                   const mlkv_cache* cache, const mlkv_map* map,
                                   const int32_t* ctx_lens, int rotary_dims, double rotary_base,

@@ -38,6 +38,10 @@ hipError_t launch_stream_read_timed(const void*, size_t, uint32_t*, int, hipStre
                                     hipEvent_t) {
   return no_device();
 }
+hipError_t scratch_for_current_device(hipStream_t, void** ptr) {
+  *ptr = nullptr;
+  return no_device();
+}
 // The planner's device facts, fixed at MI355X's: 256 compute units, three
 // four-wave attention workgroups resident per compute unit.
 int max_batch() { return 2048; }

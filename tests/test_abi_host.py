@@ -293,3 +293,23 @@ def test_capacity_sizing_matches_the_cache_formula():
         budget = 280 * 10**9
         B = synth.capacity_batch(w, budget, S)
         assert B * per_seq <= budget < (B + 1) * per_seq
+
+
+def test_noalloc_step_rejects_a_need_above_its_static_scratch():
+    """mlkv_decode_step_noalloc refuses, before any HIP call, a step whose
+    split-run partials need more than its 16 MiB static scratch (here 511
+    sequences of 16384 positions, MLKV-4: 17.9 MB on two workgroups per
+    compute unit), naming the size; argument errors come first."""
+    mp = mlkv.Map.uniform(12, 12, 4, 1)
+    L = mlkv.lib()
+    names = mlkv.STATUS_NAMES
+    big = mlkv._Cache(0x10000, 0x20000, 4, 511, 16384, 64)
+    st = L.mlkv_decode_step_noalloc(0x30000, 0x30000, 0x30000, ctypes.byref(big), mp.handle,
+                                    0x40000, 0x50000, 0, 0, None)
+    assert names[st] == "MLKV_ERR_WORKSPACE"
+    assert "16777216-byte static scratch" in L.mlkv_last_error().decode()
+    ref, _keep = _fake_cache()
+    assert names[L.mlkv_decode_step_noalloc(None, 0x30000, 0x30000, ref, mp.handle, 0x40000,
+                                            0x50000, 0, 0, None)] == "MLKV_ERR_INVALID_ARG"
+    assert names[L.mlkv_decode_step_noalloc(0x30000, 0x30000, 0x30000, ref, mp.handle, 0x40000,
+                                            0x50004, 0, 0, None)] == "MLKV_ERR_ALIGNMENT"
