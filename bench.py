@@ -609,6 +609,8 @@ def main():
                     help="rotate the newest token's queries and keys inside the step "
                          "(GPT-NeoX rotary embedding; Pythia-160M: 16)")
     ap.add_argument("--rotary-base", type=float, default=10000.0)
+    ap.add_argument("--batch", type=int, default=0,
+                    help="model workload: batch size other than the workload's")
     ap.add_argument("--no-graph", action="store_true",
                     help="model workload: time eager launches only (default: graph replays)")
     ap.add_argument("--pmc-pass", action="store_true",
@@ -645,6 +647,10 @@ def main():
         elif w.sweep:
             m, g = w.sweep[-1]
             w = w.with_map(m, g)
+        if args.batch:
+            import dataclasses
+
+            w = dataclasses.replace(w, B=args.batch, name=f"{w.name}-b{args.batch}")
         run_model(args, w)
         return
     if args.map:

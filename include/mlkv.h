@@ -361,9 +361,9 @@ mlkv_status mlkv_prefill_step(const void* q_all, const void* k_new_all, const vo
  *   ctx_lens[b] + 1 positions of its KV head (as mlkv_decode_step)
  *   x += (o W_o + b_o) + (GELU(h2 W_1 + b_1) W_2 + b_2)  (exact GELU; the
  *   parallel residual)
- * Matrix products take bf16 operands and accumulate in fp32.  Up to 64
- * sequences, when the model holds packed weights (mlkv_model_create), they
- * run in two fused kernels per layer around the attention: layer norms, the
+ * Matrix products take bf16 operands and accumulate in fp32.  When the model
+ * holds packed weights (mlkv_model_create), they run, for any batch, in two
+ * fused kernels per layer around the attention: layer norms, the
  * q/k/v and fc1 products, bias, rotation and GELU in one; the output and fc2
  * products, biases and the residual in the other (weights packed into the
  * matrix cores' operand tiles).  Otherwise the products are library GEMMs (rocBLAS)
@@ -422,7 +422,7 @@ mlkv_status mlkv_model_decode_step(mlkv_model* model, float* x, const mlkv_cache
 /* ----------------------------------------------------------------------- */
 
 /* 1 when mlkv_model_decode_step runs `batch` sequences on the fused kernels
- * (packed weights, batch <= 64, MLKV_MODEL_GEMM not "library"), 0 when on
+ * (packed weights, MLKV_MODEL_GEMM not "library"), 0 when on
  * library GEMMs or for invalid arguments. */
 int mlkv_model_fused_path(const mlkv_model* model, int batch);
 

@@ -150,7 +150,7 @@ struct ResidualParams {  // x += (a32 + b_o) + (m32 + b_2)
 // element (n, k) sits at ((k % 32) / 8) * 128 + (n % 16) * 8 + k % 8, so lane
 // l of a wave reads elements 8 l .. 8 l + 7 (16 contiguous bytes).
 constexpr int kPackTile = 512;  // bf16 elements per packed tile
-constexpr int kFusedMaxBatch = 64;  // rows of a model step on the fused path
+constexpr int kFusedMaxBatch = 2048;  // rows of a model step on the fused path
 struct PackParams {  // source W[k_rows][n_cols] row-major -> tiles (nt0 + nt, kb0 + kb)
   const uint16_t* src;
   uint16_t* dst;

@@ -1169,8 +1169,8 @@ mlkv_status pack_weights(mlkv_model* m) {
   return MLKV_OK;
 }
 
-// The fused path serves batches up to kFusedMaxBatch rows (its products
-// re-read the weights once per 16 rows); MLKV_MODEL_GEMM=library forces the
+// The fused path serves every batch the decode path takes (its products
+// read the weights once per 16 rows); MLKV_MODEL_GEMM=library forces the
 // library GEMMs.
 bool use_fused(const mlkv_model* m, int B) {
   if (!m->packed || B > mlkv::kFusedMaxBatch) return false;

@@ -1,7 +1,7 @@
 // HIP kernels around attention in a GPT-NeoX decode step (the architecture of
 // the paper's Pythia models, Section 4.2), for CDNA4 (gfx950).
 //
-// Fused path (batches up to kFusedMaxBatch rows; two launches around each
+// Fused path (any batch, in tiles of 16 rows; two launches around each
 // layer's attention):
 //   pack_kernel         once, at model creation: weights into MFMA A-operand
 //                       tiles (layout in kernels.h)
@@ -11,7 +11,8 @@
 //                       token's position, exact GELU for fc1, bf16 rounding
 //   layer_out_kernel    x += (o W_o + b_o) + (f W_2 + b_2) on the matrix cores
 //
-// Library path (larger batches): plain library GEMMs between
+// Library path (d_ff not a multiple of 32, layer-norm vectors not 16-byte
+// aligned, or MLKV_MODEL_GEMM=library): plain library GEMMs between
 //   norm2_kernel        both layer norms of x (fp32) -> h1, h2 (bf16)
 //   qkv_epilogue_kernel bias, rotary embedding at the token's position and
 //                       bf16 rounding of the query (every head) and the

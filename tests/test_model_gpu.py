@@ -180,8 +180,9 @@ def test_model_step_full_size_benchmark_configuration():
 
 
 def test_model_step_library_gemm_path(monkeypatch):
-    """The library-GEMM path (forced here; taken by itself above 64 rows or
-    when d_ff is not a multiple of 32) against the same oracle."""
+    """The library-GEMM path (forced here; taken by itself when d_ff is not a
+    multiple of 32 or the layer-norm vectors are not 16-byte aligned) against
+    the same oracle."""
     monkeypatch.setenv("MLKV_MODEL_GEMM", "library")
     _run_case(12, 12, 64, 3072, 4, 1, B=4, ctx=[0, 33, 100, 257], seed=91, label="library MLKV-4",
               fused=False)
@@ -195,11 +196,16 @@ def test_model_step_batch_tiles_ragged():
     _run_case(3, 4, 64, 256, 3, 2, B=20, ctx=ctx, seed=96, label="B20")
 
 
-def test_model_step_large_batch_and_ragged_ff_take_the_library_path():
-    """65 rows (above the fused path's 64) and d_ff = 400 (not a multiple of
-    32, so no packed weights): both run on library GEMMs."""
-    ctx = [int(c) for c in np.random.default_rng(97).integers(0, 90, 65)]
-    _run_case(2, 4, 64, 256, 2, 1, B=65, ctx=ctx, seed=97, label="B65", fused=False)
+@pytest.mark.parametrize("B", [65, 130, 256])
+def test_model_step_serving_batches_on_the_fused_kernels(B):
+    """Batches above 64 rows (five, nine and sixteen 16-row tiles, the last
+    two ragged) run on the fused kernels too: no library GEMM."""
+    ctx = [int(c) for c in np.random.default_rng(97 + B).integers(0, 90, B)]
+    _run_case(2, 4, 64, 256, 2, 1, B=B, ctx=ctx, seed=97, label=f"B{B}", fused=True)
+
+
+def test_model_step_ragged_ff_takes_the_library_path():
+    """d_ff = 400 (not a multiple of 32, so no packed weights): library GEMMs."""
     _run_case(2, 4, 64, 400, 1, 1, B=3, ctx=[3, 40, 77], seed=98, label="ff400", fused=False)
 
 
