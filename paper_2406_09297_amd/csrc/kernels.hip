@@ -224,16 +224,13 @@ __device__ __forceinline__ void store_out4(const AttnParams& p, size_t row, int 
   }
 }
 
-__device__ __forceinline__ int wave_sum_int(int v) {
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
-  return v;
-}
+constexpr int kMaxWaves = 16;  // waves of the widest attention workgroup the schedule serves
 
 struct SchedShared {
   int q[kMaxBatch + 1];  // first run (workgroup) of each sequence, in runs of all its units
   int len[kMaxBatch];    // attended lengths
   int sched[3];          // run length R, run count N, sequence of this workgroup's run
+  int wsum[2][kMaxWaves][4];  // per-wave totals of the two scans
 };
 
 // Partial outputs the last run of a unit can stage in LDS to merge in place.
@@ -287,18 +284,54 @@ __device__ __forceinline__ long div_up64(long x, long y) {
   return q + (q * y < x ? 1 : 0);
 }
 
-// The run schedule every workgroup derives identically from the lengths
-// (computed by wave 0; the other waves wait at the barrier that follows):
-// tiles t_b = ceil(L_b / 32); run length R is the least of ceil(T / W), +1,
-// +2 (T = all tiles, W = workgroups) whose run count N(R) = n_groups *
-// sum_b ceil(t_b / R) fits W, else ceil(T / (W - U)) (U = non-empty units),
-// which always fits; never below min_tiles.  Leaves sm.q[b] = runs before
-// sequence b, sm.len, and sm.sched = {R, N, sequence of run g}.
-__device__ void schedule_wave0(const AttnParams& p, SchedShared& sm, int g) {
-  const int lane = threadIdx.x;
-  const int per = (p.B + 63) / 64;  // sequences per lane
-  const int b0 = lane * per;
+// Inclusive prefix sum over the 64 lanes of a wave: within each row of 16
+// lanes by shifted adds (1, 2, 4, 8), then the last lane of row 0 into row 1
+// and of row 2 into row 3, then the last lane of row 1 into rows 2 and 3
+// (row broadcasts).  Lane 63 ends with the wave's total.
+__device__ __forceinline__ int wave_incl_scan(int v) {
+  v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xf, 0xf, false);  // row_shr:1
+  v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xf, 0xf, false);  // row_shr:2
+  v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xf, 0xf, false);  // row_shr:4
+  v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xf, 0xf, false);  // row_shr:8
+  v += __builtin_amdgcn_update_dpp(0, v, 0x142, 0xa, 0xf, false);  // row_bcast:15
+  v += __builtin_amdgcn_update_dpp(0, v, 0x143, 0xc, 0xf, false);  // row_bcast:31
+  return v;
+}
+
+__device__ __forceinline__ int wave_total(int incl) { return __builtin_amdgcn_readlane(incl, 63); }
+
+// ceil(x / y) for 0 <= x < 2^21, 1 <= y < 2^21, ry = the float reciprocal of
+// y (uniform divisors take it once): an estimate off by at most one, then one
+// correction each way; the products stay below 2^23, so 24-bit multiplies
+// are exact.
+__device__ __forceinline__ int div_up_r(int x, int y, float ry) {
+  int q = static_cast<int>(static_cast<float>(x) * ry);
+  const int r = x - static_cast<int>(__umul24(q, y));  // in (-y, 2y)
+  q += r < 0 ? -1 : (r >= y ? 1 : 0);
+  const int r2 = r < 0 ? r + y : (r >= y ? r - y : r);  // x - q*y, now in [0, y)
+  return q + (r2 > 0 ? 1 : 0);
+}
+
+// The run schedule every workgroup derives identically from the lengths,
+// computed by all NT threads together (the sequences split evenly over them)
+// between two barriers: tiles t_b = ceil(L_b / 32); run length R is the
+// least of R0 = ceil(T / W), R0 + 1, R0 + 2 (T = all tiles, W = workgroups,
+// never below min_tiles) whose run count N(R) = n_groups * sum_b ceil(t_b /
+// R) fits W, else RF = ceil(T / (W - U)) (U = non-empty units), which always
+// fits.  One scan (per wave, then across the waves' totals) gives T and U; a
+// second scans the four candidates' per-thread run counts at once, so each
+// thread's first run under the chosen R is its prefix less its own count.
+// Leaves sm.q[b] = runs before sequence b, sm.len, and sm.sched = {R, N,
+// sequence of run g} (-1 if no sequence holds run g); ends with a barrier.
+template <int NT>
+__device__ void schedule(const AttnParams& p, SchedShared& sm, int g) {
+  constexpr int NW = NT / 64;
+  static_assert(NW <= kMaxWaves, "schedule: too many waves");
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int per = (p.B + NT - 1) / NT;  // sequences per thread
+  const int b0 = tid * per;
   const int b1 = b0 + per < p.B ? b0 + per : p.B;
+  if (tid == 0) sm.sched[2] = -1;
   int tot = 0, nonempty = 0;
   for (int b = b0; b < b1; ++b) {
     const int L = attended_len(p, b);
@@ -307,55 +340,82 @@ __device__ void schedule_wave0(const AttnParams& p, SchedShared& sm, int g) {
     tot += t;
     nonempty += t > 0 ? 1 : 0;
   }
-  tot = wave_sum_int(tot);
-  nonempty = wave_sum_int(nonempty);
-  const long T = static_cast<long>(tot) * p.n_groups;
-  const long U = static_cast<long>(nonempty) * p.n_groups;
+  tot = wave_incl_scan(tot);
+  nonempty = wave_incl_scan(nonempty);
+  if (lane == 63) {
+    sm.wsum[0][wave][0] = tot;
+    sm.wsum[0][wave][1] = nonempty;
+  }
+  __syncthreads();
+  int all_tot = 0, all_nonempty = 0;
+#pragma unroll
+  for (int w = 0; w < NW; ++w) {
+    all_tot += sm.wsum[0][w][0];
+    all_nonempty += sm.wsum[0][w][1];
+  }
+  const long T = static_cast<long>(all_tot) * p.n_groups;
+  const long U = static_cast<long>(all_nonempty) * p.n_groups;
   const long W = p.n_blocks;
-  int R = static_cast<int>(div_up64(T, W));
-  R = R < p.min_tiles ? p.min_tiles : R;
-  int n0 = 0, n1 = 0, n2 = 0;
+  int R0 = static_cast<int>(div_up64(T, W));
+  R0 = R0 < p.min_tiles ? p.min_tiles : R0;
+  const long spare = W - U;  // > 0 whenever the host launches W > units
+  int RF = spare > 0 ? static_cast<int>(div_up64(T, spare)) : p.max_len;
+  RF = RF < p.min_tiles ? p.min_tiles : RF;
+  const int Rc[4] = {R0, R0 + 1, R0 + 2, RF};
+  float rc[4];
+#pragma unroll
+  for (int c = 0; c < 4; ++c) rc[c] = __builtin_amdgcn_rcpf(static_cast<float>(Rc[c]));
+  int own[4] = {0, 0, 0, 0};
   for (int b = b0; b < b1; ++b) {
     const int t = tiles_of(sm.len[b]);
-    n0 += div_up(t, R);
-    n1 += div_up(t, R + 1);
-    n2 += div_up(t, R + 2);
-  }
-  n0 = wave_sum_int(n0);
-  n1 = wave_sum_int(n1);
-  n2 = wave_sum_int(n2);
-  if (static_cast<long>(n0) * p.n_groups <= W) {
-  } else if (static_cast<long>(n1) * p.n_groups <= W) {
-    R += 1;
-  } else if (static_cast<long>(n2) * p.n_groups <= W) {
-    R += 2;
-  } else {
-    const long spare = W - U;  // > 0 whenever the host launches W > units
-    R = spare > 0 ? static_cast<int>(div_up64(T, spare)) : p.max_len;
-    R = R < p.min_tiles ? p.min_tiles : R;
-  }
-  // Exclusive scan of runs per sequence (times n_groups) across the wave.
-  int local = 0;
-  for (int b = b0; b < b1; ++b) local += div_up(tiles_of(sm.len[b]), R);
-  local *= p.n_groups;
-  int x = local;
 #pragma unroll
-  for (int off = 1; off < 64; off <<= 1) {
-    const int y = __shfl_up(x, off);
-    if (lane >= off) x += y;
+    for (int c = 0; c < 4; ++c) own[c] += div_up_r(t, Rc[c], rc[c]);
   }
-  int excl = x - local;
+  int incl[4];
+#pragma unroll
+  for (int c = 0; c < 4; ++c) incl[c] = wave_incl_scan(own[c]);
+  if (lane == 63) {
+#pragma unroll
+    for (int c = 0; c < 4; ++c) sm.wsum[1][wave][c] = incl[c];
+  }
+  __syncthreads();
+  int total[4] = {0, 0, 0, 0}, before[4] = {0, 0, 0, 0};
+#pragma unroll
+  for (int w = 0; w < NW; ++w)
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int v = sm.wsum[1][w][c];
+      total[c] += v;
+      before[c] += w < wave ? v : 0;
+    }
+  int pick = 3;
+#pragma unroll
+  for (int c = 2; c >= 0; --c)
+    if (static_cast<long>(total[c]) * p.n_groups <= W) pick = c;
+  int R = Rc[3], own_p = own[3], incl_p = incl[3], before_p = before[3];
+  float rR = rc[3];
+#pragma unroll
+  for (int c = 2; c >= 0; --c)
+    if (pick == c) {
+      R = Rc[c];
+      rR = rc[c];
+      own_p = own[c];
+      incl_p = incl[c];
+      before_p = before[c];
+    }
+  int excl = (before_p + incl_p - own_p) * p.n_groups;  // runs before this thread's sequences
   for (int b = b0; b < b1; ++b) {
-    const int runs = p.n_groups * div_up(tiles_of(sm.len[b]), R);
+    const int runs = p.n_groups * div_up_r(tiles_of(sm.len[b]), R, rR);
     sm.q[b] = excl;
     if (excl <= g && g < excl + runs) sm.sched[2] = b;  // exactly one sequence holds run g
     excl += runs;
   }
-  if (lane == 63) {
+  if (tid == NT - 1) {
     sm.q[p.B] = excl;
     sm.sched[0] = R;
     sm.sched[1] = excl;
   }
+  __syncthreads();
 }
 
 // Register budget: at least 3 waves per SIMD for D = 64 and 2 for D = 128
@@ -390,7 +450,7 @@ void attention_kernel(AttnParams p) {
     if (item.z >= 0)
       for (int i = threadIdx.x; i < p.h * D4; i += NT)
         store_out4<D>(p, static_cast<size_t>(item.z) * p.h, i * 4, f32x4{0.f, 0.f, 0.f, 0.f});
-    if (item.b < 0) return;
+    if (item.b < 0 || item.b >= p.B) return;
     b = item.b;
     r = item.r;
     j = item.j;
@@ -407,8 +467,7 @@ void attention_kernel(AttnParams p) {
     L = p.max_len;
     k1 = tiles_of(L);
   } else {
-    if (wave == 0) schedule_wave0(p, sm.sc, g);
-    __syncthreads();
+    schedule<NT>(p, sm.sc, g);
     const int R = sm.sc.sched[0];
     const int n_runs = sm.sc.sched[1];
     if (g == 0 && p.runs)  // runs per sequence, for the merge kernel
@@ -427,6 +486,10 @@ void attention_kernel(AttnParams p) {
     }
     // Run g: sequence b, KV group r, run j of that unit.
     b = sm.sc.sched[2];
+    if (b < 0 || b >= p.B) {  // no sequence holds run g (never for a consistent schedule)
+      if (plan_out && threadIdx.x == 0) plan_out[g] = RunItem{-1, 0, 0, 0, 0, 0, 0, z};
+      return;
+    }
     L = sm.sc.len[b];
     const int tiles_b = tiles_of(L);
     nb = div_up(tiles_b, R);  // runs of each unit of sequence b
