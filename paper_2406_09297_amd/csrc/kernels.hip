@@ -58,7 +58,10 @@ __device__ __forceinline__ int attended_len(const AttnParams& p, int b) {
   return L > p.max_len ? p.max_len : L;
 }
 
-__device__ __forceinline__ int tiles_of(int L) { return (L + kTile - 1) / kTile; }
+// Tiles of L >= 0 positions.
+__device__ __forceinline__ int tiles_of(int L) {
+  return static_cast<int>((static_cast<unsigned>(L) + kTile - 1) / kTile);
+}
 
 // ---------------------------------------------------------------------------
 // Rotary position embedding of the GPT-NeoX architecture (the paper's Pythia
@@ -227,10 +230,17 @@ __device__ __forceinline__ void store_out4(const AttnParams& p, size_t row, int 
 constexpr int kMaxWaves = 16;  // waves of the widest attention workgroup the schedule serves
 
 struct SchedShared {
-  int q[kMaxBatch + 1];  // first run (workgroup) of each sequence, in runs of all its units
-  int len[kMaxBatch];    // attended lengths
-  int sched[3];          // run length R, run count N, sequence of this workgroup's run
+  int len[kMaxBatch];         // attended lengths (each thread's own sequences)
   int wsum[2][kMaxWaves][4];  // per-wave totals of the two scans
+};
+
+// A run of the plan: sequence b, KV group r, run j of nb of that unit,
+// attended length L, tiles [k0, k1).  b < 0 marks a workgroup with no run.
+// z >= 0: sequence z attends to nothing and this workgroup writes its zero
+// output (a launch has at least as many workgroups as sequences).
+struct alignas(16) RunItem {
+  int b, r, j, nb;
+  int L, k0, k1, z;
 };
 
 // Partial outputs the last run of a unit can stage in LDS to merge in place.
@@ -249,6 +259,7 @@ struct alignas(16) AttnShared {
     float stage[kStageFloats];
   };
   float stage_ml[kStageMl];
+  RunItem run;                          // this workgroup's run, from the schedule
   alignas(16) uint16_t new_row[2 * D];  // newest token's key and value (fused append)
   double2 rope[kMaxRopePairs];          // the sequence's rotary (cos, sin) pairs
   // QK_VALU: the group's queries (16 heads, zero-padded) and each wave's
@@ -257,32 +268,6 @@ struct alignas(16) AttnShared {
   alignas(16) float s_lds[QK_VALU ? W * 16 * kTile : 4];
   int last;
 };
-
-// A run of the plan: sequence b, KV group r, run j of nb of that unit,
-// attended length L, tiles [k0, k1).  b < 0 marks a workgroup with no run.
-// z >= 0: sequence z attends to nothing and this workgroup writes its zero
-// output (a launch has at least as many workgroups as sequences).
-struct RunItem {
-  int b, r, j, nb;
-  int L, k0, k1, z;
-};
-
-// ceil(x / y) for 0 <= x < 2^21, 1 <= y < 2^21 without the integer-division
-// routine: a float estimate (off by at most one) and one correction each way.
-__device__ __forceinline__ int div_up(int x, int y) {
-  int q = static_cast<int>(static_cast<float>(x) * __builtin_amdgcn_rcpf(static_cast<float>(y)));
-  q -= q * y > x ? 1 : 0;
-  q += (q + 1) * y <= x ? 1 : 0;  // now q = floor(x / y)
-  return q + (q * y < x ? 1 : 0);
-}
-
-// ceil(x / y) for 0 <= x < 2^50, 1 <= y: a double estimate and corrections.
-__device__ __forceinline__ long div_up64(long x, long y) {
-  long q = static_cast<long>(static_cast<double>(x) * __builtin_amdgcn_rcp(static_cast<double>(y)));
-  q -= q * y > x ? 1 : 0;
-  q += (q + 1) * y <= x ? 1 : 0;  // now q = floor(x / y)
-  return q + (q * y < x ? 1 : 0);
-}
 
 // Inclusive prefix sum over the 64 lanes of a wave: within each row of 16
 // lanes by shifted adds (1, 2, 4, 8), then the last lane of row 0 into row 1
@@ -300,38 +285,41 @@ __device__ __forceinline__ int wave_incl_scan(int v) {
 
 __device__ __forceinline__ int wave_total(int incl) { return __builtin_amdgcn_readlane(incl, 63); }
 
-// ceil(x / y) for 0 <= x < 2^21, 1 <= y < 2^21, ry = the float reciprocal of
-// y (uniform divisors take it once): an estimate off by at most one, then one
-// correction each way; the products stay below 2^23, so 24-bit multiplies
-// are exact.
-__device__ __forceinline__ int div_up_r(int x, int y, float ry) {
-  int q = static_cast<int>(static_cast<float>(x) * ry);
-  const int r = x - static_cast<int>(__umul24(q, y));  // in (-y, 2y)
-  q += r < 0 ? -1 : (r >= y ? 1 : 0);
-  const int r2 = r < 0 ? r + y : (r >= y ? r - y : r);  // x - q*y, now in [0, y)
-  return q + (r2 > 0 ? 1 : 0);
-}
+// floor(x) as an integer (the convert rounds toward minus infinity).
+__device__ __forceinline__ int floor_int(float x) { return static_cast<int>(__builtin_floorf(x)); }
+
+// ceil(t / R) for integers 0 <= t < 2^21 and R >= 1, from th = t - 1/2 and
+// rR = the float reciprocal of R (within one ulp): th / R lies at least
+// 1 / (2R) from every integer, farther than the product's rounding error
+// (below th * 2^-22 / R), so floor(th * rR) = ceil(t / R) - 1 exactly (also
+// for t = 0, where it is -1).
+__device__ __forceinline__ int ceil_div_half(float th, float rR) { return floor_int(th * rR) + 1; }
 
 // The run schedule every workgroup derives identically from the lengths,
 // computed by all NT threads together (the sequences split evenly over them)
-// between two barriers: tiles t_b = ceil(L_b / 32); run length R is the
-// least of R0 = ceil(T / W), R0 + 1, R0 + 2 (T = all tiles, W = workgroups,
-// never below min_tiles) whose run count N(R) = n_groups * sum_b ceil(t_b /
-// R) fits W, else RF = ceil(T / (W - U)) (U = non-empty units), which always
-// fits.  One scan (per wave, then across the waves' totals) gives T and U; a
-// second scans the four candidates' per-thread run counts at once, so each
-// thread's first run under the chosen R is its prefix less its own count.
-// Leaves sm.q[b] = runs before sequence b, sm.len, and sm.sched = {R, N,
-// sequence of run g} (-1 if no sequence holds run g); ends with a barrier.
+// between barriers: tiles t_b = ceil(L_b / 32); run length R is the least of
+// R0 = ceil(T / W), R0 + 1, R0 + 2 (T = all tiles, W = workgroups, never
+// below min_tiles) whose run count N(R) = n_groups * sum_b ceil(t_b / R) fits
+// W, else RF = ceil(T / (W - U)) (U = non-empty units), which always fits.
+// One scan (per wave, then across the waves' totals) gives T and U, and the
+// uniform arithmetic on them runs on the scalar unit.  A second scan covers
+// the four candidates' per-thread run counts at once, two to a 32-bit word:
+// every count and prefix is at most N(R) / n_groups <= W + U <= 2W <= 2^15
+// (the host schedules at most 2^14 workgroups), so the 16-bit halves never
+// carry.  Each thread's first run under the chosen R is its prefix less its
+// own count.  The thread whose sequence holds run g writes that run to `run`
+// (b stays -1 when no sequence does), the thread of sequence g marks it for
+// zeroing when it attends to nothing, and workgroup 0 writes the runs per
+// sequence to p.runs (the merge kernel's input).  Ends with a barrier.
 template <int NT>
-__device__ void schedule(const AttnParams& p, SchedShared& sm, int g) {
+__device__ void schedule(const AttnParams& p, SchedShared& sm, RunItem& run, int g) {
   constexpr int NW = NT / 64;
   static_assert(NW <= kMaxWaves, "schedule: too many waves");
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int per = (p.B + NT - 1) / NT;  // sequences per thread
   const int b0 = tid * per;
   const int b1 = b0 + per < p.B ? b0 + per : p.B;
-  if (tid == 0) sm.sched[2] = -1;
+  if (tid == 0) run = RunItem{-1, 0, 0, 0, 0, 0, 0, -1};
   int tot = 0, nonempty = 0;
   for (int b = b0; b < b1; ++b) {
     const int L = attended_len(p, b);
@@ -347,73 +335,92 @@ __device__ void schedule(const AttnParams& p, SchedShared& sm, int g) {
     sm.wsum[0][wave][1] = nonempty;
   }
   __syncthreads();
-  int all_tot = 0, all_nonempty = 0;
+  unsigned all_tot = 0, all_nonempty = 0;
 #pragma unroll
   for (int w = 0; w < NW; ++w) {
-    all_tot += sm.wsum[0][w][0];
-    all_nonempty += sm.wsum[0][w][1];
+    all_tot += __builtin_amdgcn_readfirstlane(sm.wsum[0][w][0]);
+    all_nonempty += __builtin_amdgcn_readfirstlane(sm.wsum[0][w][1]);
   }
-  const long T = static_cast<long>(all_tot) * p.n_groups;
-  const long U = static_cast<long>(all_nonempty) * p.n_groups;
-  const long W = p.n_blocks;
-  int R0 = static_cast<int>(div_up64(T, W));
-  R0 = R0 < p.min_tiles ? p.min_tiles : R0;
-  const long spare = W - U;  // > 0 whenever the host launches W > units
-  int RF = spare > 0 ? static_cast<int>(div_up64(T, spare)) : p.max_len;
-  RF = RF < p.min_tiles ? p.min_tiles : RF;
-  const int Rc[4] = {R0, R0 + 1, R0 + 2, RF};
+  const unsigned T = all_tot * static_cast<unsigned>(p.n_groups);  // below 2^30
+  const unsigned U = all_nonempty * static_cast<unsigned>(p.n_groups);
+  const unsigned W = static_cast<unsigned>(p.n_blocks);  // at least the units, so U <= W
+  const unsigned mt = static_cast<unsigned>(p.min_tiles);
+  unsigned R0 = (T + W - 1) / W;
+  R0 = R0 < mt ? mt : R0;
+  unsigned RF = U < W ? (T + (W - U) - 1) / (W - U) : static_cast<unsigned>(p.max_len);
+  RF = RF < mt ? mt : RF;
+  const int Rc[4] = {static_cast<int>(R0), static_cast<int>(R0 + 1), static_cast<int>(R0 + 2),
+                     static_cast<int>(RF)};
   float rc[4];
 #pragma unroll
   for (int c = 0; c < 4; ++c) rc[c] = __builtin_amdgcn_rcpf(static_cast<float>(Rc[c]));
   int own[4] = {0, 0, 0, 0};
   for (int b = b0; b < b1; ++b) {
-    const int t = tiles_of(sm.len[b]);
+    const float th = static_cast<float>(tiles_of(sm.len[b])) - 0.5f;
 #pragma unroll
-    for (int c = 0; c < 4; ++c) own[c] += div_up_r(t, Rc[c], rc[c]);
+    for (int c = 0; c < 4; ++c) own[c] += floor_int(th * rc[c]);
   }
-  int incl[4];
-#pragma unroll
-  for (int c = 0; c < 4; ++c) incl[c] = wave_incl_scan(own[c]);
+  const int nseq = b1 > b0 ? b1 - b0 : 0;  // the +1 of each ceil_div_half
+  const int own01 = (own[0] + nseq) | ((own[1] + nseq) << 16);
+  const int own23 = (own[2] + nseq) | ((own[3] + nseq) << 16);
+  const int incl01 = wave_incl_scan(own01);
+  const int incl23 = wave_incl_scan(own23);
   if (lane == 63) {
-#pragma unroll
-    for (int c = 0; c < 4; ++c) sm.wsum[1][wave][c] = incl[c];
+    sm.wsum[1][wave][0] = incl01;
+    sm.wsum[1][wave][1] = incl23;
   }
   __syncthreads();
-  int total[4] = {0, 0, 0, 0}, before[4] = {0, 0, 0, 0};
+  unsigned tot01 = 0, tot23 = 0;
+  int before01 = 0, before23 = 0;
 #pragma unroll
-  for (int w = 0; w < NW; ++w)
-#pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      const int v = sm.wsum[1][w][c];
-      total[c] += v;
-      before[c] += w < wave ? v : 0;
-    }
+  for (int w = 0; w < NW; ++w) {
+    const int v01 = __builtin_amdgcn_readfirstlane(sm.wsum[1][w][0]);
+    const int v23 = __builtin_amdgcn_readfirstlane(sm.wsum[1][w][1]);
+    tot01 += static_cast<unsigned>(v01);
+    tot23 += static_cast<unsigned>(v23);
+    before01 += w < wave ? v01 : 0;
+    before23 += w < wave ? v23 : 0;
+  }
+  const unsigned total[4] = {tot01 & 0xffffu, tot01 >> 16, tot23 & 0xffffu, tot23 >> 16};
   int pick = 3;
 #pragma unroll
   for (int c = 2; c >= 0; --c)
-    if (static_cast<long>(total[c]) * p.n_groups <= W) pick = c;
-  int R = Rc[3], own_p = own[3], incl_p = incl[3], before_p = before[3];
+    if (total[c] * static_cast<unsigned>(p.n_groups) <= W) pick = c;
+  int R = Rc[3];
   float rR = rc[3];
 #pragma unroll
   for (int c = 2; c >= 0; --c)
     if (pick == c) {
       R = Rc[c];
       rR = rc[c];
-      own_p = own[c];
-      incl_p = incl[c];
-      before_p = before[c];
     }
-  int excl = (before_p + incl_p - own_p) * p.n_groups;  // runs before this thread's sequences
+  // This thread's exclusive prefix under the chosen candidate (packed halves
+  // subtract without borrow: each half of incl is at least that of own).
+  const int pre2 = pick < 2 ? before01 + incl01 - own01 : before23 + incl23 - own23;
+  int excl = ((pre2 >> ((pick & 1) * 16)) & 0xffff) * p.n_groups;  // runs before this thread's
   for (int b = b0; b < b1; ++b) {
-    const int runs = p.n_groups * div_up_r(tiles_of(sm.len[b]), R, rR);
-    sm.q[b] = excl;
-    if (excl <= g && g < excl + runs) sm.sched[2] = b;  // exactly one sequence holds run g
+    const int L = sm.len[b];
+    const int t = tiles_of(L);
+    const int nb = ceil_div_half(static_cast<float>(t) - 0.5f, rR);  // runs of each unit of b
+    const int runs = p.n_groups * nb;
+    if (g == 0 && p.runs) p.runs[b] = nb;
+    if (excl <= g && g < excl + runs) {  // exactly one sequence holds run g
+      const int rem = g - excl;
+      // floor(rem / nb): (rem + 1/2) / nb lies at least 1 / (2 nb) from an integer.
+      const int r = floor_int((static_cast<float>(rem) + 0.5f) *
+                              __builtin_amdgcn_rcpf(static_cast<float>(nb)));
+      const int j = rem - r * nb;
+      const int k0 = j * R;
+      run.b = b;
+      run.r = r;
+      run.j = j;
+      run.nb = nb;
+      run.L = L;
+      run.k0 = k0;
+      run.k1 = k0 + R < t ? k0 + R : t;
+    }
+    if (b == g && L == 0) run.z = g;
     excl += runs;
-  }
-  if (tid == NT - 1) {
-    sm.q[p.B] = excl;
-    sm.sched[0] = R;
-    sm.sched[1] = excl;
   }
   __syncthreads();
 }
@@ -467,42 +474,24 @@ void attention_kernel(AttnParams p) {
     L = p.max_len;
     k1 = tiles_of(L);
   } else {
-    schedule<NT>(p, sm.sc, g);
-    const int R = sm.sc.sched[0];
-    const int n_runs = sm.sc.sched[1];
-    if (g == 0 && p.runs)  // runs per sequence, for the merge kernel
-      for (int bb = threadIdx.x; bb < p.B; bb += NT)
-        p.runs[bb] = div_up(tiles_of(sm.sc.len[bb]), R);
-    for (int bb = g; bb < p.B; bb += p.n_blocks) {  // sequences with nothing to attend
-      if (sm.sc.len[bb] > 0) continue;
+    schedule<NT>(p, sm.sc, sm.run, g);
+    // The run item lies outside the schedule's LDS tables, so the waves'
+    // merge may overwrite those while other waves still read it.
+    const RunItem item = sm.run;
+    const int ib = __builtin_amdgcn_readfirstlane(item.b);
+    const int iz = __builtin_amdgcn_readfirstlane(item.z);
+    if (p.plan_out && threadIdx.x == 0) reinterpret_cast<RunItem*>(p.plan_out)[g] = item;
+    if (iz >= 0)
       for (int i = threadIdx.x; i < p.h * D4; i += NT)
-        store_out4<D>(p, static_cast<size_t>(bb) * p.h, i * 4, f32x4{0.f, 0.f, 0.f, 0.f});
-    }
-    RunItem* const plan_out = reinterpret_cast<RunItem*>(p.plan_out);
-    const int z = g < p.B && sm.sc.len[g] == 0 ? g : -1;
-    if (g >= n_runs) {
-      if (plan_out && threadIdx.x == 0) plan_out[g] = RunItem{-1, 0, 0, 0, 0, 0, 0, z};
-      return;
-    }
-    // Run g: sequence b, KV group r, run j of that unit.
-    b = sm.sc.sched[2];
-    if (b < 0 || b >= p.B) {  // no sequence holds run g (never for a consistent schedule)
-      if (plan_out && threadIdx.x == 0) plan_out[g] = RunItem{-1, 0, 0, 0, 0, 0, 0, z};
-      return;
-    }
-    L = sm.sc.len[b];
-    const int tiles_b = tiles_of(L);
-    nb = div_up(tiles_b, R);  // runs of each unit of sequence b
-    const int rem = g - sm.sc.q[b];
-    r = div_up(rem + 1, nb) - 1;  // floor(rem / nb)
-    j = rem - r * nb;
-    k0 = j * R;
-    k1 = k0 + R < tiles_b ? k0 + R : tiles_b;
-    if (plan_out && threadIdx.x == 0) plan_out[g] = RunItem{b, r, j, nb, L, k0, k1, z};
-    // The schedule tables share LDS with the waves' merge area: every wave
-    // has read them (the run is in registers) before any wave, possibly one
-    // with no tiles of its own, writes its partial there.
-    __syncthreads();
+        store_out4<D>(p, static_cast<size_t>(iz) * p.h, i * 4, f32x4{0.f, 0.f, 0.f, 0.f});
+    if (ib < 0 || ib >= p.B) return;  // no run for this workgroup
+    b = ib;
+    r = __builtin_amdgcn_readfirstlane(item.r);
+    j = __builtin_amdgcn_readfirstlane(item.j);
+    nb = __builtin_amdgcn_readfirstlane(item.nb);
+    L = __builtin_amdgcn_readfirstlane(item.L);
+    k0 = __builtin_amdgcn_readfirstlane(item.k0);
+    k1 = __builtin_amdgcn_readfirstlane(item.k1);
   }
 
   const int kv = p.kv_begin + r;

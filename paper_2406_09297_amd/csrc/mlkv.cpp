@@ -157,7 +157,10 @@ struct Plan {
 };
 constexpr int kMinTiles = 4;
 constexpr int kMaxRunsPerUnit = 128;
-constexpr long kCounterSlots = 65536;  // arrival counters of a workspace (bounds the workgroups)
+constexpr long kCounterSlots = 65536;  // arrival counters of a workspace
+// Launches that schedule their runs on the device use at most this many
+// workgroups (the schedule counts runs in 16-bit halves).
+constexpr long kMaxScheduledWorkgroups = 16384;
 constexpr int kFallbackResident = 768;  // 256 CUs x 3 when no device can be queried
 constexpr int kWorkgroupsPerCu = 2;
 
@@ -191,7 +194,7 @@ long workgroup_budget(int head_dim) {
     const long w = std::atol(env);
     if (w > 0) resident = w;
   }
-  return resident < kCounterSlots ? resident : kCounterSlots;
+  return resident < kMaxScheduledWorkgroups ? resident : kMaxScheduledWorkgroups;
 }
 
 Plan plan(const mlkv_map* map, int layer, int batch, int max_len, int head_dim) {
@@ -266,11 +269,22 @@ size_t rope_table_bytes(int batch, int rotary_dims) {
 
 // Plans that schedule runs inside the kernel keep per-sequence tables in LDS,
 // which bounds the batch; direct plans (a workgroup per unit) have no bound.
-mlkv_status check_plan_batch(const Plan& pl, int batch) {
-  if (pl.direct || pl.n_blocks <= 1 || batch <= mlkv::max_batch()) return MLKV_OK;
-  return fail(MLKV_ERR_UNSUPPORTED,
-              "batch %d above %d needs one workgroup per (sequence, KV head): %d workgroups "
-              "planned", batch, mlkv::max_batch(), pl.n_blocks);
+// The in-kernel schedule also counts all tiles of a layer in 32 bits (below
+// 2^30, far above any cache that fits a device) and gives each workgroup at
+// most one sequence with nothing to attend (at least one workgroup per
+// sequence, which the plan always launches).
+mlkv_status check_plan_batch(const Plan& pl, int batch, int kv_count) {
+  if (pl.direct || pl.n_blocks <= 1) return MLKV_OK;
+  if (batch > mlkv::max_batch())
+    return fail(MLKV_ERR_UNSUPPORTED,
+                "batch %d above %d needs one workgroup per (sequence, KV head): %d workgroups "
+                "planned", batch, mlkv::max_batch(), pl.n_blocks);
+  if (static_cast<long>(batch) * kv_count * pl.max_tiles >= (1L << 30))
+    return fail(MLKV_ERR_UNSUPPORTED, "%d sequences x %d KV heads x %d tiles: too many tiles",
+                batch, kv_count, pl.max_tiles);
+  if (pl.n_blocks < batch)
+    return fail(MLKV_ERR_UNSUPPORTED, "plan of %d workgroups for %d sequences", pl.n_blocks, batch);
+  return MLKV_OK;
 }
 
 // Workspace layout of one call (nothing when one workgroup does all):
@@ -346,7 +360,8 @@ mlkv_status attention_impl(int layer, const void* q, const mlkv_cache* cache, co
   const int B = cache->batch, S = cache->capacity, D = cache->head_dim;
   const int max_len = max_len_hint <= 0 ? S : max_len_hint;
   const Plan pl = plan(map, layer, B, max_len, D);
-  if (const mlkv_status bs = check_plan_batch(pl, B); bs != MLKV_OK) return bs;
+  if (const mlkv_status bs = check_plan_batch(pl, B, map->kv_count[layer]); bs != MLKV_OK)
+    return bs;
   const size_t need = workspace_need(B, map->h, D, pl);
   if (need > 0 && (!ws || ws_bytes < need))
     return fail(MLKV_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need,
@@ -835,7 +850,7 @@ mlkv_status decode_step_check(const void* q_all, const void* k_new_all, const vo
     const int max_len = max_len_hint <= 0 ? cache->capacity : max_len_hint;
     for (int n = 0; n < map->l; ++n) {
       const Plan pl = plan(map, n, B, max_len, D);
-      if ((s = check_plan_batch(pl, B)) != MLKV_OK) return s;
+      if ((s = check_plan_batch(pl, B, map->kv_count[n])) != MLKV_OK) return s;
       const size_t need = workspace_need(B, h, D, pl);
       if (need > 0 && (!workspace || workspace_bytes < need))
         return fail(MLKV_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need,
