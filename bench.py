@@ -566,11 +566,13 @@ def launch_floor(workgroups: int) -> dict:
     return {"launch_floor_us": round(mlkv.profile_launch_floor(workgroups, 256, 100) * 1e3, 3)}
 
 
-def read_reference(bytes_per_launch: int, hbm_bytes: int = 2 << 30) -> dict:
+def read_reference(bytes_per_launch: int, hbm_bytes: int = 2 << 30, cold_reps: int = 0) -> dict:
     """Achievable read rates, timed like the attention launches (event pairs
     recorded with each dispatch): a plain streaming read of the same bytes as
     one attention launch, warm in the caches (median of 20 back-to-back
-    launches), and of a 2 GiB buffer, eight times the Infinity Cache (HBM)."""
+    launches) and, with cold_reps, cold (the median of that many launches,
+    each after the same 1 GiB flush read as the cold attention launches), and
+    of a 2 GiB buffer, eight times the Infinity Cache (HBM)."""
     import torch
     import paper_2406_09297_amd as mlkv
 
@@ -578,6 +580,15 @@ def read_reference(bytes_per_launch: int, hbm_bytes: int = 2 << 30) -> dict:
     same = torch.ones((int(bytes_per_launch) + 16 + 15) // 16 * 4, dtype=torch.int32, device="cuda")
     mlkv.profile_read_bandwidth(same, reps=3)  # warm
     out["same_bytes_warm_gbs"] = round(mlkv.profile_read_bandwidth(same, reps=20)[0], 1)
+    if cold_reps:
+        flush = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
+        sink = torch.zeros((), device="cuda")
+        cold = []
+        for _ in range(cold_reps):
+            flush_caches(flush, sink)
+            cold.append(mlkv.profile_read_bandwidth(same, reps=1)[0])
+        out["same_bytes_cold_gbs"] = round(float(np.median(cold)), 1)
+        del flush
     del same
     if hbm_bytes:
         big = torch.ones(hbm_bytes // 4, dtype=torch.int32, device="cuda")
@@ -811,7 +822,7 @@ def measure_decode(args, w, dev, headline: bool):
 
     workgroups, max_parts = mp.plan(0, w.B, S, w.D, max_len)
     floor = launch_floor(workgroups)
-    ref = read_reference(int(attn_bytes))
+    ref = read_reference(int(attn_bytes), cold_reps=15)
     p10, p50, p90 = (float(np.percentile(c_dur, pq)) for pq in (10, 50, 90))
     gbs = step_total / (ms_step * 1e-3) / 1e9
     warm_gbs = step_total / (ms_warm * 1e-3) / 1e9
@@ -837,6 +848,7 @@ def measure_decode(args, w, dev, headline: bool):
         "attainable_frac": attainable(attn_bytes, floor["launch_floor_us"]),
         "read_reference": ref,
         "frac_of_hbm_read": round(achieved / ref["hbm_2GiB_gbs"], 4),
+        "frac_of_same_bytes_cold_read": round(achieved / ref["same_bytes_cold_gbs"], 4),
     }
     result = {
         "metric": "decode-attention HBM GB/s (% of peak) + decode steps/s, MLKV Pythia-160M shape",
