@@ -200,6 +200,45 @@ def test_schedule_path_with_many_short_runs(workgroups):
     check_close(out, ref, f"short runs step wg{workgroups}")
 
 
+def test_schedule_path_at_the_table_limit():
+    """The in-kernel schedule at its table size: 2048 sequences, eight per
+    thread, under a workgroup budget of 4096, so the per-thread loops, the
+    packed run-count scans (about 3700 runs) and the run lookup across
+    thread slices all run, with units split into up to three runs merged in
+    place; ragged lengths (0..400 positions, a few sequences attending
+    nothing), then a whole step (its first layer records the plan, the
+    others follow it)."""
+    rng = np.random.default_rng(37)
+    lens = rng.integers(0, 401, size=2048).astype(np.int32)
+    lens[:4] = [0, 1, 400, 33]
+    lens[-3:] = [0, 32, 64]
+    w = _sweep_workload(64, 4, 1, np.maximum(lens, 1), h=12, l=4, seed=137)
+    dw = DeviceWorkload(w)
+    lens_d = torch.from_numpy(lens).cuda()
+    with plan_env(workgroups="4096"):
+        assert dw.map.plan(0, w.B, dw.S, w.D, int(lens.max()))[0] == 4096  # > units: scheduled
+        # The default plan gives each of the 2048 units its own workgroup and
+        # needs no workspace; this budget's plan does.
+        dw.ws = mlkv.workspace(dw.map, w.B, dw.S, w.D)
+        for n in (0, 1):
+            say(f"table limit B={w.B} layer={n}")
+            out = torch.empty((w.B, w.h, w.D), dtype=torch.float32, device="cuda")
+            mlkv.decode_attention(n, dw.q[n], dw.cache, dw.map, lens_d, out, ws=dw.ws)
+            torch.cuda.synchronize()
+            ref = oracle.decode_attention(n, dw.host["q"][n], dw.host["k_cache"],
+                                          dw.host["v_cache"], dw.kv_of, lens)
+            got = out.cpu().numpy()
+            assert np.all(got[lens == 0] == 0.0), "sequences attending nothing must be zero"
+            check_close(got, ref, f"table limit L{n}")
+        say("table limit: step")
+        _with_contexts(dw, np.maximum(lens, 1) - 1)
+        out = _run_step(dw).cpu().numpy()
+    k_gpu, v_gpu = dw.read_cache()
+    ref, k_ref, v_ref = _oracle_step(dw)
+    assert np.array_equal(k_gpu, k_ref) and np.array_equal(v_gpu, v_ref), "cache differs"
+    check_close(out, ref, "table limit step")
+
+
 def test_split_count_invariance_and_determinism():
     """Results do not depend on how many workgroups share the tiles (up to
     rounding), and a repeated call is bitwise identical."""
