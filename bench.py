@@ -156,7 +156,7 @@ def prefill_flops(w, ctx):
     return w.l * w.h * pairs * 4 * w.D
 
 
-def run_prefill(args, w):
+def run_prefill(args, w, emit: bool = True):
     import torch
     import synth
     import paper_2406_09297_amd as mlkv
@@ -274,10 +274,12 @@ def run_prefill(args, w):
             "sample": f"{runs} x layer 0 of one sequence ({w.T} tokens, fp64 oracle, "
                       f"OpenMP over (token, head)), {spent:.1f} s; tokens/s scaled to all "
                       f"{w.l} layers"}
-    print(json.dumps(result), flush=True)
+    if emit:
+        print(json.dumps(result), flush=True)
+    return result
 
 
-def run_model(args, w):
+def run_model(args, w, emit: bool = True):
     """Whole-model decode step (mlkv_model_decode_step): tokens/s at batch B."""
     import torch
     import synth
@@ -403,7 +405,9 @@ def run_model(args, w):
             "kind": "oracle",
             "sample": f"{runs} whole model step(s) of the same workload (float64 numpy oracle), "
                       f"{spent:.1f} s"}
-    print(json.dumps(result), flush=True)
+    if emit:
+        print(json.dumps(result), flush=True)
+    return result
 
 
 CAPACITY_MARGIN = 4 << 30  # device bytes left free beside the step's buffers
@@ -624,6 +628,8 @@ def main():
                     help="model workload: batch size other than the workload's")
     ap.add_argument("--no-graph", action="store_true",
                     help="model workload: time eager launches only (default: graph replays)")
+    ap.add_argument("--no-next-rows", action="store_true",
+                    help="default workload: skip the prefill and model-step objects of the line")
     ap.add_argument("--pmc-pass", action="store_true",
                     help="for rocprofv3 --pmc runs: a 256 MiB reference copy, then a few steps")
     args = ap.parse_args()
@@ -678,6 +684,22 @@ def main():
         wl = synth.get_workload(extra)
         sub = measure_decode(args, wl, dev, headline=False)
         result["long_context"] = sub
+    if w.name == DEFAULT_WORKLOAD and not args.map and not args.no_next_rows:
+        # The rows after the decode path, timed in the same run: the causal
+        # prefill of a 2000-token prompt and the whole-model decode step
+        # (fewer steps; the line's CPU baseline is the decode step's).
+        import copy
+
+        sub_args = copy.copy(args)
+        sub_args.no_cpu_baseline = True
+        sub_args.steps = max(1, min(args.steps, 20))
+        sub_args.warmup = max(1, min(args.warmup, 3))
+        pw = synth.get_workload("prefill_b8_2000")
+        mw = synth.get_workload("model_b8")
+        if mw.sweep:
+            mw = mw.with_map(*mw.sweep[-1])
+        result["next_rows"] = {"prefill": run_prefill(sub_args, pw, emit=False),
+                               "model_step": run_model(sub_args, mw, emit=False)}
     print(json.dumps(result), flush=True)
 
 
