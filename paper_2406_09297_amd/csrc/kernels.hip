@@ -211,6 +211,13 @@ __global__ __launch_bounds__(kRowsThreads) void cache_rows_kernel(CacheRowsParam
   }
 }
 
+// acc / den for den > 0, zeros otherwise: one reciprocal (within one ulp)
+// for the four channels.  A normalised softmax has den >= 1 (the largest
+// weight is at least one), and den = 1 leaves acc exact.
+__device__ __forceinline__ f32x4 normalize4(f32x4 acc, float den) {
+  return den > 0.f ? acc * __builtin_amdgcn_rcpf(den) : f32x4{0.f, 0.f, 0.f, 0.f};
+}
+
 // ---------------------------------------------------------------------------
 // Split-K attention over a balanced flat tile list.
 // ---------------------------------------------------------------------------
@@ -668,7 +675,7 @@ void attention_kernel(AttnParams p) {
       }
     }
     if (nb == 1) {
-      store_out4<D>(p, out_row0 + hh, d, wsum > 0.f ? o / wsum : f32x4{0.f, 0.f, 0.f, 0.f});
+      store_out4<D>(p, out_row0 + hh, d, normalize4(o, wsum));
     } else if (fuse) {
       store4_device(rsrc_acc, (j * GD + hh * D + d) * 4, o);
       if (d == 0) {
@@ -742,7 +749,7 @@ void attention_kernel(AttnParams p) {
         o += f * *reinterpret_cast<const f32x4*>(&sm.stage[s2 * GD + hh * D + d]);
       }
     }
-    store_out4<D>(p, out_row0 + hh, d, den > 0.f ? o / den : f32x4{0.f, 0.f, 0.f, 0.f});
+    store_out4<D>(p, out_row0 + hh, d, normalize4(o, den));
   }
   if (threadIdx.x == 0)  // ready for the next call on this workspace
     __hip_atomic_store(&p.counters[unit], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -854,7 +861,7 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(AttnParams p) {
     for (int e = 0; e < 4; ++e) o[e] += __shfl_xor(o[e], off);
   }
   if (wpr == 1) {
-    if (sub == 0) store_out4<D>(p, rrow, c, den > 0.f ? o / den : f32x4{0.f, 0.f, 0.f, 0.f});
+    if (sub == 0) store_out4<D>(p, rrow, c, normalize4(o, den));
     return;
   }
   // Several waves per row (one row per workgroup): merge through LDS.
