@@ -533,11 +533,12 @@ def run_capacity(args, w):
         sel = torch.arange(4, device=dev)
         q_h = mlkv.bf16_bits(q.index_select(1, sel))
         kn_h, vn_h = mlkv.bf16_bits(kn[:4]), mlkv.bf16_bits(vn[:4])
-        k_h = mlkv.bf16_bits(cache.k.index_select(1, sel))
-        # value plane: 32-token blocks stored channel-major -> token rows
-        v_h = np.ascontiguousarray(
-            mlkv.bf16_bits(cache.v.index_select(1, sel)).reshape(w.n_kv, 4, S // 32, w.D, 32)
-            .transpose(0, 1, 2, 4, 3)).reshape(w.n_kv, 4, S, w.D)
+        # the sampled sequences' planes as plain token rows (mlkv_cache_read_rows)
+        sub = mlkv.Cache(cache.k.index_select(1, sel).contiguous(),
+                         cache.v.index_select(1, sel).contiguous())
+        k_r, v_r = sub.read_rows()
+        torch.cuda.synchronize()
+        k_h, v_h = mlkv.bf16_bits(k_r), mlkv.bf16_bits(v_r)
         ctx_h = np.full(4, w.ctx, dtype=np.int32)
         import oracle
 

@@ -108,8 +108,13 @@ int mlkv_map_layer_owned_begin(const mlkv_map* map, int layer);
  * Caller-owned device memory (e.g. torch tensors); the library never frees it.
  * capacity must be a multiple of 32; head_dim 64 or 128; both planes 16-byte
  * aligned.  Element (kv, b, t, d), t < capacity, lives at
- *   K: k[((kv*batch + b)*capacity + t)*head_dim + d]
- *      (each sequence's keys are contiguous token rows)
+ *   K: k[((kv*batch + b)*capacity + (t & ~31))*head_dim + 8*q(t & 31, d >> 3) + (d & 7)]
+ *      with q(u, c) = ((((u >> 2) & 1)*(head_dim/32) + (c >> 2))*64
+ *                      + (c & 3)*16 + ((u >> 3) << 2) + (u & 3))
+ *      (keys in blocks of 32 tokens; inside a block, the 16-byte chunks of
+ *      channels 8c .. 8c+7 are ordered as the matrix-core operands of the
+ *      block's two 16-token halves and 32-channel steps, so each 1 KB run of
+ *      the block is one load instruction of a wave)
  *   V: v[((kv*batch + b)*capacity + (t & ~31))*head_dim + d*32 + (t & 31)]
  *      (values in blocks of 32 tokens, channel-major inside a block, so a
  *      block is the transposed 32 x head_dim tile)

@@ -246,8 +246,10 @@ class Map:
 class Cache:
     """KV cache planes in device memory (torch tensors, caller-owned).
 
-    k: [n_kv][B][S][D] bf16;  v: [n_kv][B][S/32][D][32] bf16 (channel-major
-    32-token blocks).  The layout is the one documented in mlkv.h."""
+    k: [n_kv][B][S][D] bf16 elements, each 32-token block of a sequence in
+    the matrix-core operand order;  v: [n_kv][B][S/32][D][32] bf16
+    (channel-major 32-token blocks).  The layout is the one documented in
+    mlkv.h; write_rows / read_rows convert from and to plain token rows."""
 
     def __init__(self, k: torch.Tensor, v: torch.Tensor):
         n_kv, B, S, D = k.shape

@@ -150,7 +150,8 @@ __global__ __launch_bounds__(D / 8) void append_kernel(AppendParams p) {
     kv_k = rotate_chunk(kv_k, partner, d0, p.rope_half, [&](int j) { return cs[j]; });
   }
   const size_t seq = static_cast<size_t>(p.kv_begin + c) * p.B + b;
-  *reinterpret_cast<u16x8*>(p.k + (seq * p.S + pos) * D + d0) = kv_k;
+  *reinterpret_cast<u16x8*>(p.k + (seq * p.S + (pos & ~(kTile - 1))) * D +
+                            kchunk<D>(pos & (kTile - 1), d0 / 8) * 8) = kv_k;
   uint16_t* vdst = p.v + (seq * p.S + (pos & ~(kTile - 1))) * D + (pos & (kTile - 1));
 #pragma unroll
   for (int e = 0; e < 8; ++e) vdst[(d0 + e) * kTile] = kv_v[e];
@@ -158,9 +159,10 @@ __global__ __launch_bounds__(D / 8) void append_kernel(AppendParams p) {
 
 // ---------------------------------------------------------------------------
 // Cache planes <-> logical rows, one workgroup per 32-token block of one
-// (KV head, sequence): the block's K rows are copied as they are; its V rows
-// go through LDS, where the [32][D] tile is transposed to [D][32], so both
-// the row side and the plane side move in 16-byte pieces.
+// (KV head, sequence): the block's K rows move as 16-byte chunks to and from
+// their places in the tile (kchunk); its V rows go through LDS, where the
+// [32][D] tile is transposed to [D][32], so both the row side and the plane
+// side move in 16-byte pieces.
 // ---------------------------------------------------------------------------
 constexpr int kRowsThreads = 256;
 
@@ -175,12 +177,13 @@ __global__ __launch_bounds__(kRowsThreads) void cache_rows_kernel(CacheRowsParam
   const size_t tb = blk - seq * blocks_per_seq;
   const size_t row_off = (seq * p.S + tb * kTile) * D;  // in the rows
   const size_t plane_off = (static_cast<size_t>(p.kv_begin) * p.B * p.S) * D + row_off;
-  for (int i = threadIdx.x; i < kChunks; i += kRowsThreads) {
+  for (int i = threadIdx.x; i < kChunks; i += kRowsThreads) {  // token i / (D/8), channels
     const size_t e = static_cast<size_t>(i) * 8;
+    const size_t pe = static_cast<size_t>(kchunk<D>(i / (D / 8), i % (D / 8))) * 8;
     if (p.to_cache)
-      *reinterpret_cast<u16x8*>(p.k_plane + plane_off + e) = load16(p.k_rows + row_off + e);
+      *reinterpret_cast<u16x8*>(p.k_plane + plane_off + pe) = load16(p.k_rows + row_off + e);
     else
-      *reinterpret_cast<u16x8*>(p.k_rows + row_off + e) = load16(p.k_plane + plane_off + e);
+      *reinterpret_cast<u16x8*>(p.k_rows + row_off + e) = load16(p.k_plane + plane_off + pe);
   }
   if (p.to_cache) {
     for (int i = threadIdx.x; i < kChunks; i += kRowsThreads) {  // token i / (D/8), channels
@@ -594,7 +597,8 @@ void attention_kernel(AttnParams p) {
                             rope_half, cs_lds);
         uint16_t* kc = const_cast<uint16_t*>(kbase);  // the caller's cache, written here only
         uint16_t* vc = const_cast<uint16_t*>(vbase);
-        *reinterpret_cast<u16x8*>(kc + static_cast<size_t>(pos) * D + d0) = nk;
+        *reinterpret_cast<u16x8*>(kc + static_cast<size_t>(pos & ~(kTile - 1)) * D +
+                                  kchunk<D>(pos & (kTile - 1), d0 / 8) * 8) = nk;
         uint16_t* vdst = vc + static_cast<size_t>(pos & ~(kTile - 1)) * D + (pos & (kTile - 1));
 #pragma unroll
         for (int e = 0; e < 8; ++e) vdst[(d0 + e) * kTile] = nv[e];

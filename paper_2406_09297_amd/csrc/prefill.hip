@@ -160,8 +160,8 @@ __device__ __forceinline__ void stage_store(const TileStage<D>& s, PrefillTileLd
 #pragma unroll
   for (int u = 0; u < TileStage<D>::CH; ++u) {
     const int idx = threadIdx.x + u * 256;
-    // key chunk idx: row idx / (D/8), channels (idx % (D/8)) * 8
-    const int kr = idx / (D / 8), kc = idx - kr * (D / 8);
+    // key chunk idx of the tile (kchunk order): its token row and channel group
+    const int kr = kchunk_token<D>(idx), kc = kchunk_group<D>(idx);
     *reinterpret_cast<u16x8*>(&lds.k[kr * PrefillTileLds<D>::KSTR + kc * 8]) = s.k[u];
     // value chunk idx: channel idx / 4, tokens (idx % 4) * 8 (channel-major block)
     const int vc = idx >> 2, vp = idx & 3;
@@ -313,7 +313,8 @@ __global__ __launch_bounds__(256) void append_rows_kernel(AppendRowsParams p) {
   const u16x8 kv_k = load16(p.k_new + src);
   const u16x8 kv_v = load16(p.v_new + src);
   const size_t seq = static_cast<size_t>(p.kv_begin + c) * p.B + b;
-  *reinterpret_cast<u16x8*>(p.k + (seq * p.S + pos) * D + d0) = kv_k;
+  *reinterpret_cast<u16x8*>(p.k + (seq * p.S + (pos & ~(kTile - 1))) * D +
+                            kchunk<D>(pos & (kTile - 1), d0 / 8) * 8) = kv_k;
   uint16_t* vdst = p.v + (seq * p.S + (pos & ~static_cast<long>(kTile - 1))) * D + (pos & (kTile - 1));
 #pragma unroll
   for (int e = 0; e < 8; ++e) vdst[(d0 + e) * kTile] = kv_v[e];

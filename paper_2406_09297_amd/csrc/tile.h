@@ -97,6 +97,28 @@ __device__ __forceinline__ uint16_t f32_to_bf16_bits(float f) {
 // ---------------------------------------------------------------------------
 // One 32-token tile of keys/values against 16 query columns (a wave).
 // ---------------------------------------------------------------------------
+// Key plane: each 32-token tile keeps, for each of its two 16-token score
+// blocks and each 32-channel k-step, the 64 lanes' MFMA operands contiguous
+// (1 KB per block and k-step; lane 16 g + r holds channels 8 g .. 8 g + 7 of
+// the step for the block's row r).  The 16-byte chunk of tile token u (0 ..
+// 31) with channels 8c .. 8c + 7, so that one load instruction of a wave
+// reads 1 KB in one piece:
+template <int D>
+__device__ __forceinline__ int kchunk(int u, int c) {
+  return ((((u >> 2) & 1) * (D / 32) + (c >> 2)) * 64) + (c & 3) * 16 + ((u >> 3) << 2) + (u & 3);
+}
+// ... and its inverse: chunk q holds token (kchunk_token) and channel group
+// (kchunk_group) of the tile.
+template <int D>
+__device__ __forceinline__ int kchunk_token(int q) {
+  const int col = q & 15, sb = (q >> 6) / (D / 32);
+  return ((col >> 2) << 3) + sb * 4 + (col & 3);
+}
+template <int D>
+__device__ __forceinline__ int kchunk_group(int q) {
+  return ((q >> 4) & 3) + 4 * ((q >> 6) % (D / 32));
+}
+
 template <int D>
 struct Tile {
   static constexpr int KK = D / 32;  // k-steps of the q.K product
@@ -114,18 +136,20 @@ struct Tile {
 template <int D, bool QK_VALU>
 __device__ __forceinline__ void load_tile(Tile<D>& t, const uint16_t* kbase,
                                           const uint16_t* vbase, int t0, int col, int grp) {
-  if (QK_VALU) {
-    const uint16_t* kt = kbase + static_cast<size_t>(t0) * D + (grp * 16 + col) * 8;
+  const uint16_t* ktile = kbase + static_cast<size_t>(t0) * D;
+  if (QK_VALU) {  // rows in order: lane l of piece j holds row j * 512 / D + l / (D / 8)
+    constexpr int LPR = D / 8, RPP = 512 / D;
+    const int lane = grp * 16 + col;
 #pragma unroll
-    for (int j = 0; j < 2 * Tile<D>::KK; ++j) t.k[j / Tile<D>::KK][j % Tile<D>::KK] = load16(kt + j * 512);
-  } else {
+    for (int j = 0; j < 2 * Tile<D>::KK; ++j)
+      t.k[j / Tile<D>::KK][j % Tile<D>::KK] =
+          load16(ktile + kchunk<D>(j * RPP + lane / LPR, lane % LPR) * 8);
+  } else {  // the MFMA operands: one contiguous 1 KB piece per block and k-step
+    const uint16_t* kt = ktile + (grp * 16 + col) * 8;
 #pragma unroll
-    for (int sb = 0; sb < 2; ++sb) {
-      const int tok = t0 + (col >> 2) * 8 + sb * 4 + (col & 3);
-      const uint16_t* krow = kbase + static_cast<size_t>(tok) * D + grp * 8;
+    for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
-      for (int kk = 0; kk < Tile<D>::KK; ++kk) t.k[sb][kk] = load16(krow + kk * 32);
-    }
+      for (int kk = 0; kk < Tile<D>::KK; ++kk) t.k[sb][kk] = load16(kt + (sb * Tile<D>::KK + kk) * 512);
   }
   const uint16_t* vblk = vbase + static_cast<size_t>(t0) * D + grp * 8;
 #pragma unroll

@@ -15,7 +15,7 @@ torch = pytest.importorskip("torch")
 import oracle  # noqa: E402
 import synth  # noqa: E402
 from gpu_util import DeviceWorkload, check_close, f64, say  # noqa: E402
-from layout_ref import unpack_v  # noqa: E402
+from layout_ref import unpack_k, unpack_v  # noqa: E402
 
 pytestmark = pytest.mark.gpu
 
@@ -105,7 +105,7 @@ def test_cache_rows_through_the_library(n_kv, B, S, D):
     v_plane = mlkv.bf16_bits(cache.v).reshape(n_kv, B, S // 32, D, 32)
     nan = mlkv.bf16_bits(torch.tensor([float("nan")], dtype=torch.bfloat16))[0]
     assert np.all(k_plane[:lo] == nan) and np.all(v_plane[:lo] == nan), "other heads written"
-    assert np.array_equal(k_plane[lo:], rows_k[lo:])
+    assert np.array_equal(k_plane[lo:], layout_ref.pack_k(rows_k[lo:]))
     assert np.array_equal(v_plane[lo:], layout_ref.pack_v(rows_v[lo:]))
     k_back, v_back = cache.read_rows(lo)
     torch.cuda.synchronize()
@@ -717,7 +717,7 @@ def test_full_size_7b_step_sampled_sequences():
     sel = torch.tensor(sample, device="cuda")
 
     def rows():
-        k = mlkv.bf16_bits(cache.k.index_select(1, sel))
+        k = unpack_k(mlkv.bf16_bits(cache.k.index_select(1, sel)), w.n_kv, len(sample), S, w.D)
         v = unpack_v(mlkv.bf16_bits(cache.v.index_select(1, sel)), w.n_kv, len(sample), S, w.D)
         return k, v
 
@@ -767,7 +767,7 @@ def test_large_batch_step_sampled_sequences(m, g, B):
     sel = torch.tensor(sample, device="cuda")
 
     def rows():
-        k = mlkv.bf16_bits(cache.k.index_select(1, sel))
+        k = unpack_k(mlkv.bf16_bits(cache.k.index_select(1, sel)), w.n_kv, len(sample), S, w.D)
         v = unpack_v(mlkv.bf16_bits(cache.v.index_select(1, sel)), w.n_kv, len(sample), S, w.D)
         return k, v
 
@@ -811,7 +811,7 @@ def test_capacity_batch_step_sampled_sequences():
     sel = torch.tensor(sample, device="cuda")
 
     def rows():
-        k = mlkv.bf16_bits(cache.k.index_select(1, sel))
+        k = unpack_k(mlkv.bf16_bits(cache.k.index_select(1, sel)), w.n_kv, len(sample), S, w.D)
         v = unpack_v(mlkv.bf16_bits(cache.v.index_select(1, sel)), w.n_kv, len(sample), S, w.D)
         return k, v
 
