@@ -205,6 +205,33 @@ Plan plan(const mlkv_map* map, int layer, int batch, int max_len, int head_dim) 
   const long resident = workgroup_budget(head_dim);
   pl.min_tiles = kMinTiles;
   pl.fused = 0;
+  // A layer that only re-reads KV heads earlier layers of its group have
+  // read gives each (sequence, KV head) unit one eight-wave workgroup (no
+  // split runs, schedule or merge) when the units fill at least 3/8 of the
+  // compute units: on MI355X the Infinity Cache then serves those heads,
+  // and the workgroups stream them faster than balanced split runs plus the
+  // merge of their partials (MLKV-4 at 128 ragged sequences: 10.3 against
+  // 11.1 us per such layer; MLKV-12 at 32 sequences of 2048: 17 % off the
+  // step).  Owning layers, which read their heads from HBM first, keep the
+  // split runs, as do maps without sharing across layers.  MLKV_WIDE=0 / 1
+  // turns this off / applies it to every layer.
+  const char* wide_env = std::getenv("MLKV_WIDE");
+  const int wide_mode = wide_env ? (std::atoi(wide_env) != 0 ? 1 : 0) : -1;
+  if (wide_mode != 0 && units < resident) {
+    long cus = mlkv::compute_units();
+    if (cus <= 0) cus = kFallbackResident / 3;
+    bool rereads = true;
+    for (int c = 0; c < map->kv_count[layer]; ++c)
+      rereads = rereads && map->owner_of[map->kv_begin[layer] + c] < layer;
+    if (wide_mode == 1 || (rereads && 8 * units >= 3 * cus)) {
+      pl.n_blocks = static_cast<int>(units);
+      pl.waves = mlkv::wide_waves();
+      pl.min_tiles = pl.max_tiles;
+      pl.direct = 1;
+      pl.max_parts = 2;
+      return pl;
+    }
+  }
   const long cap_parts = mlkv::stage_floats() / (static_cast<long>(map->group[layer]) * head_dim);
   const char* comb = std::getenv("MLKV_COMBINE");
   const bool force_kernel = comb && std::strcmp(comb, "kernel") == 0;
@@ -235,16 +262,6 @@ Plan plan(const mlkv_map* map, int layer, int batch, int max_len, int head_dim) 
   long g = workgroups_for(budget, units, t_max, pl.min_tiles);
   if (units == 1 && t_max <= 4 * kMinTiles) g = 1;
   pl.waves = mlkv::default_waves();
-  // MLKV_WIDE=1: each unit becomes one run on a wider workgroup, so there
-  // are no partials and no merge kernel.  On MI355X this measured no faster
-  // than balanced runs plus the merge for a 128-sequence ragged batch (the
-  // longest sequence bounds it), so it is not the default.
-  bool wide = false;
-  if (const char* env = std::getenv("MLKV_WIDE")) wide = std::atoi(env) != 0;
-  if (wide) {
-    g = units;
-    pl.waves = mlkv::wide_waves();
-  }
   pl.n_blocks = static_cast<int>(g);
   if (g == units) {  // one workgroup per unit: runs cover whole units, nothing to merge
     pl.min_tiles = pl.max_tiles;
@@ -256,6 +273,15 @@ Plan plan(const mlkv_map* map, int layer, int batch, int max_len, int head_dim) 
   }
   pl.max_parts = (pl.max_tiles + pl.min_tiles - 1) / pl.min_tiles + 1;
   return pl;
+}
+
+// Whether launches of this plan record (or follow) a step's run items: split
+// runs scheduled on the device; not a workgroup per unit or one workgroup.
+bool plan_records(const Plan& pl) { return !pl.direct && pl.n_blocks > 1; }
+
+// The work-plan bound of a call: the hint, or the capacity for a hint <= 0.
+int max_len_of(const mlkv_cache* cache, int max_len_hint) {
+  return max_len_hint <= 0 ? cache->capacity : max_len_hint;
 }
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
@@ -893,15 +919,18 @@ mlkv_status decode_step_launch(const void* q_all, const void* k_new_all, const v
     }
     const void* q = static_cast<const uint16_t*>(q_all) + layer_elems * n;
     void* out = static_cast<char*>(out_all) + layer_elems * out_elem_bytes * n;
-    // All layers share the lengths, so one plan serves every layer with the
-    // same number of KV heads (and hence the same workgroup count).
+    // All layers share the lengths, so one recorded plan serves every later
+    // layer with the same number of KV heads (and hence the same workgroup
+    // count) that also splits runs; layers with a workgroup per unit record
+    // and follow nothing.
     const int key = map->kv_count[n];
-    const int mode = key == planned_key ? 2 : 1;
+    const bool records = plan_records(plan(map, n, B, max_len_of(cache, max_len_hint), D));
+    const int mode = !records ? 0 : key == planned_key ? 2 : 1;
     if ((s = attention_impl(n, q, cache, map, ctx_lens, 1, out, out_dtype, max_len_hint, workspace,
                             workspace_bytes, stream, mode, fused_append ? k_new : nullptr,
                             fused_append ? v_new : nullptr, rope_cs, rope_half)) != MLKV_OK)
       return s;
-    planned_key = key;
+    if (records) planned_key = key;
   }
   return ok();
 }
@@ -1317,13 +1346,15 @@ mlkv_status mlkv_model_decode_step(mlkv_model* model, float* x, const mlkv_cache
                           stream)) != MLKV_OK)
       return st;
     const int key = map->kv_count[n];
-    const int mode = key == planned_key ? 2 : 1;
+    const bool records =
+        plan_records(plan(map, n, B, max_len_of(cache, max_len_hint), cache->head_dim));
+    const int mode = !records ? 0 : key == planned_key ? 2 : 1;
     if ((st = attention_impl(n, bf(w.q16), cache, map, ctx_lens, 1, bf(w.o16), MLKV_OUT_BF16,
                              max_len_hint, base + w.attn, w.attn_bytes, stream, mode,
                              fused_append ? bf(w.k16) : nullptr,
                              fused_append ? bf(w.v16) : nullptr)) != MLKV_OK)
       return st;
-    planned_key = key;
+    if (records) planned_key = key;
     return MLKV_OK;
   };
   const bool fused = use_fused(model, B);
