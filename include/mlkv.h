@@ -437,8 +437,11 @@ int mlkv_model_fused_path(const mlkv_model* model, int batch);
  * resident capacity if lower; capped at 128 per (sequence, KV head) and at
  * one per 4 tiles, at least one per (sequence, KV head); one workgroup for at
  * most 16 tiles; with at least as many (sequence, KV head) pairs as the
- * budget, exactly one workgroup per pair); `max_parts` bounds the workgroups
- * covering one sequence.
+ * budget, exactly one workgroup per pair).  A layer whose KV heads were all
+ * appended by earlier layers (it re-reads them) gets one eight-wave
+ * workgroup per pair instead when the pairs number at least 3/8 of the
+ * compute units and fewer than the budget.  `max_parts` bounds the
+ * workgroups covering one sequence.
  * Environment overrides, read on every call (tests and tuning):
  *   MLKV_WORKGROUPS=n   workgroup budget n instead of the device's;
  *   MLKV_COMBINE=kernel always merge split runs with the separate merge
@@ -449,8 +452,9 @@ int mlkv_model_fused_path(const mlkv_model* model, int batch);
  *                       units and at least one per compute unit);
  *   MLKV_COMBINE=fused  merge in place also when that costs up to half of
  *                       the workgroups;
- *   MLKV_WIDE=1         one run per unit on a wider workgroup (no partials,
- *                       no merge kernel);
+ *   MLKV_WIDE=1 / 0     one eight-wave workgroup per (sequence, KV head) in
+ *                       every layer below the budget / in no layer (the
+ *                       default: only in re-reading layers, as above);
  *   MLKV_QK=valu        q.K as bf16 dot products on the vector ALUs instead
  *                       of matrix-core (MFMA) instructions.
  * The workspace size from mlkv_workspace_bytes covers every choice.

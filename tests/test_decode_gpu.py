@@ -40,7 +40,9 @@ def plan_env(workgroups="", merge="", wide="", qk=""):
     MLKV_WORKGROUPS (workgroup budget), MLKV_COMBINE=kernel/fused (merge
     split runs in a separate kernel / in place even at a cost in
     workgroups), MLKV_WIDE=0/1 (one run per unit on a wide
-    workgroup: off / forced), MLKV_QK=valu (q.K on the vector ALUs)."""
+    workgroup: in no layer / in every layer; unset: in the layers that
+    re-read KV heads, when there are enough units), MLKV_QK=valu (q.K on
+    the vector ALUs)."""
     names = {"MLKV_WORKGROUPS": workgroups, "MLKV_COMBINE": merge, "MLKV_WIDE": wide,
              "MLKV_QK": qk}
     for k, v in names.items():
@@ -365,6 +367,7 @@ def test_step_mlkv2_empty_context_outputs_new_value_exactly():
 
 @pytest.mark.parametrize("wname,wide,qk", [("mlkv2_b1", "", ""), ("mlkv4_b128_ragged", "", ""),
                                            ("mlkv4_b128_ragged", "1", ""),
+                                           ("mlkv4_b128_ragged", "0", ""),
                                            ("mlkv4_b128_ragged", "", "valu"),
                                            ("mlkv4_b8_long", "", "")])
 def test_full_size_step_matches_oracle(wname, wide, qk):
@@ -485,6 +488,30 @@ def test_step_fused_append_across_tile_boundaries(D, m, g, workgroups, wide, qk)
     ref, k_ref, v_ref = _oracle_step(dw)
     assert np.array_equal(k_gpu, k_ref) and np.array_equal(v_gpu, v_ref), "cache differs"
     check_close(out, ref, f"fused append D{D} m{m} g{g} wg{workgroups} {wide} {qk}")
+
+
+def test_step_mixing_split_runs_and_a_workgroup_per_unit():
+    """By default a step gives the layers that only re-read KV heads (here
+    layers 1 and 3 of MLKV-2) one eight-wave workgroup per (sequence, KV
+    head), while the owning layers split runs on a recorded plan; the cache
+    and every layer's output match the oracle, with and without rotation."""
+    rng = np.random.default_rng(41)
+    ctx = rng.integers(0, 400, size=100).astype(np.int32)
+    ctx[:3] = [0, 31, 399]
+    w = synth.Workload("mixed", l=4, h=12, m=2, g=1, D=64, B=100, ctx=int(ctx.max()), seed=141)
+    dw = _with_contexts(DeviceWorkload(w), ctx)
+    S = dw.S
+    with plan_env():
+        p0 = dw.map.plan(0, w.B, S, w.D, S)[0]
+        p1 = dw.map.plan(1, w.B, S, w.D, S)[0]
+        assert p0 > w.B and p1 == w.B, (p0, p1)  # layer 0 splits runs, layer 1 one per unit
+        say("mixed plans: step")
+        out = _run_step(dw).cpu().numpy()
+    k_gpu, v_gpu = dw.read_cache()
+    ref, k_ref, v_ref = _oracle_step(dw)
+    assert np.array_equal(k_gpu, k_ref) and np.array_equal(v_gpu, v_ref), "cache differs"
+    check_close(out, ref, "mixed plans step")
+    _check_rope_step(dw, 16, "mixed plans rope")
 
 
 def test_step_owner_that_does_not_read_its_head():
