@@ -39,14 +39,17 @@ REF_COPY_BYTES = 256 << 20
 SLEEP_CYCLES = 40_000_000  # ~17 ms at 2.4 GHz: longer than the host needs to enqueue 10 steps
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix cores, published
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attention_kernel_traffic.md")
+# The decode kernels and the host planner that picks their launch shapes
+# (both decide the bytes a launch moves).
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2406_09297_amd", "csrc", f)
-                  for f in ("kernels.hip", "tile.h")]
+                  for f in ("kernels.hip", "tile.h", "mlkv.cpp")]
 
 
 def kernel_code_sha256() -> str:
-    """SHA-256 over the decode kernels' code (kernels.hip then tile.h) with
-    comments removed and whitespace collapsed, so that editing a comment does
-    not void a counter record taken from the same code."""
+    """SHA-256 over the decode kernels' code and the host planner
+    (kernels.hip, tile.h, then mlkv.cpp) with comments removed and whitespace
+    collapsed, so that editing a comment does not void a counter record taken
+    from the same code."""
     import hashlib
     import re
 
