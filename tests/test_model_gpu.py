@@ -204,6 +204,17 @@ def test_model_step_serving_batches_on_the_fused_kernels(B):
     _run_case(2, 4, 64, 256, 2, 1, B=B, ctx=ctx, seed=97, label=f"B{B}", fused=True)
 
 
+def test_model_step_re_reading_layers_on_a_workgroup_per_unit():
+    """MLKV-2 at 100 sequences: the layers that re-read the owner's KV heads
+    (1 and 3) run one eight-wave attention workgroup per (sequence, KV head)
+    inside the model step, the owning layers split runs on a recorded plan."""
+    ctx = [int(c) for c in np.random.default_rng(101).integers(0, 120, 100)]
+    mp = mlkv.Map.uniform(4, 4, 2, 1)
+    S = (max(ctx) + 1 + 63) // 64 * 64
+    assert mp.plan(1, 100, S, 64, S)[0] == 100 and mp.plan(0, 100, S, 64, S)[0] > 100
+    _run_case(4, 4, 64, 256, 2, 1, B=100, ctx=ctx, seed=102, label="B100 MLKV-2", fused=True)
+
+
 def test_model_step_ragged_ff_takes_the_library_path():
     """d_ff = 400 (not a multiple of 32, so no packed weights): library GEMMs."""
     _run_case(2, 4, 64, 400, 1, 1, B=3, ctx=[3, 40, 77], seed=98, label="ff400", fused=False)
