@@ -184,11 +184,15 @@ long workgroups_for(long resident, long units, long t_max, int min_tiles) {
 // workgroups per compute unit: on MI355X fewer, longer runs beat filling
 // every resident slot (fewer partials, longer pipelines), and a whole
 // multiple of the compute units keeps their bandwidth shares equal.
+long compute_units_or_fallback() {
+  const long cus = mlkv::compute_units();
+  return cus > 0 ? cus : kFallbackResident / 3;
+}
+
 long workgroup_budget(int head_dim) {
   long resident = mlkv::resident_workgroups(head_dim);
   if (resident <= 0) resident = kFallbackResident;
-  long cus = mlkv::compute_units();
-  if (cus <= 0) cus = kFallbackResident / 3;
+  const long cus = compute_units_or_fallback();
   if (resident > kWorkgroupsPerCu * cus) resident = kWorkgroupsPerCu * cus;
   if (const char* env = std::getenv("MLKV_WORKGROUPS")) {
     const long w = std::atol(env);
@@ -210,16 +214,15 @@ Plan plan(const mlkv_map* map, int layer, int batch, int max_len, int head_dim) 
   // split runs, schedule or merge) when the units fill at least 3/8 of the
   // compute units: on MI355X the Infinity Cache then serves those heads,
   // and the workgroups stream them faster than balanced split runs plus the
-  // merge of their partials (MLKV-4 at 128 ragged sequences: 10.3 against
-  // 11.1 us per such layer; MLKV-12 at 32 sequences of 2048: 17 % off the
-  // step).  Owning layers, which read their heads from HBM first, keep the
-  // split runs, as do maps without sharing across layers.  MLKV_WIDE=0 / 1
-  // turns this off / applies it to every layer.
+  // merge of their partials (12-layer steps back to back: MLKV-4 at 128
+  // ragged sequences 136 against 143 us, MLKV-12 at 32 sequences of 2048
+  // tokens 136 against 157 us).  Owning layers, which read their heads from
+  // HBM first, keep the split runs, as do maps without sharing across
+  // layers.  MLKV_WIDE=0 / 1 turns this off / applies it to every layer.
   const char* wide_env = std::getenv("MLKV_WIDE");
   const int wide_mode = wide_env ? (std::atoi(wide_env) != 0 ? 1 : 0) : -1;
+  const long cus = compute_units_or_fallback();
   if (wide_mode != 0 && units < resident) {
-    long cus = mlkv::compute_units();
-    if (cus <= 0) cus = kFallbackResident / 3;
     bool rereads = true;
     for (int c = 0; c < map->kv_count[layer]; ++c)
       rereads = rereads && map->owner_of[map->kv_begin[layer] + c] < layer;
@@ -242,8 +245,6 @@ Plan plan(const mlkv_map* map, int layer, int batch, int max_len, int head_dim) 
     mt = mt > kMinTiles ? mt : kMinTiles;
     const long g = workgroups_for(resident, units, t_max, static_cast<int>(mt));
     const long g_plain = workgroups_for(resident, units, t_max, kMinTiles);
-    long cus = mlkv::compute_units();
-    if (cus <= 0) cus = kFallbackResident / 3;
     bool accept = force_fused ? 2 * g >= resident || g >= units * ((pl.max_tiles + mt - 1) / mt)
                               : g >= g_plain;
     // A merge in place on fewer workgroups, at least one per compute unit
@@ -1540,9 +1541,7 @@ mlkv_status mlkv_profile_read_bandwidth(const void* buffer, size_t bytes, int re
   if (!aligned16(buffer)) return fail(MLKV_ERR_ALIGNMENT, "buffer must be 16-byte aligned");
   const size_t body = bytes / 16 * 16 - 16;  // the last 16 bytes hold the sink word
   uint32_t* sink = reinterpret_cast<uint32_t*>(static_cast<char*>(const_cast<void*>(buffer)) + body);
-  long cus = mlkv::compute_units();
-  if (cus <= 0) cus = kFallbackResident / 3;
-  const int workgroups = static_cast<int>(8 * cus);
+  const int workgroups = static_cast<int>(8 * compute_units_or_fallback());
   std::vector<hipEvent_t> ev(2 * static_cast<size_t>(reps), nullptr);
   mlkv_status s = MLKV_OK;
   for (auto& e : ev)
