@@ -280,6 +280,20 @@ Plan plan(const mlkv_map* map, int layer, int batch, int max_len, int head_dim) 
 // runs scheduled on the device; not a workgroup per unit or one workgroup.
 bool plan_records(const Plan& pl) { return !pl.direct && pl.n_blocks > 1; }
 
+// Layers of a step share the lengths, so a layer can follow the run items an
+// earlier layer recorded exactly when both plans split the same number of KV
+// heads' units the same way: equal keys.
+struct PlanKey {
+  int kv_count = -1, n_blocks = 0, min_tiles = 0, waves = 0, fused = 0;
+  bool operator==(const PlanKey& o) const {
+    return kv_count == o.kv_count && n_blocks == o.n_blocks && min_tiles == o.min_tiles &&
+           waves == o.waves && fused == o.fused;
+  }
+};
+PlanKey plan_key(const Plan& pl, int kv_count) {
+  return PlanKey{kv_count, pl.n_blocks, pl.min_tiles, pl.waves, pl.fused};
+}
+
 // The work-plan bound of a call: the hint, or the capacity for a hint <= 0.
 int max_len_of(const mlkv_cache* cache, int max_len_hint) {
   return max_len_hint <= 0 ? cache->capacity : max_len_hint;
@@ -905,7 +919,7 @@ mlkv_status decode_step_launch(const void* q_all, const void* k_new_all, const v
   const size_t out_elem_bytes = out_dtype == MLKV_OUT_BF16 ? 2 : 4;
   const uint16_t* k_new = static_cast<const uint16_t*>(k_new_all);
   const uint16_t* v_new = static_cast<const uint16_t*>(v_new_all);
-  int planned_key = -1;
+  PlanKey planned_key;
   for (int n = 0; n < map->l; ++n) {
     // The attention launch appends the heads the layer owns when it reads
     // them all; otherwise a separate append runs first.
@@ -920,12 +934,11 @@ mlkv_status decode_step_launch(const void* q_all, const void* k_new_all, const v
     }
     const void* q = static_cast<const uint16_t*>(q_all) + layer_elems * n;
     void* out = static_cast<char*>(out_all) + layer_elems * out_elem_bytes * n;
-    // All layers share the lengths, so one recorded plan serves every later
-    // layer with the same number of KV heads (and hence the same workgroup
-    // count) that also splits runs; layers with a workgroup per unit record
-    // and follow nothing.
-    const int key = map->kv_count[n];
-    const bool records = plan_records(plan(map, n, B, max_len_of(cache, max_len_hint), D));
+    // One recorded plan serves every later layer whose plan has the same
+    // key; layers with a workgroup per unit record and follow nothing.
+    const Plan pl = plan(map, n, B, max_len_of(cache, max_len_hint), D);
+    const bool records = plan_records(pl);
+    const PlanKey key = plan_key(pl, map->kv_count[n]);
     const int mode = !records ? 0 : key == planned_key ? 2 : 1;
     if ((s = attention_impl(n, q, cache, map, ctx_lens, 1, out, out_dtype, max_len_hint, workspace,
                             workspace_bytes, stream, mode, fused_append ? k_new : nullptr,
@@ -1335,8 +1348,8 @@ mlkv_status mlkv_model_decode_step(mlkv_model* model, float* x, const mlkv_cache
   auto u16 = [](const void* p) { return static_cast<const uint16_t*>(p); };
   // Attention of layer n with the owner's append (inside the attention launch
   // when the layer reads every head it owns).  The schedule is planned again
-  // only when the number of KV heads read changes.
-  auto layer_attention = [&](int n, int& planned_key) -> mlkv_status {
+  // only when the plan's key changes.
+  auto layer_attention = [&](int n, PlanKey& planned_key) -> mlkv_status {
     mlkv_status st;
     const int owned = map->own_count[n];
     const int own0 = owned ? map->own_begin[n] * D : 0;
@@ -1346,9 +1359,9 @@ mlkv_status mlkv_model_decode_step(mlkv_model* model, float* x, const mlkv_cache
         (st = append_impl(n, map, cache, bf(w.k16) + own0, bf(w.v16) + own0, kvD, ctx_lens,
                           stream)) != MLKV_OK)
       return st;
-    const int key = map->kv_count[n];
-    const bool records =
-        plan_records(plan(map, n, B, max_len_of(cache, max_len_hint), cache->head_dim));
+    const Plan pl = plan(map, n, B, max_len_of(cache, max_len_hint), cache->head_dim);
+    const bool records = plan_records(pl);
+    const PlanKey key = plan_key(pl, map->kv_count[n]);
     const int mode = !records ? 0 : key == planned_key ? 2 : 1;
     if ((st = attention_impl(n, bf(w.q16), cache, map, ctx_lens, 1, bf(w.o16), MLKV_OUT_BF16,
                              max_len_hint, base + w.attn, w.attn_bytes, stream, mode,
@@ -1359,7 +1372,7 @@ mlkv_status mlkv_model_decode_step(mlkv_model* model, float* x, const mlkv_cache
     return MLKV_OK;
   };
   const bool fused = use_fused(model, B);
-  int planned_key = -1;
+  PlanKey planned_key;
   for (int n = 0; n < map->l; ++n) {
     const mlkv_layer_weights& lw = model->layers[n];
     const int owned = map->own_count[n];
