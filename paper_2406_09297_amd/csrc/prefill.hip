@@ -34,26 +34,22 @@ namespace mlkv {
 // One 32-token tile against the wave's NB column blocks.  The tile's key and
 // value registers serve every block.  Phases: the scores of all blocks
 // (MFMA); the causal mask (MASK: the tile may cross some column's limit);
-// one wave-wide vote on whether any score exceeds its column's reference max
-// by more than kLazyRescale (each lane tests its own eight scores, so the
-// common case needs no cross-lane traffic); on a yes, the column maxima
-// through the wave and the rescale of the blocks that need it; then the
-// weights and the value products of all blocks.
-// Maximum of a lane's eight scores in four three-input maxima.  Written as
-// instructions because fmaxf on matrix-core results makes the compiler
-// canonicalise every input first (a max of the value with itself), which
-// doubled the count; the scores are finite or -inf, never NaN.
+// the weights' exponents y = scaled score - column reference (FIRST: the
+// wave's first tile sets each reference to its column's maximum); one
+// wave-wide vote on whether any y exceeds kLazyRescale (each lane tests its
+// own eight, so the common case needs no cross-lane traffic); on a yes, the
+// column maxima through the wave and the rescale of the blocks that need it;
+// then the weights and the value products of all blocks.
+// Maximum of a lane's eight values.  Over multiply-add results (canonical
+// floats) the compiler forms three-input maxima with no canonicalising maxes;
+// being compiler-visible, the reads of matrix-core results also get the wait
+// states the hardware requires after a matrix-core write.
 __device__ __forceinline__ float max8(const float (&x)[8]) {
-  float a, b, c;
-  asm("v_max3_f32 %0, %1, %2, %3" : "=v"(a) : "v"(x[0]), "v"(x[1]), "v"(x[2]));
-  asm("v_max3_f32 %0, %1, %2, %3" : "=v"(b) : "v"(x[3]), "v"(x[4]), "v"(x[5]));
-  asm("v_max3_f32 %0, %1, %2, %3" : "=v"(c) : "v"(x[6]), "v"(x[7]), "v"(a));
-  float m;
-  asm("v_max_f32 %0, %1, %2" : "=v"(m) : "v"(b), "v"(c));
-  return m;
+  return fmaxf(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])),
+               fmaxf(fmaxf(x[4], x[5]), fmaxf(x[6], x[7])));
 }
 
-template <int D, int NB, bool MASK>
+template <int D, int NB, bool MASK, bool FIRST>
 __device__ __forceinline__ void prefill_tile(WaveState<D> (&st)[NB], Tile<D>& t,
                                              const bf16x8 (&qf)[NB][Tile<D>::KK], int t0, int L,
                                              const int (&lim)[NB], int grp, float scale_log2) {
@@ -86,26 +82,49 @@ __device__ __forceinline__ void prefill_tile(WaveState<D> (&st)[NB], Tile<D>& t,
       }
     }
   }
-  float lmax[NB];
-  bool up = false;
-#pragma unroll
-  for (int c = 0; c < NB; ++c) {
-    lmax[c] = max8(x[c]);
-    up = up || fmaf(lmax[c], scale_log2, -st[c].m) > kLazyRescale;
-  }
-  if (__ballot(up)) {  // some column needs a new reference max
+  if (FIRST) {
+    // The wave's first tile (positions 0..31, which every column attends at
+    // position 0): each column's reference is its maximum scaled score.
 #pragma unroll
     for (int c = 0; c < NB; ++c) {
-      float cm = fmaxf(lmax[c], __shfl_xor(lmax[c], 16));
-      cm = fmaxf(cm, __shfl_xor(cm, 32)) * scale_log2;
-      const bool raise = cm > st[c].m + kLazyRescale;  // uniform over the column's lanes
-      if (__ballot(raise)) {
-        const float m_new = raise ? cm : st[c].m;
-        const float alpha = fast_exp2(st[c].m - m_new);  // 0 on the first tile
-        st[c].m = m_new;
-        st[c].den *= alpha;
+      const float lmax = max8(x[c]);
+      const float cm = fmaxf(lmax, __shfl_xor(lmax, 16));
+      st[c].m = fmaxf(cm, __shfl_xor(cm, 32)) * scale_log2;
+    }
+  }
+  // y = scaled score - reference (log2 units): the weights' exponents.
 #pragma unroll
-        for (int db = 0; db < DB; ++db) st[c].acc[db] *= alpha;
+  for (int c = 0; c < NB; ++c) {
+    const float neg_m = -st[c].m;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) x[c][e] = fmaf(x[c][e], scale_log2, neg_m);
+  }
+  if (!FIRST) {
+    float ymax[NB];
+    bool up = false;
+#pragma unroll
+    for (int c = 0; c < NB; ++c) {
+      ymax[c] = max8(x[c]);
+      up = up || ymax[c] > kLazyRescale;
+    }
+    if (__ballot(up)) {  // some column needs a new reference
+#pragma unroll
+      for (int c = 0; c < NB; ++c) {
+        float cm = fmaxf(ymax[c], __shfl_xor(ymax[c], 16));
+        cm = fmaxf(cm, __shfl_xor(cm, 32));
+        const bool raise = cm > kLazyRescale;  // uniform over the column's lanes
+        if (__ballot(raise)) {
+          // The reference moves up by the column's excess d: weights and the
+          // running sums are scaled by 2^-d.
+          const float d = raise ? cm : 0.f;
+          const float alpha = fast_exp2(-d);
+          st[c].m += d;
+          st[c].den *= alpha;
+#pragma unroll
+          for (int db = 0; db < DB; ++db) st[c].acc[db] *= alpha;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) x[c][e] -= d;
+        }
       }
     }
   }
@@ -113,10 +132,8 @@ __device__ __forceinline__ void prefill_tile(WaveState<D> (&st)[NB], Tile<D>& t,
 #pragma unroll
   for (int c = 0; c < NB; ++c) {
     u16x8 pbits;
-    const float neg_m = -st[c].m;
 #pragma unroll
-    for (int e = 0; e < 8; ++e)
-      pbits[e] = f32_to_bf16_bits(fast_exp2(fmaf(x[c][e], scale_log2, neg_m)));
+    for (int e = 0; e < 8; ++e) pbits[e] = f32_to_bf16_bits(fast_exp2(x[c][e]));
     const bf16x8 pf = as_bf16(pbits);
     st[c].den = mfma_bf16(as_bf16(ones), pf, st[c].den);
 #pragma unroll
@@ -260,10 +277,12 @@ void prefill_kernel(PrefillParams p) {
     if (it < n_tiles) {
       Tile<D> t;
       tile_from_lds<D>(t, lds[it & 1], col, grp);
-      if (it >= first_masked)
-        prefill_tile<D, NB, true>(st, t, qf, it * kTile, L, lim, grp, p.scale_log2);
+      if (it == 0)
+        prefill_tile<D, NB, true, true>(st, t, qf, 0, L, lim, grp, p.scale_log2);
+      else if (it >= first_masked)
+        prefill_tile<D, NB, true, false>(st, t, qf, it * kTile, L, lim, grp, p.scale_log2);
       else
-        prefill_tile<D, NB, false>(st, t, qf, it * kTile, L, lim, grp, p.scale_log2);
+        prefill_tile<D, NB, false, false>(st, t, qf, it * kTile, L, lim, grp, p.scale_log2);
     }
     if (more) stage_store<D>(stg, lds[(it + 1) & 1]);
     __syncthreads();
