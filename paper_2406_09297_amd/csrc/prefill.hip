@@ -141,68 +141,70 @@ __device__ __forceinline__ void prefill_tile(WaveState<D> (&st)[NB], Tile<D>& t,
   }
 }
 
-// Key/value tiles staged in LDS, shared by the workgroup's four waves: key
-// rows padded to D + 8 and value channel rows (32 tokens) to 40 elements, so
-// that the sixteen lanes reading sixteen rows at one offset hit distinct
-// banks.
-template <int D>
-struct PrefillTileLds {
-  static constexpr int KSTR = D + 8;
-  static constexpr int VSTR = kTile + 8;
-  alignas(16) uint16_t k[kTile * KSTR];
-  alignas(16) uint16_t v[D * VSTR];
-};
-
-// Global -> register staging of one tile: thread i holds CH 16-byte chunks
-// of the key rows and CH of the value block (CH = D / 64).
-template <int D>
-struct TileStage {
-  static constexpr int CH = D / 64;
-  u16x8 k[CH], v[CH];
-};
+// Key/value tiles staged in LDS by direct global-to-LDS loads
+// (global_load_lds_dwordx4: lane l of a wave writes its 16 bytes at the
+// wave-uniform LDS address + 16 l), double-buffered and shared by the
+// workgroup's four waves; no registers hold a tile in transit and no LDS
+// store instructions are issued.  Key chunks keep the plane's order, in
+// which a wave's operand reads are lane-contiguous; the value chunk
+// of channel c and 8-token part p sits at slot 4 c + (p ^ vswz(c)), so that
+// the sixteen lanes reading channels c .. c + 15 at one part hit distinct
+// banks (for both 32- and 64-bank phase groupings).
+constexpr int kRing = 2;
+__device__ __forceinline__ int vswz(int c) { return ((c >> 1) ^ (c >> 3)) & 3; }
 
 template <int D>
-__device__ __forceinline__ void stage_load(TileStage<D>& s, const uint16_t* kbase,
+struct PrefillRing {
+  alignas(16) uint16_t k[kRing][kTile * D];
+  alignas(16) uint16_t v[kRing][kTile * D];
+};
+
+// Wait until this wave's vector memory loads, the direct loads included,
+// have landed (vmcnt(0); the other counters are left alone).
+__device__ __forceinline__ void wait_loads() { __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8)); }
+
+// A shared-memory pointer as the LDS address the direct loads take.
+__device__ __forceinline__ __attribute__((address_space(3))) void* lds_address(uint16_t* p) {
+  return (__attribute__((address_space(3))) void*)p;
+}
+
+// Requests the tile at position t0 into buffer s: each thread issues D/64
+// key and D/64 value chunk loads, 2 D/64 instructions per wave.
+template <int D>
+__device__ __forceinline__ void ring_issue(PrefillRing<D>& rg, int s, const uint16_t* kbase,
                                            const uint16_t* vbase, int t0) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
 #pragma unroll
-  for (int u = 0; u < TileStage<D>::CH; ++u) {
-    const int idx = threadIdx.x + u * 256;  // chunk of the tile's 4*D (K) and 4*D (V) chunks
-    s.k[u] = load16(kbase + static_cast<size_t>(t0) * D + idx * 8);
-    s.v[u] = load16(vbase + static_cast<size_t>(t0) * D + idx * 8);
+  for (int u = 0; u < D / 64; ++u) {
+    const int slot0 = u * 256 + wave * 64;  // this wave's 64 slots (1 KB) of the buffer
+    const int q = slot0 + lane;
+    __builtin_amdgcn_global_load_lds(
+        static_cast<const void*>(kbase + static_cast<size_t>(t0) * D + q * 8),
+        lds_address(&rg.k[s][slot0 * 8]), 16, 0, 0);
+    const int c = q >> 2, part = (q & 3) ^ vswz(c);
+    __builtin_amdgcn_global_load_lds(
+        static_cast<const void*>(vbase + static_cast<size_t>(t0) * D + (c * 4 + part) * 8),
+        lds_address(&rg.v[s][slot0 * 8]), 16, 0, 0);
   }
 }
 
-template <int D>
-__device__ __forceinline__ void stage_store(const TileStage<D>& s, PrefillTileLds<D>& lds) {
-#pragma unroll
-  for (int u = 0; u < TileStage<D>::CH; ++u) {
-    const int idx = threadIdx.x + u * 256;
-    // key chunk idx of the tile (kchunk order): its token row and channel group
-    const int kr = kchunk_token<D>(idx), kc = kchunk_group<D>(idx);
-    *reinterpret_cast<u16x8*>(&lds.k[kr * PrefillTileLds<D>::KSTR + kc * 8]) = s.k[u];
-    // value chunk idx: channel idx / 4, tokens (idx % 4) * 8 (channel-major block)
-    const int vc = idx >> 2, vp = idx & 3;
-    *reinterpret_cast<u16x8*>(&lds.v[vc * PrefillTileLds<D>::VSTR + vp * 8]) = s.v[u];
-  }
-}
-
-// A wave's MFMA operands of one tile from LDS (the same register layout as
+// A wave's MFMA operands of one tile from buffer s (the register layout of
 // load_tile: permuted key rows, V^T rows).
 template <int D>
-__device__ __forceinline__ void tile_from_lds(Tile<D>& t, const PrefillTileLds<D>& lds, int col,
-                                              int grp) {
+__device__ __forceinline__ void tile_from_ring(Tile<D>& t, const PrefillRing<D>& rg, int s, int col,
+                                               int grp) {
+  const int lane = grp * 16 + col;
 #pragma unroll
-  for (int sb = 0; sb < 2; ++sb) {
-    const int tok = (col >> 2) * 8 + sb * 4 + (col & 3);
+  for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
     for (int kk = 0; kk < Tile<D>::KK; ++kk)
       t.k[sb][kk] = *reinterpret_cast<const u16x8*>(
-          &lds.k[tok * PrefillTileLds<D>::KSTR + grp * 8 + kk * 32]);
-  }
+          &rg.k[s][((sb * Tile<D>::KK + kk) * 64 + lane) * 8]);
 #pragma unroll
-  for (int db = 0; db < Tile<D>::DB; ++db)
-    t.v[db] = *reinterpret_cast<const u16x8*>(
-        &lds.v[(db * 16 + col) * PrefillTileLds<D>::VSTR + grp * 8]);
+  for (int db = 0; db < Tile<D>::DB; ++db) {
+    const int c = db * 16 + col;
+    t.v[db] = *reinterpret_cast<const u16x8*>(&rg.v[s][(c * 4 + (grp ^ vswz(c))) * 8]);
+  }
 }
 
 template <int D, int NB>
@@ -210,7 +212,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(D == 64 ? 4
 void prefill_kernel(PrefillParams p) {
   constexpr int KK = Tile<D>::KK, DB = Tile<D>::DB;
   constexpr int WAVE_ROWS = 16 * NB;
-  __shared__ PrefillTileLds<D> lds[2];
+  __shared__ PrefillRing<D> rg;
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int col = lane & 15;
@@ -238,9 +240,7 @@ void prefill_kernel(PrefillParams p) {
   const size_t seq = static_cast<size_t>(kv) * p.B + b;
   const uint16_t* kbase = p.k + seq * p.S * D;
   const uint16_t* vbase = p.v + seq * p.S * D;
-
-  TileStage<D> stg;
-  stage_load<D>(stg, kbase, vbase, 0);
+  ring_issue<D>(rg, 0, kbase, vbase, 0);  // every workgroup has at least one tile
 
   // Column block c: row row0 + 16c + col, its token, head and causal limit
   // (rows past the end: token 0, zero query, output not stored).
@@ -266,17 +266,18 @@ void prefill_kernel(PrefillParams p) {
 #pragma unroll
     for (int db = 0; db < DB; ++db) st[c].acc[db] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
-  stage_store<D>(stg, lds[0]);
-  __syncthreads();
-
-  // Tile it sits in lds[it & 1]; the next tile's global loads are in flight
-  // while it is used, and land in the other buffer before the barrier.
+  // Tile it sits in buffer it & 1.  At the barrier this wave's direct loads
+  // have landed (waited for explicitly; the barrier's release fence would
+  // wait for them too, as they count as writes to LDS), so every wave's part
+  // of tile it is there, and every wave is done with tile it - 1, whose
+  // buffer then takes tile it + 1 while tile it is used.
   for (int it = 0; it < n_tiles_wg; ++it) {
-    const bool more = it + 1 < n_tiles_wg;
-    if (more) stage_load<D>(stg, kbase, vbase, (it + 1) * kTile);
+    wait_loads();
+    __syncthreads();
+    if (it + 1 < n_tiles_wg) ring_issue<D>(rg, (it + 1) & 1, kbase, vbase, (it + 1) * kTile);
     if (it < n_tiles) {
       Tile<D> t;
-      tile_from_lds<D>(t, lds[it & 1], col, grp);
+      tile_from_ring<D>(t, rg, it & 1, col, grp);
       if (it == 0)
         prefill_tile<D, NB, true, true>(st, t, qf, 0, L, lim, grp, p.scale_log2);
       else if (it >= first_masked)
@@ -284,8 +285,6 @@ void prefill_kernel(PrefillParams p) {
       else
         prefill_tile<D, NB, false, false>(st, t, qf, it * kTile, L, lim, grp, p.scale_log2);
     }
-    if (more) stage_store<D>(stg, lds[(it + 1) & 1]);
-    __syncthreads();
   }
 
   // Lane (col, grp) holds channels db*16 + 4*grp .. +3 of its row in each block.
