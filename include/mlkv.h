@@ -454,9 +454,7 @@ int mlkv_model_fused_path(const mlkv_model* model, int batch);
  *                       the workgroups;
  *   MLKV_WIDE=1 / 0     one eight-wave workgroup per (sequence, KV head) in
  *                       every layer below the budget / in no layer (the
- *                       default: only in re-reading layers, as above);
- *   MLKV_QK=valu        q.K as bf16 dot products on the vector ALUs instead
- *                       of matrix-core (MFMA) instructions.
+ *                       default: only in re-reading layers, as above).
  * The workspace size from mlkv_workspace_bytes covers every choice.
  * Returns MLKV_ERR_* on invalid arguments. */
 mlkv_status mlkv_plan(const mlkv_map* map, int layer, int batch, int capacity, int head_dim,

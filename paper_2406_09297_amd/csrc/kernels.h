@@ -98,7 +98,6 @@ struct AttnParams {
   int merge_first;           // partial slots the merge reads before it knows the run count
   int waves;                 // waves per attention workgroup: 4, or wide_waves() for single runs
   int direct;                // 1: n_blocks = B*n_groups, workgroup g is unit g (no schedule)
-  int qk_valu;               // 1: q.K on the vector ALUs (dot2) instead of MFMA (four-wave layout)
   float scale_log2;          // log2(e) / sqrt(D)
   // Fused append (owning layer of a decode step), k_new null when none: row
   // of KV head kv for sequence b at k_new + b*new_stride + kv*D; heads

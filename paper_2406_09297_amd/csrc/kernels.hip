@@ -16,8 +16,6 @@
 //   combine_kernel    log-sum-exp merge of a unit's partials, fixed order
 //                     (when they were not merged in place)
 //   fill_kernel       zero fill of a workspace
-//   (QK_VALU: a variant computing q.K with bf16 dot2 on the vector ALUs,
-//   kept to compare with the matrix-core path.)
 //
 // Math (paper Section 2.1 Eqs. 1-3; MLKV head map Section 3 Eqs. 13-17):
 //   o = sum_t softmax_t(q.k_t / sqrt(D)) v_t.  Scores are kept in the log2
@@ -257,7 +255,7 @@ struct alignas(16) RunItem {
 constexpr int kStageFloats = 8192;
 constexpr int kStageMl = 512;
 
-template <int D, int W, bool QK_VALU>
+template <int D, int W>
 struct alignas(16) AttnShared {
   union {  // phases: schedule, then the waves' merge, then (last run only) staging
     SchedShared sc;
@@ -272,10 +270,6 @@ struct alignas(16) AttnShared {
   RunItem run;                          // this workgroup's run, from the schedule
   alignas(16) uint16_t new_row[2 * D];  // newest token's key and value (fused append)
   double2 rope[kMaxRopePairs];          // the sequence's rotary (cos, sin) pairs
-  // QK_VALU: the group's queries (16 heads, zero-padded) and each wave's
-  // score block [16 heads][32 tokens].
-  alignas(16) uint16_t q_lds[QK_VALU ? 16 * D : 8];
-  alignas(16) float s_lds[QK_VALU ? W * 16 * kTile : 4];
   int last;
 };
 
@@ -437,13 +431,13 @@ __device__ void schedule(const AttnParams& p, SchedShared& sm, RunItem& run, int
 
 // Register budget: at least 3 waves per SIMD for D = 64 and 2 for D = 128
 // with four-wave workgroups (12 / 8 waves per compute unit in flight).
-template <int D, int W, bool QK_VALU>
+template <int D, int W>
 __global__ __launch_bounds__(W * 64) __attribute__((amdgpu_waves_per_eu(D == 64 ? 3 : 2)))
 void attention_kernel(AttnParams p) {
   constexpr int KK = Tile<D>::KK, DB = Tile<D>::DB;
   constexpr int NT = W * 64;  // threads
   constexpr int D4 = D / 4;    // four-channel groups of a head
-  __shared__ AttnShared<D, W, QK_VALU> sm;
+  __shared__ AttnShared<D, W> sm;
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int col = lane & 15;  // query head inside the group / MFMA row
@@ -535,7 +529,7 @@ void attention_kernel(AttnParams p) {
 #pragma unroll
   for (int db = 0; db < DB; ++db) st.acc[db] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  if (it < k1) load_tile<D, QK_VALU>(ta, kbase, vbase, it * kTile, col, grp);
+  if (it < k1) load_tile<D>(ta, kbase, vbase, it * kTile, col, grp);
   if (single) {  // the actual length (the tile above may go unused)
     L = attended_len(p, 0);
     k1 = tiles_of(L);
@@ -553,23 +547,6 @@ void attention_kernel(AttnParams p) {
     for (int kk = 0; kk < KK; ++kk)
       qraw[kk] = rotate_chunk(qraw[kk], qpart[kk], grp * 8 + kk * 32, rope_half, cs_lds);
   }
-  if (QK_VALU) {  // stage the group's queries (padded heads zero) and zero padded score rows
-    for (int idx = threadIdx.x; idx < 16 * D / 8; idx += NT) {
-      const int hh = idx / (D / 8);
-      const int c = (idx - hh * (D / 8)) * 8;
-      u16x8 v = {0, 0, 0, 0, 0, 0, 0, 0};
-      if (hh < p.G) {
-        const uint16_t* row = p.q + (static_cast<size_t>(b) * p.h + head0 + hh) * D;
-        v = load16(row + c);
-        if (c < 2 * rope_half)
-          v = rotate_chunk(v, load16(row + partner_chunk(c, rope_half)), c, rope_half, cs_lds);
-      }
-      *reinterpret_cast<u16x8*>(&sm.q_lds[hh * D + c]) = v;
-    }
-    for (int idx = threadIdx.x; idx < W * 16 * kTile; idx += NT)
-      if ((idx / kTile) % 16 >= p.G) sm.s_lds[idx] = 0.f;
-    __syncthreads();
-  }
   bf16x8 qf[KK];
 #pragma unroll
   for (int kk = 0; kk < KK; ++kk) {
@@ -577,7 +554,6 @@ void attention_kernel(AttnParams p) {
     qf[kk] = as_bf16(valid ? qraw[kk] : zero);  // padded heads score zero
   }
   const bool has_tiles = it < k1;
-  float* const s_wave = sm.s_lds + (QK_VALU ? wave * 16 * kTile : 0);
 
   // Fused append of the owning layer (Section 2.4): the last run of each
   // owned unit writes the newest token's K/V row into slot lens[b] +
@@ -619,22 +595,20 @@ void attention_kernel(AttnParams p) {
     for (;;) {
       const int nxt = it + W;
       if (nxt >= k1) break;  // ta holds the last tile
-      load_tile<D, QK_VALU>(tb, kbase, vbase, nxt * kTile, col, grp);
-      process_tile<D, false, QK_VALU>(st, ta, qf, it * kTile, L, col, grp, p.scale_log2, -1,
-                                      nullptr, sm.q_lds, s_wave, p.G);
+      load_tile<D>(tb, kbase, vbase, nxt * kTile, col, grp);
+      process_tile<D, false>(st, ta, qf, it * kTile, L, col, grp, p.scale_log2, -1, nullptr);
       it = nxt;
       const int nx2 = it + W;
       if (nx2 >= k1) {  // tb holds the last tile
         ta = tb;
         break;
       }
-      load_tile<D, QK_VALU>(ta, kbase, vbase, nx2 * kTile, col, grp);
-      process_tile<D, false, QK_VALU>(st, tb, qf, it * kTile, L, col, grp, p.scale_log2, -1,
-                                      nullptr, sm.q_lds, s_wave, p.G);
+      load_tile<D>(ta, kbase, vbase, nx2 * kTile, col, grp);
+      process_tile<D, false>(st, tb, qf, it * kTile, L, col, grp, p.scale_log2, -1, nullptr);
       it = nx2;
     }
-    process_tile<D, true, QK_VALU>(st, ta, qf, it * kTile, L, col, grp, p.scale_log2, pos_new,
-                                   sm.new_row, sm.q_lds, s_wave, p.G);
+    process_tile<D, true>(st, ta, qf, it * kTile, L, col, grp, p.scale_log2, pos_new,
+                          sm.new_row);
   }
 
   // Merge the four waves through LDS.
@@ -912,11 +886,11 @@ hipError_t launch_append(const AppendParams& p, int head_dim, int owned_count,
   return hipGetLastError();
 }
 
-template <int D, int W, bool QK_VALU = false>
+template <int D, int W>
 static void launch_attention_t(const AttnParams& p, hipStream_t stream, hipEvent_t start,
                                hipEvent_t stop) {
   const dim3 grid(p.n_blocks), block(W * 64);
-  auto kernel = attention_kernel<D, W, QK_VALU>;
+  auto kernel = attention_kernel<D, W>;
   if (start)  // timed: events recorded with the dispatch itself
     hipExtLaunchKernelGGL(kernel, grid, block, 0, stream, start, stop, 0, p);
   else
@@ -929,15 +903,11 @@ hipError_t launch_attention_main(const AttnParams& p, int head_dim, hipStream_t 
   if (head_dim == 64) {
     if (wide)
       launch_attention_t<64, kWideWaves>(p, stream, start, stop);
-    else if (p.qk_valu)
-      launch_attention_t<64, kWaves, true>(p, stream, start, stop);
     else
       launch_attention_t<64, kWaves>(p, stream, start, stop);
   } else {
     if (wide)
       launch_attention_t<128, kWideWaves>(p, stream, start, stop);
-    else if (p.qk_valu)
-      launch_attention_t<128, kWaves, true>(p, stream, start, stop);
     else
       launch_attention_t<128, kWaves>(p, stream, start, stop);
   }
@@ -986,8 +956,8 @@ int resident_workgroups(int head_dim) {
     return 0;
   const hipError_t err =
       head_dim == 64
-          ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attention_kernel<64, kWaves, false>, kThreads, 0)
-          : hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attention_kernel<128, kWaves, false>, kThreads, 0);
+          ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attention_kernel<64, kWaves>, kThreads, 0)
+          : hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attention_kernel<128, kWaves>, kThreads, 0);
   if (err != hipSuccess) return 0;
   v = cus * per_cu;
   slot.store(v, std::memory_order_relaxed);

@@ -435,7 +435,6 @@ mlkv_status attention_impl(int layer, const void* q, const mlkv_cache* cache, co
   p.fused = pl.fused;
   p.waves = pl.waves;
   p.direct = pl.direct;
-  if (const char* env = std::getenv("MLKV_QK")) p.qk_valu = std::strcmp(env, "valu") == 0 ? 1 : 0;
   // One wave merges a row when units average at most 16 runs, else four;
   // the merge's first reads cover twice the average runs per unit.
   const long units = static_cast<long>(B) * map->kv_count[layer];

@@ -33,37 +33,6 @@ __device__ __forceinline__ f32x4 mfma_bf16(bf16x8 a, bf16x8 b, f32x4 c) {
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
-typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-
-// Dot product of 8 bf16 pairs' worth of channels in fp32 (exact products).
-__device__ __forceinline__ float dot8_bf16(u16x8 a, u16x8 b) {
-  const bf16x8 x = as_bf16(a), y = as_bf16(b);
-  float c = 0.f;
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-    c = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{x[2 * i], x[2 * i + 1]}, bf16x2{y[2 * i], y[2 * i + 1]},
-                                        c, false);
-  return c;
-}
-
-// DPP move of a float within rows of 16 lanes.
-template <int CTRL>
-__device__ __forceinline__ float dpp(float v) {
-  return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), CTRL, 0xF,
-                                                            0xF, false));
-}
-
-// Sum over aligned groups of N (8 or 16) consecutive lanes, left in every
-// lane of the group: swaps inside quads, then half-row and row mirrors.
-template <int N>
-__device__ __forceinline__ float row_group_sum(float v) {
-  v += dpp<0xB1>(v);   // quad_perm [1,0,3,2]
-  v += dpp<0x4E>(v);   // quad_perm [2,3,0,1]
-  v += dpp<0x141>(v);  // row_half_mirror: lane i <-> 7-i within 8
-  if (N == 16) v += dpp<0x140>(v);  // row_mirror: lane i <-> 15-i within 16
-  return v;
-}
-
 // Device-scope (all XCDs) stores and loads for partials merged inside the
 // attention kernel: on CDNA3/4 the scope travels with each access (SC bits),
 // so no L2 writeback or invalidate is needed, only completion of the stores
@@ -107,18 +76,6 @@ template <int D>
 __device__ __forceinline__ int kchunk(int u, int c) {
   return ((((u >> 2) & 1) * (D / 32) + (c >> 2)) * 64) + (c & 3) * 16 + ((u >> 3) << 2) + (u & 3);
 }
-// ... and its inverse: chunk q holds token (kchunk_token) and channel group
-// (kchunk_group) of the tile.
-template <int D>
-__device__ __forceinline__ int kchunk_token(int q) {
-  const int col = q & 15, sb = (q >> 6) / (D / 32);
-  return ((col >> 2) << 3) + sb * 4 + (col & 3);
-}
-template <int D>
-__device__ __forceinline__ int kchunk_group(int q) {
-  return ((q >> 4) & 3) + 4 * ((q >> 6) % (D / 32));
-}
-
 template <int D>
 struct Tile {
   static constexpr int KK = D / 32;  // k-steps of the q.K product
@@ -130,27 +87,15 @@ struct Tile {
 // Score block sb, MFMA row rr holds token 8*(rr/4) + 4*sb + rr%4, so the result
 // lane (col, grp) ends up with tokens 8*grp + 4*sb + i: the P^T k-slots it owns.
 //
-// QK_VALU (the VALU dot-product variant of q.K): the tile's key rows are read
-// as contiguous 1 KB pieces instead; lane l of piece j holds channels
-// 8*(l % (D/8)) .. +7 of row j*(512/D) + l/(D/8).
-template <int D, bool QK_VALU>
+template <int D>
 __device__ __forceinline__ void load_tile(Tile<D>& t, const uint16_t* kbase,
                                           const uint16_t* vbase, int t0, int col, int grp) {
-  const uint16_t* ktile = kbase + static_cast<size_t>(t0) * D;
-  if (QK_VALU) {  // rows in order: lane l of piece j holds row j * 512 / D + l / (D / 8)
-    constexpr int LPR = D / 8, RPP = 512 / D;
-    const int lane = grp * 16 + col;
+  // The key operands: one contiguous 1 KB piece per score block and k-step.
+  const uint16_t* kt = kbase + static_cast<size_t>(t0) * D + (grp * 16 + col) * 8;
 #pragma unroll
-    for (int j = 0; j < 2 * Tile<D>::KK; ++j)
-      t.k[j / Tile<D>::KK][j % Tile<D>::KK] =
-          load16(ktile + kchunk<D>(j * RPP + lane / LPR, lane % LPR) * 8);
-  } else {  // the MFMA operands: one contiguous 1 KB piece per block and k-step
-    const uint16_t* kt = ktile + (grp * 16 + col) * 8;
+  for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
-    for (int sb = 0; sb < 2; ++sb)
-#pragma unroll
-      for (int kk = 0; kk < Tile<D>::KK; ++kk) t.k[sb][kk] = load16(kt + (sb * Tile<D>::KK + kk) * 512);
-  }
+    for (int kk = 0; kk < Tile<D>::KK; ++kk) t.k[sb][kk] = load16(kt + (sb * Tile<D>::KK + kk) * 512);
   const uint16_t* vblk = vbase + static_cast<size_t>(t0) * D + grp * 8;
 #pragma unroll
   for (int db = 0; db < Tile<D>::DB; ++db) t.v[db] = load16(vblk + (db * 16 + col) * kTile);
@@ -172,33 +117,18 @@ constexpr float kLazyRescale = 8.f;
 // ragged end of a sequence or the newest token.  pos_new >= 0: position of
 // the newest token, whose key and value are taken from new_row (LDS: key
 // then value, D each) instead of the loaded tile.
-// CAUSAL (prefill): this lane's column attends positions <= lim only (its own
-// causal limit); positions >= L still take no value.  LAST then marks a tile
-// that may cross some column's limit.
-template <int D, bool LAST, bool QK_VALU, bool CAUSAL = false>
+template <int D, bool LAST>
 __device__ __forceinline__ void process_tile(WaveState<D>& st, Tile<D>& t, const bf16x8* qf,
                                              int t0, int L, int col, int grp, float scale_log2,
-                                             int pos_new, const uint16_t* new_row,
-                                             const uint16_t* q_lds, float* s_lds, int G,
-                                             int lim = 0) {
+                                             int pos_new, const uint16_t* new_row) {
   constexpr int KK = Tile<D>::KK, DB = Tile<D>::DB;
-  constexpr int LPR = D / 8;         // QK_VALU: lanes holding one key row
-  constexpr int RPP = 512 / D;       // QK_VALU: rows per 1 KB piece
-  const int lane = grp * 16 + col;
   if (LAST && pos_new >= t0 && pos_new < t0 + kTile) {
-    if (QK_VALU) {
 #pragma unroll
-      for (int j = 0; j < 2 * KK; ++j)
-        if (t0 + j * RPP + lane / LPR == pos_new)
-          t.k[j / KK][j % KK] = *reinterpret_cast<const u16x8*>(new_row + (lane % LPR) * 8);
-    } else {
+    for (int sb = 0; sb < 2; ++sb) {
+      if (t0 + (col >> 2) * 8 + sb * 4 + (col & 3) == pos_new) {
 #pragma unroll
-      for (int sb = 0; sb < 2; ++sb) {
-        if (t0 + (col >> 2) * 8 + sb * 4 + (col & 3) == pos_new) {
-#pragma unroll
-          for (int kk = 0; kk < KK; ++kk)
-            t.k[sb][kk] = *reinterpret_cast<const u16x8*>(new_row + grp * 8 + kk * 32);
-        }
+        for (int kk = 0; kk < KK; ++kk)
+          t.k[sb][kk] = *reinterpret_cast<const u16x8*>(new_row + grp * 8 + kk * 32);
       }
     }
     const int e_new = pos_new - t0 - grp * 8;  // in [0, 8) for the lanes holding it
@@ -211,36 +141,7 @@ __device__ __forceinline__ void process_tile(WaveState<D>& st, Tile<D>& t, const
     }
   }
   float x[8];  // raw scores q.k of tokens 8*grp + e
-  if (QK_VALU) {
-    // Per head: each lane dots its 8 channels of each held row with q
-    // (v_dot2 on bf16 pairs, fp32 sums), the LPR lanes of a row add up by
-    // DPP, and the row scores go through this wave's LDS block s_lds[16][32]
-    // to the lanes that use them as P^T k-slots.
-    const int c8 = lane % LPR;
-    for (int hh = 0; hh < G; ++hh) {
-      const u16x8 qq = *reinterpret_cast<const u16x8*>(q_lds + hh * D + c8 * 8);
-      float part[2 * KK];
-#pragma unroll
-      for (int j = 0; j < 2 * KK; ++j) part[j] = dot8_bf16(t.k[j / KK][j % KK], qq);
-#pragma unroll
-      for (int j = 0; j < 2 * KK; ++j) part[j] = row_group_sum<LPR>(part[j]);
-      if (c8 == hh % LPR) {
-#pragma unroll
-        for (int j = 0; j < 2 * KK; ++j) s_lds[hh * kTile + j * RPP + lane / LPR] = part[j];
-      }
-    }
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    const f32x4 lo = *reinterpret_cast<const f32x4*>(s_lds + col * kTile + grp * 8);
-    const f32x4 hi = *reinterpret_cast<const f32x4*>(s_lds + col * kTile + grp * 8 + 4);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      x[i] = lo[i];
-      x[4 + i] = hi[i];
-    }
-    __builtin_amdgcn_wave_barrier();  // reads done before the next tile's writes
-  } else {
+  {
     f32x4 s[2];
 #pragma unroll
     for (int sb = 0; sb < 2; ++sb) {
@@ -254,19 +155,7 @@ __device__ __forceinline__ void process_tile(WaveState<D>& st, Tile<D>& t, const
       for (int i = 0; i < 4; ++i) x[sb * 4 + i] = s[sb][i];
   }
 
-  if constexpr (CAUSAL) {
-    if (LAST) {  // positions past the column's limit take no weight, positions >= L no value
-      const int first = t0 + grp * 8;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        if (first + e > lim) x[e] = -INFINITY;
-        if (first + e >= L) {
-#pragma unroll
-          for (int db = 0; db < DB; ++db) t.v[db][e] = 0;
-        }
-      }
-    }
-  } else if (LAST && t0 + kTile > L) {  // ragged tail: positions >= L take no weight and no value
+  if (LAST && t0 + kTile > L) {  // ragged tail: positions >= L take no weight and no value
     const int first = t0 + grp * 8;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {

@@ -35,16 +35,14 @@ def small(name, **kw):
 
 
 @contextlib.contextmanager
-def plan_env(workgroups="", merge="", wide="", qk=""):
+def plan_env(workgroups="", merge="", wide=""):
     """Launch-plan overrides read by the library on every call:
     MLKV_WORKGROUPS (workgroup budget), MLKV_COMBINE=kernel/fused (merge
     split runs in a separate kernel / in place even at a cost in
     workgroups), MLKV_WIDE=0/1 (one run per unit on a wide
     workgroup: in no layer / in every layer; unset: in the layers that
-    re-read KV heads, when there are enough units), MLKV_QK=valu (q.K on
-    the vector ALUs)."""
-    names = {"MLKV_WORKGROUPS": workgroups, "MLKV_COMBINE": merge, "MLKV_WIDE": wide,
-             "MLKV_QK": qk}
+    re-read KV heads, when there are enough units)."""
+    names = {"MLKV_WORKGROUPS": workgroups, "MLKV_COMBINE": merge, "MLKV_WIDE": wide}
     for k, v in names.items():
         if v:
             os.environ[k] = v
@@ -154,20 +152,19 @@ def test_length_sweep_across_tile_boundaries(D, m, g):
     dw = DeviceWorkload(w)
     lens = np.array(LEN_SWEEP, dtype=np.int32)
     lens_d = torch.from_numpy(lens).cuda()
-    for wg, comb, wide, qk in (("", "", "", ""), ("3", "", "", ""), ("40", "", "", ""),
-                               ("", "fused", "", ""), ("40", "fused", "", ""),
-                               ("", "kernel", "", ""), ("40", "kernel", "", ""), ("", "", "1", ""),
-                               ("", "", "0", ""), ("", "", "", "valu"), ("40", "", "", "valu")):
-        with plan_env(wg, comb, wide, qk):
+    for wg, comb, wide in (("", "", ""), ("3", "", ""), ("40", "", ""), ("", "fused", ""),
+                           ("40", "fused", ""), ("", "kernel", ""), ("40", "kernel", ""),
+                           ("", "", "1"), ("", "", "0")):
+        with plan_env(wg, comb, wide):
             for n in (0, w.l - 1):
                 say(f"length sweep D={D} m={m} g={g} layer={n} workgroups={wg or 'auto'} "
-                    f"merge={comb or 'kernel'} wide={wide or 'auto'} qk={qk or 'mfma'}")
+                    f"merge={comb or 'kernel'} wide={wide or 'auto'}")
                 out = torch.empty((w.B, w.h, w.D), dtype=torch.float32, device="cuda")
                 mlkv.decode_attention(n, dw.q[n], dw.cache, dw.map, lens_d, out, ws=dw.ws)
                 torch.cuda.synchronize()
                 ref = oracle.decode_attention(n, dw.host["q"][n], dw.host["k_cache"],
                                               dw.host["v_cache"], dw.kv_of, lens)
-                check_close(out.cpu().numpy(), ref, f"sweep D{D} g{g} L{n} wg{wg} {comb} {wide} {qk}")
+                check_close(out.cpu().numpy(), ref, f"sweep D{D} g{g} L{n} wg{wg} {comb} {wide}")
 
 
 @pytest.mark.parametrize("workgroups", ["", "600", "1500"])
@@ -365,20 +362,18 @@ def test_step_mlkv2_empty_context_outputs_new_value_exactly():
                                       f64(dw.host["v_new"][b, n // 6]).astype(np.float32))
 
 
-@pytest.mark.parametrize("wname,wide,qk", [("mlkv2_b1", "", ""), ("mlkv4_b128_ragged", "", ""),
-                                           ("mlkv4_b128_ragged", "1", ""),
-                                           ("mlkv4_b128_ragged", "0", ""),
-                                           ("mlkv4_b128_ragged", "", "valu"),
-                                           ("mlkv4_b8_long", "", "")])
-def test_full_size_step_matches_oracle(wname, wide, qk):
+@pytest.mark.parametrize("wname,wide", [("mlkv2_b1", ""), ("mlkv4_b128_ragged", ""),
+                                        ("mlkv4_b128_ragged", "1"), ("mlkv4_b128_ragged", "0"),
+                                        ("mlkv4_b8_long", "")])
+def test_full_size_step_matches_oracle(wname, wide):
     """Full-size workloads in the launch configuration the benchmark times
-    (and the ragged batch also with one wide workgroup per sequence, and with
-    q.K on the vector ALUs)."""
+    (and the ragged batch also with one wide workgroup per sequence in every
+    layer, and with split runs in every layer)."""
     w = synth.get_workload(wname)
-    say(f"full step {wname} wide={wide or 'auto'} qk={qk or 'mfma'}: uploading")
+    say(f"full step {wname} wide={wide or 'auto'}: uploading")
     dw = DeviceWorkload(w)
     say(f"full step {wname}: running")
-    with plan_env(wide=wide, qk=qk):
+    with plan_env(wide=wide):
         out = _run_step(dw).cpu().numpy()
     k_gpu, v_gpu = dw.read_cache()
     say(f"full step {wname}: oracle")
@@ -467,11 +462,10 @@ def _with_contexts(dw, ctx):
 APPEND_CTX = [0, 1, 30, 31, 32, 33, 63, 64, 95, 96, 127, 128, 200, 254, 255]
 
 
-@pytest.mark.parametrize("D,m,g,workgroups,wide,qk", [
-    (64, 4, 1, "", "", ""), (64, 4, 1, "7", "", ""), (64, 4, 1, "", "1", ""),
-    (64, 4, 3, "40", "", ""), (128, 2, 4, "", "", ""), (128, 2, 4, "", "1", ""),
-    (64, 4, 1, "", "", "valu"), (128, 2, 4, "7", "", "valu")])
-def test_step_fused_append_across_tile_boundaries(D, m, g, workgroups, wide, qk):
+@pytest.mark.parametrize("D,m,g,workgroups,wide", [
+    (64, 4, 1, "", ""), (64, 4, 1, "7", ""), (64, 4, 1, "", "1"),
+    (64, 4, 3, "40", ""), (128, 2, 4, "", ""), (128, 2, 4, "", "1"), (128, 2, 4, "7", "")])
+def test_step_fused_append_across_tile_boundaries(D, m, g, workgroups, wide):
     """The owning layers append inside their attention launch: the new token
     lands at every offset of a 32-token tile (and in the last slot of the
     cache), is attended by the owner in the same launch and by the later
@@ -480,14 +474,13 @@ def test_step_fused_append_across_tile_boundaries(D, m, g, workgroups, wide, qk)
                        ctx=max(APPEND_CTX), seed=77)
     dw = _with_contexts(DeviceWorkload(w), APPEND_CTX)
     assert dw.S == 256  # the last context appends into the last slot
-    say(f"fused append D={D} m={m} g={g} workgroups={workgroups or 'auto'} wide={wide or 'auto'} "
-        f"qk={qk or 'mfma'}")
-    with plan_env(workgroups=workgroups, wide=wide, qk=qk):
+    say(f"fused append D={D} m={m} g={g} workgroups={workgroups or 'auto'} wide={wide or 'auto'}")
+    with plan_env(workgroups=workgroups, wide=wide):
         out = _run_step(dw).cpu().numpy()
     k_gpu, v_gpu = dw.read_cache()
     ref, k_ref, v_ref = _oracle_step(dw)
     assert np.array_equal(k_gpu, k_ref) and np.array_equal(v_gpu, v_ref), "cache differs"
-    check_close(out, ref, f"fused append D{D} m{m} g{g} wg{workgroups} {wide} {qk}")
+    check_close(out, ref, f"fused append D{D} m{m} g{g} wg{workgroups} {wide}")
 
 
 def test_step_mixing_split_runs_and_a_workgroup_per_unit():
@@ -566,11 +559,10 @@ def _check_rope_step(dw, rd, label, base=10000.0):
     check_close(out, ref, label)
 
 
-@pytest.mark.parametrize("D,m,g,rd,wide,qk", [
-    (64, 4, 1, 16, "", ""), (64, 4, 1, 64, "", ""), (64, 4, 3, 32, "1", ""),
-    (128, 2, 4, 128, "", ""), (128, 2, 4, 32, "1", ""),
-    (64, 4, 1, 16, "", "valu"), (128, 2, 4, 64, "", "valu")])
-def test_step_rope_across_tile_boundaries(D, m, g, rd, wide, qk):
+@pytest.mark.parametrize("D,m,g,rd,wide", [
+    (64, 4, 1, 16, ""), (64, 4, 1, 64, ""), (64, 4, 3, 32, "1"),
+    (128, 2, 4, 128, ""), (128, 2, 4, 32, "1"), (128, 2, 4, 64, "")])
+def test_step_rope_across_tile_boundaries(D, m, g, rd, wide):
     """Rotary embedding of the newest token inside the step: its queries are
     rotated as each layer's attention loads them and its keys as the owner
     appends them, at every offset of a 32-token tile; the cache (rotated keys)
@@ -578,9 +570,9 @@ def test_step_rope_across_tile_boundaries(D, m, g, rd, wide, qk):
     w = synth.Workload("rope_sweep", l=4, h=12, m=m, g=g, D=D, B=len(APPEND_CTX),
                        ctx=max(APPEND_CTX), seed=78)
     dw = _with_contexts(DeviceWorkload(w), APPEND_CTX)
-    say(f"rope step D={D} m={m} g={g} rd={rd} wide={wide or 'auto'} qk={qk or 'mfma'}")
-    with plan_env(wide=wide, qk=qk):
-        _check_rope_step(dw, rd, f"rope D{D} m{m} g{g} rd{rd} {wide} {qk}")
+    say(f"rope step D={D} m={m} g={g} rd={rd} wide={wide or 'auto'}")
+    with plan_env(wide=wide):
+        _check_rope_step(dw, rd, f"rope D{D} m{m} g{g} rd{rd} {wide}")
 
 
 def test_step_rope_general_map_separate_append():
