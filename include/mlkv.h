@@ -435,8 +435,9 @@ int mlkv_model_fused_path(const mlkv_model* model, int batch);
  * 32-token tiles of all (sequence, KV head) pairs form one flat list shared
  * equally by `workgroups` workgroups (two per compute unit, or the device's
  * resident capacity if lower; capped at 128 per (sequence, KV head) and at
- * one per 4 tiles, at least one per (sequence, KV head); one workgroup for at
- * most 16 tiles; with at least as many (sequence, KV head) pairs as the
+ * one per 8 tiles; above the compute-unit count a whole multiple of it; at
+ * least one per (sequence, KV head); one workgroup for at most 16 tiles;
+ * with at least as many (sequence, KV head) pairs as the
  * budget, exactly one workgroup per pair).  A layer whose KV heads were all
  * appended by earlier layers (it re-reads them) gets one eight-wave
  * workgroup per pair instead when the pairs number at least 3/8 of the

@@ -143,9 +143,10 @@ int tiles_of(int len) { return (len + kTileTokens - 1) / kTileTokens; }
 // unit into runs of R tiles, R chosen on the device from the actual lengths
 // so that all runs fit the launched workgroups.  The host picks that count:
 // the device's resident capacity, capped at 128 per unit (more would only
-// multiply partials to merge) and at what runs of kMinTiles tiles need, but
-// at least one per unit; a single unit of at most 16 tiles takes one
-// workgroup (no partials at all).
+// multiply partials to merge) and at what runs of kMinTiles tiles need,
+// above the compute-unit count a whole multiple of it, but at least one per
+// unit; a single unit of at most kSingleUnitTiles tiles takes one workgroup
+// (no partials at all).
 struct Plan {
   int n_blocks;
   int max_parts;  // bound on the runs of one unit
@@ -155,7 +156,14 @@ struct Plan {
   int waves;      // waves per attention workgroup
   int direct;     // 1: one workgroup per unit in unit order (no schedule, no workspace)
 };
-constexpr int kMinTiles = 4;
+// Runs of at least 8 tiles (two per wave): shorter runs leave each wave one
+// tile, which only its first load's latency covers, and multiply partials.
+// On MI355X the whole-model step at batch 8 (12 layers of Pythia-160M
+// shape, 2000 cached tokens) runs 0.244 / 0.252 / 0.251 ms per step for
+// MLKV-4 / MLKV-12 / MQA-12 against 0.252 / 0.270 / 0.259 ms with runs of 4;
+// the ragged and long decode batches keep their plans.
+constexpr int kMinTiles = 8;
+constexpr int kSingleUnitTiles = 16;
 constexpr int kMaxRunsPerUnit = 128;
 constexpr long kCounterSlots = 65536;  // arrival counters of a workspace
 // Launches that schedule their runs on the device use at most this many
@@ -164,11 +172,21 @@ constexpr long kMaxScheduledWorkgroups = 16384;
 constexpr int kFallbackResident = 768;  // 256 CUs x 3 when no device can be queried
 constexpr int kWorkgroupsPerCu = 2;
 
+long compute_units_or_fallback() {
+  const long cus = mlkv::compute_units();
+  return cus > 0 ? cus : kFallbackResident / 3;
+}
+
 long workgroups_for(long resident, long units, long t_max, int min_tiles) {
   long g = resident < kMaxRunsPerUnit * units ? resident : kMaxRunsPerUnit * units;
   // Runs of min_tiles tiles always fit this many workgroups: no more needed.
   const long enough = (t_max + min_tiles - 1) / min_tiles + units;
   g = g < enough ? g : enough;
+  // Above the compute units, a whole multiple of them keeps their bandwidth
+  // shares equal (MQA-12 at 32 sequences of 2048 tokens: 288 workgroups of
+  // 8-tile runs take 135 us per cold-start step, 256 take 127 us).
+  const long cus = compute_units_or_fallback();
+  if (g > cus) g = g / cus * cus;
   return g > units ? g : units;
 }
 
@@ -184,11 +202,6 @@ long workgroups_for(long resident, long units, long t_max, int min_tiles) {
 // workgroups per compute unit: on MI355X fewer, longer runs beat filling
 // every resident slot (fewer partials, longer pipelines), and a whole
 // multiple of the compute units keeps their bandwidth shares equal.
-long compute_units_or_fallback() {
-  const long cus = mlkv::compute_units();
-  return cus > 0 ? cus : kFallbackResident / 3;
-}
-
 long workgroup_budget(int head_dim) {
   long resident = mlkv::resident_workgroups(head_dim);
   if (resident <= 0) resident = kFallbackResident;
@@ -253,7 +266,7 @@ Plan plan(const mlkv_map* map, int layer, int batch, int max_len, int head_dim) 
     // 109 / 102 us per 12-layer step instead of 122 / 108 us.
     if (!accept && !force_fused && g >= cus) {
       accept = true;
-      budget = g / cus * cus;
+      budget = g;
     }
     if (accept) {
       pl.min_tiles = static_cast<int>(mt);
@@ -261,7 +274,7 @@ Plan plan(const mlkv_map* map, int layer, int batch, int max_len, int head_dim) 
     }
   }
   long g = workgroups_for(budget, units, t_max, pl.min_tiles);
-  if (units == 1 && t_max <= 4 * kMinTiles) g = 1;
+  if (units == 1 && t_max <= kSingleUnitTiles) g = 1;
   pl.waves = mlkv::default_waves();
   pl.n_blocks = static_cast<int>(g);
   if (g == units) {  // one workgroup per unit: runs cover whole units, nothing to merge
