@@ -227,10 +227,34 @@ __global__ __launch_bounds__(kFusedThreads) void layer_in_kernel(LayerInParams p
   };
   issue(wave);
 
-  // Rotation angles of the tile's rows (q and k blocks), in double, while the
-  // loads are in flight: sc[row][j] = (sin, cos) of pos[row] * inv_freq[j].
   const int half = p.dims / 2;
   const int role = blk < p.h ? 0 : blk < p.h + p.owned ? 1 : blk < p.h + 2 * p.owned ? 2 : 3;
+  // The epilogue's biases (element e = threadIdx.x + k * kFusedThreads of the
+  // 16 x D tile: its own and, for rotated channels, its partner's), requested
+  // now so that their latency hides under the products.
+  constexpr int kEpi = 16 * D / kFusedThreads;
+  const uint16_t* const bias = role == 0 ? p.b_q : role == 1 ? p.b_k : role == 2 ? p.b_v : p.b_fc1;
+  const int jb = role == 0 ? blk : role == 1 ? blk - p.h : role == 2 ? blk - p.h - p.owned
+                                                                     : blk - p.h - 2 * p.owned;
+  float bias_own[kEpi], bias_partner[kEpi];
+#pragma unroll
+  for (int k = 0; k < kEpi; ++k) {
+    const int e = threadIdx.x + k * kFusedThreads, rr = e / D, c = e % D;
+    bias_own[k] = bias_partner[k] = 0.f;
+    if (b0 + rr >= p.rows) continue;
+    if (role == 3) {
+      if (jb * D + c < p.ff) bias_own[k] = bf16_to_f32(bias[jb * D + c]);
+      continue;
+    }
+    bias_own[k] = bf16_to_f32(bias[jb * D + c]);
+    if (role < 2 && c < p.dims) {
+      const int partner = c < half ? c + half : c - half;
+      bias_partner[k] = bf16_to_f32(bias[jb * D + partner]);
+    }
+  }
+
+  // Rotation angles of the tile's rows (q and k blocks), in double, while the
+  // loads are in flight: sc[row][j] = (sin, cos) of pos[row] * inv_freq[j].
   if (role < 2) {
     for (int e = threadIdx.x; e < 16 * half; e += kFusedThreads) {
       const int row = e / half, jj = e % half;
@@ -333,36 +357,35 @@ __global__ __launch_bounds__(kFusedThreads) void layer_in_kernel(LayerInParams p
 
   // Epilogue, in double as the library path's: bias, rotation (q and k),
   // GELU (fc1), one rounding to bf16.
-  for (int e = threadIdx.x; e < 16 * D; e += kFusedThreads) {
+#pragma unroll
+  for (int k = 0; k < kEpi; ++k) {
+    const int e = threadIdx.x + k * kFusedThreads;
     const int rr = e / D, c = e % D, b = b0 + rr;
     if (b >= p.rows) continue;
     const double u = y[rr][c];
     if (role == 3) {
-      const int col = (blk - p.h - 2 * p.owned) * D + c;
+      const int col = jb * D + c;
       if (col >= p.ff) continue;
-      const double z = u + static_cast<double>(bf16_to_f32(p.b_fc1[col]));
+      const double z = u + static_cast<double>(bias_own[k]);
       p.f16[static_cast<size_t>(b) * p.ff + col] =
           f64_to_bf16_rne(0.5 * z * (1.0 + erf(z * 0.70710678118654752440)));
       continue;
     }
-    const int j = role == 0 ? blk : role == 1 ? blk - p.h : blk - p.h - p.owned;
-    const uint16_t* bias = role == 0 ? p.b_q : role == 1 ? p.b_k : p.b_v;
-    const double ub = u + static_cast<double>(bf16_to_f32(bias[j * D + c]));
+    const double ub = u + static_cast<double>(bias_own[k]);
     uint16_t out;
     if (role == 2 || c >= p.dims) {
       out = f64_to_bf16_rne(ub);
     } else {
       const int partner = c < half ? c + half : c - half;
-      const double w =
-          static_cast<double>(y[rr][partner]) + static_cast<double>(bf16_to_f32(bias[j * D + partner]));
+      const double w = static_cast<double>(y[rr][partner]) + static_cast<double>(bias_partner[k]);
       const int jj = c < half ? c : c - half;
       const double sn = sc[rr][jj][0], cs = sc[rr][jj][1];
       out = f64_to_bf16_rne(c < half ? ub * cs - w * sn : ub * cs + w * sn);
     }
     if (role == 0)
-      p.q16[static_cast<size_t>(b) * p.h * D + j * D + c] = out;
+      p.q16[static_cast<size_t>(b) * p.h * D + jb * D + c] = out;
     else
-      (role == 1 ? p.k16 : p.v16)[static_cast<size_t>(b) * p.kv_stride + p.kv_offset + j * D + c] = out;
+      (role == 1 ? p.k16 : p.v16)[static_cast<size_t>(b) * p.kv_stride + p.kv_offset + jb * D + c] = out;
   }
 }
 
@@ -383,6 +406,22 @@ __global__ __launch_bounds__(kFusedThreads) void layer_out_kernel(LayerOutParams
   const uint16_t* orow = p.o16 + static_cast<size_t>(b0 + (live ? r : 0)) * p.hD + 8 * grp;
   const uint16_t* frow = p.f16 + static_cast<size_t>(b0 + (live ? r : 0)) * p.ff + 8 * grp;
   const u16x8 zero = {0, 0, 0, 0, 0, 0, 0, 0};
+  // The epilogue's inputs (lane l < 64 finishes four outputs of one row: the
+  // residual and both biases), requested now so that their latency hides
+  // under the products.
+  const int b_out = b0 + (threadIdx.x & 15);
+  const int n0 = blk * 16 + 4 * ((threadIdx.x >> 4) & 3);
+  const bool writer = threadIdx.x < 64 && b_out < p.rows;
+  float4 x_old = {0.f, 0.f, 0.f, 0.f};
+  float bo[4] = {0.f, 0.f, 0.f, 0.f}, b2[4] = {0.f, 0.f, 0.f, 0.f};
+  if (writer) {
+    x_old = *reinterpret_cast<const float4*>(p.x + static_cast<size_t>(b_out) * p.d + n0);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      bo[i] = bf16_to_f32(p.b_o[n0 + i]);
+      b2[i] = bf16_to_f32(p.b_2[n0 + i]);
+    }
+  }
   f32x4 acc_a = {0.f, 0.f, 0.f, 0.f}, acc_m = {0.f, 0.f, 0.f, 0.f};
   for (int base = wave; base < KT; base += PRE * kFusedWaves) {
     u16x8 a[PRE], v[PRE];
@@ -414,14 +453,13 @@ __global__ __launch_bounds__(kFusedThreads) void layer_out_kernel(LayerOutParams
       sa += part[w][0][l];
       sm += part[w][1][l];
     }
-    const int b = b0 + (l & 15);
-    if (b < p.rows) {
-      float* xr = p.x + static_cast<size_t>(b) * p.d;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int n = blk * 16 + 4 * (l >> 4) + i;
-        xr[n] += (sa[i] + bf16_to_f32(p.b_o[n])) + (sm[i] + bf16_to_f32(p.b_2[n]));
-      }
+    if (writer) {
+      float4 x_new;
+      x_new.x = x_old.x + ((sa[0] + bo[0]) + (sm[0] + b2[0]));
+      x_new.y = x_old.y + ((sa[1] + bo[1]) + (sm[1] + b2[1]));
+      x_new.z = x_old.z + ((sa[2] + bo[2]) + (sm[2] + b2[2]));
+      x_new.w = x_old.w + ((sa[3] + bo[3]) + (sm[3] + b2[3]));
+      *reinterpret_cast<float4*>(p.x + static_cast<size_t>(b_out) * p.d + n0) = x_new;
     }
   }
 }
