@@ -247,6 +247,39 @@ def test_large_batch_plans_one_workgroup_per_unit(monkeypatch):
                                     F, S, 0x60000, 1 << 30, None)] == "MLKV_ERR_UNSUPPORTED"
 
 
+def test_planner_rules_on_representative_shapes(monkeypatch):
+    """The attention planner's documented rules on the shapes the benchmark
+    and the model step use (256 compute units, the fallback when no device is
+    visible and MI355X's count): runs of at least 8 tiles, counts above the
+    compute units rounded down to a whole multiple of them, the in-place
+    merge whenever every unit's partials fit, one workgroup per unit for
+    re-reading layers with enough units, one workgroup for a lone short unit."""
+    for k in ("MLKV_WORKGROUPS", "MLKV_COMBINE", "MLKV_WIDE"):
+        monkeypatch.delenv(k, raising=False)
+    L = mlkv.lib()
+    merge_kernel = lambda mp, n, B, S, ml: L.mlkv_plan_merge_kernel(mp.handle, n, B, S, 64, ml)
+    mlkv4 = mlkv.Map.uniform(12, 12, 4, 1)
+    # model step at batch 8, 2000 cached tokens: 8 units x 63 tiles in runs of
+    # at least 8 tiles -> 504 / 8 + 8 workgroups, partials merged in place
+    assert mlkv4.plan(0, 8, 2048, 64, 2001)[0] == 71
+    assert merge_kernel(mlkv4, 0, 8, 2048, 2001) == 0
+    # MQA-12 at 32 x 2048: 2048 / 8 + 32 = 288 workgroups, rounded to 256
+    mqa = mlkv.Map.uniform(12, 12, 12, 1)
+    assert mqa.plan(0, 32, 2048, 64, 2048)[0] == 256
+    assert merge_kernel(mqa, 0, 32, 2048, 2048) == 0
+    # ragged 128-sequence batch: the owner splits runs over two workgroups per
+    # compute unit, the re-reading layer takes one eight-wave workgroup per unit
+    assert mlkv4.plan(0, 128, 2048, 64, 2048)[0] == 512
+    assert mlkv4.plan(1, 128, 2048, 64, 2048) == (128, 2)
+    # long 8 x 32768 batch: 64 runs per unit, too many to stage -> merge kernel
+    assert mlkv4.plan(0, 8, 32768, 64, 32768)[0] == 512
+    assert merge_kernel(mlkv4, 0, 8, 32768, 32768) == 1
+    # one sequence: a single workgroup up to 16 tiles, else runs of >= 8 tiles
+    mlkv2 = mlkv.Map.uniform(12, 12, 2, 1)
+    assert mlkv2.plan(0, 1, 2048, 64, 512)[0] == 1
+    assert mlkv2.plan(0, 1, 2048, 64, 2048)[0] == 64 // 8 + 1
+
+
 def test_layout_reference_pack_and_unpack_agree():
     """The tests' two statements of the value-plane layout (the index formula
     and the block transpose) agree with each other."""
