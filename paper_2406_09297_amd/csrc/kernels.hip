@@ -212,11 +212,13 @@ __global__ __launch_bounds__(kRowsThreads) void cache_rows_kernel(CacheRowsParam
   }
 }
 
-// acc / den for den > 0, zeros otherwise: one reciprocal (within one ulp)
-// for the four channels.  A normalised softmax has den >= 1 (the largest
-// weight is at least one), and den = 1 leaves acc exact.
+// acc / den with one reciprocal (within one ulp) for the four channels; zeros
+// for an empty row (den = 0).  A row with any attended position has den >= 1
+// (its largest weight is at least one), and den = 1 leaves acc exact;
+// non-finite inputs give a non-finite den, which propagates as in the
+// definition rather than being taken for an empty row.
 __device__ __forceinline__ f32x4 normalize4(f32x4 acc, float den) {
-  return den > 0.f ? acc * __builtin_amdgcn_rcpf(den) : f32x4{0.f, 0.f, 0.f, 0.f};
+  return den != 0.f ? acc * __builtin_amdgcn_rcpf(den) : f32x4{0.f, 0.f, 0.f, 0.f};
 }
 
 // ---------------------------------------------------------------------------
@@ -863,7 +865,7 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(AttnParams p) {
       dd += fv * sm_den[v];
       oo += fv * sm_o[v][lane];
     }
-    store_out4<D>(p, rrow, c, dd > 0.f ? oo / dd : f32x4{0.f, 0.f, 0.f, 0.f});
+    store_out4<D>(p, rrow, c, dd != 0.f ? oo / dd : f32x4{0.f, 0.f, 0.f, 0.f});
   }
 }
 
