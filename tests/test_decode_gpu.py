@@ -14,7 +14,8 @@ torch = pytest.importorskip("torch")
 
 import oracle  # noqa: E402
 import synth  # noqa: E402
-from gpu_util import DeviceWorkload, check_close, f64, say  # noqa: E402
+from gpu_util import (BOUND_MAX_POSITIONS, DeviceWorkload, check_close, f64,  # noqa: E402
+                      layer_rounding_bound, say, step_rounding_bound)
 from layout_ref import unpack_k, unpack_v  # noqa: E402
 
 pytestmark = pytest.mark.gpu
@@ -133,7 +134,16 @@ def test_decode_attention_matches_oracle(wname, kw, layers):
         torch.cuda.synchronize()
         ref = oracle.decode_attention(n, dw.host["q"][n], dw.host["k_cache"], dw.host["v_cache"],
                                       dw.kv_of, lens)
-        check_close(out.cpu().numpy(), ref, f"{w.name} L{n}")
+        check_close(out.cpu().numpy(), ref, f"{w.name} L{n}",
+                    bound=_layer_bound(dw, n, dw.host["k_cache"], lens, ref))
+
+
+def _layer_bound(dw, n, k_cache, lens, ref):
+    """Rounding bound of layer n's outputs (None for rows too long for it)."""
+    if int(np.max(lens, initial=0)) > BOUND_MAX_POSITIONS:
+        return None
+    return layer_rounding_bound(dw.host["q"][n], k_cache, dw.host["v_cache"], dw.kv_of[n], lens,
+                                ref)
 
 
 def _sweep_workload(D, m, g, lens, h=12, l=4, k_scale=1.0, seed=99):
@@ -152,6 +162,9 @@ def test_length_sweep_across_tile_boundaries(D, m, g):
     dw = DeviceWorkload(w)
     lens = np.array(LEN_SWEEP, dtype=np.int32)
     lens_d = torch.from_numpy(lens).cuda()
+    refs = {n: oracle.decode_attention(n, dw.host["q"][n], dw.host["k_cache"],
+                                       dw.host["v_cache"], dw.kv_of, lens) for n in (0, w.l - 1)}
+    bounds = {n: _layer_bound(dw, n, dw.host["k_cache"], lens, refs[n]) for n in refs}
     for wg, comb, wide in (("", "", ""), ("3", "", ""), ("40", "", ""), ("", "fused", ""),
                            ("40", "fused", ""), ("", "kernel", ""), ("40", "kernel", ""),
                            ("", "", "1"), ("", "", "0")):
@@ -162,9 +175,8 @@ def test_length_sweep_across_tile_boundaries(D, m, g):
                 out = torch.empty((w.B, w.h, w.D), dtype=torch.float32, device="cuda")
                 mlkv.decode_attention(n, dw.q[n], dw.cache, dw.map, lens_d, out, ws=dw.ws)
                 torch.cuda.synchronize()
-                ref = oracle.decode_attention(n, dw.host["q"][n], dw.host["k_cache"],
-                                              dw.host["v_cache"], dw.kv_of, lens)
-                check_close(out.cpu().numpy(), ref, f"sweep D{D} g{g} L{n} wg{wg} {comb} {wide}")
+                check_close(out.cpu().numpy(), refs[n],
+                            f"sweep D{D} g{g} L{n} wg{wg} {comb} {wide}", bound=bounds[n])
 
 
 @pytest.mark.parametrize("workgroups", ["", "600", "1500"])
@@ -189,14 +201,15 @@ def test_schedule_path_with_many_short_runs(workgroups):
             torch.cuda.synchronize()
             ref = oracle.decode_attention(n, dw.host["q"][n], dw.host["k_cache"],
                                           dw.host["v_cache"], dw.kv_of, lens)
-            check_close(out.cpu().numpy(), ref, f"short runs wg{workgroups} L{n}")
+            check_close(out.cpu().numpy(), ref, f"short runs wg{workgroups} L{n}",
+                        bound=_layer_bound(dw, n, dw.host["k_cache"], lens, ref))
         say(f"short runs workgroups={workgroups or 'auto'}: step")
         _with_contexts(dw, lens - 1)
         out = _run_step(dw).cpu().numpy()
     k_gpu, v_gpu = dw.read_cache()
     ref, k_ref, v_ref = _oracle_step(dw)
     assert np.array_equal(k_gpu, k_ref) and np.array_equal(v_gpu, v_ref), "cache differs"
-    check_close(out, ref, f"short runs step wg{workgroups}")
+    _check_step(dw, out, ref, k_ref, v_ref, f"short runs step wg{workgroups}")
 
 
 def test_schedule_path_at_the_table_limit():
@@ -228,14 +241,15 @@ def test_schedule_path_at_the_table_limit():
                                           dw.host["v_cache"], dw.kv_of, lens)
             got = out.cpu().numpy()
             assert np.all(got[lens == 0] == 0.0), "sequences attending nothing must be zero"
-            check_close(got, ref, f"table limit L{n}")
+            check_close(got, ref, f"table limit L{n}",
+                        bound=_layer_bound(dw, n, dw.host["k_cache"], lens, ref))
         say("table limit: step")
         _with_contexts(dw, np.maximum(lens, 1) - 1)
         out = _run_step(dw).cpu().numpy()
     k_gpu, v_gpu = dw.read_cache()
     ref, k_ref, v_ref = _oracle_step(dw)
     assert np.array_equal(k_gpu, k_ref) and np.array_equal(v_gpu, v_ref), "cache differs"
-    check_close(out, ref, "table limit step")
+    _check_step(dw, out, ref, k_ref, v_ref, "table limit step")
 
 
 def test_split_count_invariance_and_determinism():
@@ -284,6 +298,44 @@ def test_single_position_and_empty():
                 assert np.all(out[b, i] == 0)
 
 
+def test_non_finite_inputs_propagate_as_in_the_definition():
+    """A NaN key inside the attended range makes every output of the heads
+    reading it NaN, and an infinite value makes their outputs in that
+    channel infinite, as Eq. 3 evaluated in IEEE arithmetic (the oracle)
+    gives; only a row that attends nothing (zero weight sum) is zero.
+    Every plan: one run per unit, split runs merged in place or by the
+    merge kernel, a wide workgroup per unit."""
+    lens = np.array([300, 300, 300, 0, 70], np.int32)
+    w = _sweep_workload(64, 4, 1, lens, h=12, l=4, seed=61)
+    dw = DeviceWorkload(w)
+    kc, vc = dw.host["k_cache"], dw.host["v_cache"]
+    kc[0, 1, 131] = synth.BF16_NAN      # sequence 1: a NaN key (KV head 0)
+    vc[0, 2, 40, 5] = 0x7F80            # sequence 2: +inf in channel 5 of one value
+    kc[0, 4, 200] = synth.BF16_NAN      # sequence 4: past its length, never read
+    dw.cache.load_rows(kc, vc)
+    lens_d = torch.from_numpy(lens).cuda()
+    ref = oracle.decode_attention(0, dw.host["q"][0], kc, vc, dw.kv_of, lens)
+    assert np.all(np.isnan(ref[1])) and np.all(np.isposinf(ref[2][:, 5]))
+    clean = [0, 2, 3, 4]  # sequence 2 without its channel 5
+    with np.errstate(invalid="ignore"):
+        bound = layer_rounding_bound(dw.host["q"][0][clean], kc[:, clean], vc[:, clean],
+                                     dw.kv_of[0], lens[clean], ref[clean])
+    keep = np.ones(ref[clean].shape, bool)
+    keep[1, :, 5] = False
+    for wg, comb, wide in (("", "", ""), ("40", "fused", ""), ("40", "kernel", ""), ("", "", "1")):
+        with plan_env(wg, comb, wide):
+            say(f"non-finite inputs workgroups={wg or 'auto'} merge={comb or 'auto'} "
+                f"wide={wide or 'auto'}")
+            out = torch.full((w.B, w.h, w.D), 7.0, dtype=torch.float32, device="cuda")
+            mlkv.decode_attention(0, dw.q[0], dw.cache, dw.map, lens_d, out, ws=dw.ws)
+            torch.cuda.synchronize()
+        got = out.cpu().numpy()
+        assert np.all(np.isnan(got[1])), "a NaN key must make its rows NaN"
+        assert np.all(np.isposinf(got[2][:, 5])), "an infinite value must give +inf"
+        check_close(got[clean][keep], ref[clean][keep], "non-finite: the finite outputs",
+                    bound=bound[keep])
+
+
 @pytest.mark.parametrize("pos_kind", ["first", "tile_end", "tile_start", "split_edge", "last"])
 def test_needle_token(pos_kind):
     """A key aligned with q and scaled up takes (almost) all weight: o = v_needle
@@ -307,7 +359,8 @@ def test_needle_token(pos_kind):
     ref = oracle.decode_attention(0, dw.host["q"][0], kc, dw.host["v_cache"], dw.kv_of, lens)
     _, alpha = oracle.attend_one(q, kc[0, b, :L], dw.host["v_cache"][0, b, :L])
     assert alpha[pos] > 0.99
-    check_close(out.cpu().numpy(), ref, f"needle {pos_kind}")
+    check_close(out.cpu().numpy(), ref, f"needle {pos_kind}",
+                bound=_layer_bound(dw, 0, kc, lens, ref))
 
 
 def test_bf16_output_is_the_rounded_fp32_result():
@@ -350,6 +403,17 @@ def _oracle_step(dw):
     return out, k, v
 
 
+def _check_step(dw, out, ref, k_ref, v_ref, tag):
+    """A step's outputs against the oracle's, each within its rounding bound
+    (computed from the caches after the step) where the rows are short enough
+    for it to be tight."""
+    ctx = dw.host["ctx"]
+    bound = None
+    if int(ctx.max(initial=0)) + 1 <= BOUND_MAX_POSITIONS:
+        bound = step_rounding_bound(dw.host["q"], k_ref, v_ref, dw.kv_of, ctx, ref)
+    check_close(out, ref, tag, bound=bound)
+
+
 def test_step_mlkv2_empty_context_outputs_new_value_exactly():
     w = synth.Workload("mlkv2_ctx0", l=12, h=12, m=2, g=1, D=64, B=3, ctx=0, seed=5)
     dw = DeviceWorkload(w)
@@ -379,7 +443,7 @@ def test_full_size_step_matches_oracle(wname, wide):
     say(f"full step {wname}: oracle")
     ref, k_ref, v_ref = _oracle_step(dw)
     assert np.array_equal(k_gpu, k_ref) and np.array_equal(v_gpu, v_ref), "cache differs"
-    check_close(out, ref, f"step {wname}")
+    _check_step(dw, out, ref, k_ref, v_ref, f"step {wname}")
 
 
 @pytest.mark.parametrize("mg", [(12, 12), (12, 4), (12, 1), (6, 1), (4, 1), (1, 1)])
@@ -393,7 +457,7 @@ def test_map_sweep_full_size(mg):
     say(f"sweep step {w.name}: oracle")
     ref, k_ref, v_ref = _oracle_step(dw)
     assert np.array_equal(k_gpu, k_ref) and np.array_equal(v_gpu, v_ref), "cache differs"
-    check_close(out, ref, f"step {w.name}")
+    _check_step(dw, out, ref, k_ref, v_ref, f"step {w.name}")
 
 
 @pytest.mark.parametrize("merge", ["", "kernel"])
@@ -413,7 +477,7 @@ def test_full_size_step_twice_on_one_workspace(merge):
     k_gpu, v_gpu = dw2.read_cache()
     ref, k_ref, v_ref = _oracle_step(dw2)
     assert np.array_equal(k_gpu, k_ref) and np.array_equal(v_gpu, v_ref), "cache differs"
-    check_close(out, ref, f"step twice merge={merge or 'auto'}")
+    _check_step(dw2, out, ref, k_ref, v_ref, f"step twice merge={merge or 'auto'}")
 
 
 def test_one_workspace_shared_by_steps_of_different_batches():
@@ -440,7 +504,7 @@ def test_one_workspace_shared_by_steps_of_different_batches():
         k_gpu, v_gpu = dw.read_cache()
         ref, k_ref, v_ref = _oracle_step(dw)
         assert np.array_equal(k_gpu, k_ref) and np.array_equal(v_gpu, v_ref), "cache differs"
-        check_close(out, ref, f"shared workspace {w.name}")
+        _check_step(dw, out, ref, k_ref, v_ref, f"shared workspace {w.name}")
 
 
 # ---------------------------------------------------- fused append in step --
@@ -480,7 +544,7 @@ def test_step_fused_append_across_tile_boundaries(D, m, g, workgroups, wide):
     k_gpu, v_gpu = dw.read_cache()
     ref, k_ref, v_ref = _oracle_step(dw)
     assert np.array_equal(k_gpu, k_ref) and np.array_equal(v_gpu, v_ref), "cache differs"
-    check_close(out, ref, f"fused append D{D} m{m} g{g} wg{workgroups} {wide}")
+    _check_step(dw, out, ref, k_ref, v_ref, f"fused append D{D} m{m} g{g} wg{workgroups} {wide}")
 
 
 def test_step_mixing_split_runs_and_a_workgroup_per_unit():
@@ -503,7 +567,7 @@ def test_step_mixing_split_runs_and_a_workgroup_per_unit():
     k_gpu, v_gpu = dw.read_cache()
     ref, k_ref, v_ref = _oracle_step(dw)
     assert np.array_equal(k_gpu, k_ref) and np.array_equal(v_gpu, v_ref), "cache differs"
-    check_close(out, ref, "mixed plans step")
+    _check_step(dw, out, ref, k_ref, v_ref, "mixed plans step")
     _check_rope_step(dw, 16, "mixed plans rope")
 
 
@@ -523,7 +587,7 @@ def test_step_owner_that_does_not_read_its_head():
     k_gpu, v_gpu = dw.read_cache()
     ref, k_ref, v_ref = _oracle_step(dw)
     assert np.array_equal(k_gpu, k_ref) and np.array_equal(v_gpu, v_ref), "cache differs"
-    check_close(out, ref, "general map")
+    _check_step(dw, out, ref, k_ref, v_ref, "general map")
 
 
 # ------------------------------------------------------ rotary embedding --
@@ -551,12 +615,17 @@ def _check_rope_step(dw, rd, label, base=10000.0):
     assert np.array_equal(k2, k_gpu) and np.array_equal(v2, v_gpu), f"{label}: cache changed"
     out = out.cpu().numpy()
     k, v = dw.host["k_cache"].copy(), dw.host["v_cache"].copy()
-    ref = oracle.decode_step_rope(dw.host["q"], k, v, dw.host["k_new"], dw.host["v_new"],
-                                  dw.kv_of, dw.owner_of, dw.host["ctx"], rd, base)
+    ref, q_rot, _ = oracle.decode_step_rope(dw.host["q"], k, v, dw.host["k_new"],
+                                            dw.host["v_new"], dw.kv_of, dw.owner_of,
+                                            dw.host["ctx"], rd, base, return_rotated=True)
     bad = np.argwhere(k_gpu != k)
     assert bad.size == 0, f"{label}: cached (rotated) keys differ at {bad[:4].tolist()}"
     assert np.array_equal(v_gpu, v), f"{label}: cached values differ"
-    check_close(out, ref, label)
+    ctx = dw.host["ctx"]
+    bound = None
+    if int(ctx.max(initial=0)) + 1 <= BOUND_MAX_POSITIONS:  # rows of the rotated queries
+        bound = step_rounding_bound(q_rot, k, v, dw.kv_of, ctx, ref)
+    check_close(out, ref, label, bound=bound)
 
 
 @pytest.mark.parametrize("D,m,g,rd,wide", [
@@ -627,7 +696,7 @@ def test_step_sequence_with_nothing_cached_before_nothing_to_attend():
     ref, k_ref, v_ref = _oracle_step(dw)
     assert np.array_equal(k_gpu, k_ref) and np.array_equal(v_gpu, v_ref), "cache differs"
     assert np.all(out[:, 0] == 0)
-    check_close(out, ref, "step with -1 context")
+    _check_step(dw, out, ref, k_ref, v_ref, "step with -1 context")
 
 
 def test_lengths_above_the_hint_are_truncated_to_it():
@@ -644,7 +713,8 @@ def test_lengths_above_the_hint_are_truncated_to_it():
     torch.cuda.synchronize()
     ref = oracle.decode_attention(1, dw.host["q"][1], dw.host["k_cache"], dw.host["v_cache"],
                                   dw.kv_of, np.minimum(lens, hint))
-    check_close(out.cpu().numpy(), ref, "hint truncation")
+    check_close(out.cpu().numpy(), ref, "hint truncation",
+                bound=_layer_bound(dw, 1, dw.host["k_cache"], np.minimum(lens, hint), ref))
 
 
 def test_length_check_rejects_out_of_range_lengths(monkeypatch):
@@ -708,8 +778,8 @@ def test_step_captured_in_a_hip_graph_replays_like_eager(wname, kw):
         assert torch.equal(out, ref)
     k, v = dw.read_cache()
     assert np.array_equal(k, k_ref) and np.array_equal(v, v_ref)
-    ref64, _, _ = _oracle_step(dw)
-    check_close(ref.cpu().numpy(), ref64, f"graph step {w.name}")
+    ref64, k64, v64 = _oracle_step(dw)
+    _check_step(dw, ref.cpu().numpy(), ref64, k64, v64, f"graph step {w.name}")
 
 
 # --------------------------------------------------- 7B-like, full size --
@@ -806,7 +876,9 @@ def test_large_batch_step_sampled_sequences(m, g, B):
                              np.ascontiguousarray(inp["v_new"][sample]), kv_of, owner_of,
                              inp["ctx"][sample])
     assert np.array_equal(k1, k_ref) and np.array_equal(v1, v_ref), "cache rows differ"
-    check_close(out, ref, f"large batch {w.name}, sampled sequences")
+    bound = step_rounding_bound(np.ascontiguousarray(inp["q"][:, sample]), k_ref, v_ref, kv_of,
+                                inp["ctx"][sample], ref)
+    check_close(out, ref, f"large batch {w.name}, sampled sequences", bound=bound)
 
 
 def test_capacity_batch_step_sampled_sequences():
@@ -850,6 +922,6 @@ def test_capacity_batch_step_sampled_sequences():
     ref = oracle.decode_step(q_h, k_ref, v_ref, kn_h, vn_h, kv_of, owner_of,
                              np.full(len(sample), w.ctx, dtype=np.int32))
     assert np.array_equal(k1, k_ref) and np.array_equal(v1, v_ref), "cache rows differ"
-    # bf16 output (the benchmark's): its rounding (at most 2^-9 relative) fits
+    # bf16 output (the benchmark's): its rounding (at most 2^-8 relative) fits
     # inside the same bars as the fp32 output
     check_close(got, ref, "capacity batch, sampled sequences (bf16 out)")

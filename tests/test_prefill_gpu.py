@@ -12,7 +12,8 @@ torch = pytest.importorskip("torch")
 
 import oracle  # noqa: E402
 import synth  # noqa: E402
-from gpu_util import check_close, f64, say  # noqa: E402
+from gpu_util import (check_close, f64, prefill_rounding_bound, say,  # noqa: E402
+                      softmax_rounding_bound, step_rounding_bound)
 from layout_ref import unpack_k, unpack_v  # noqa: E402
 
 pytestmark = pytest.mark.gpu
@@ -83,7 +84,8 @@ def _check_case(c: PrefillCase, label: str):
     k_gpu, v_gpu = c.read_cache()
     ref, k_ref, v_ref = c.oracle()
     assert np.array_equal(k_gpu, k_ref) and np.array_equal(v_gpu, v_ref), f"{label}: cache differs"
-    check_close(out, ref, label)
+    bound = prefill_rounding_bound(c.host["q"], k_ref, v_ref, c.kv_of, c.host["ctx"], ref)
+    check_close(out, ref, label, bound=bound)
 
 
 PROMPTS = [1, 2, 5, 15, 16, 17, 31, 32, 33, 70]
@@ -214,7 +216,8 @@ def test_prefill_then_decode_continues_the_sequence():
     ref = oracle.decode_step(q2, k_ref, v_ref, kn2, vn2, c.kv_of, c.owner_of, ctx2)
     k_gpu, v_gpu = c.read_cache()
     assert np.array_equal(k_gpu, k_ref) and np.array_equal(v_gpu, v_ref)
-    check_close(out.cpu().numpy(), ref, "decode after prefill")
+    bound = step_rounding_bound(q2, k_ref, v_ref, c.kv_of, ctx2, ref)
+    check_close(out.cpu().numpy(), ref, "decode after prefill", bound=bound)
 
 
 def test_full_size_prefill_sampled_rows():
@@ -234,7 +237,7 @@ def test_full_size_prefill_sampled_rows():
         oracle.append_rows(n, k_ref, v_ref, h["k_new"], h["v_new"], c.owner_of, h["ctx"])
     assert np.array_equal(k_gpu, k_ref) and np.array_equal(v_gpu, v_ref), "cache differs"
     say("full prefill: oracle rows")
-    rows, refs = [], []
+    rows, refs, bounds = [], [], []
     for n in range(w.l):
         for b in (0, w.B - 1):
             for t in (0, 1, 31, 32, 63, 64, 1000, w.T - 2, w.T - 1):
@@ -244,4 +247,7 @@ def test_full_size_prefill_sampled_rows():
                     o, _ = oracle.attend_one(h["q"][n, b, t, i], k_ref[kv, b, :L], v_ref[kv, b, :L])
                     rows.append(out[n, b, t, i])
                     refs.append(o)
-    check_close(np.array(rows), np.array(refs), "full prefill sampled rows")
+                    bounds.append(softmax_rounding_bound(
+                        f64(h["q"][n, b, t, i])[None], f64(k_ref[kv, b, :L]), f64(v_ref[kv, b, :L]),
+                        o[None], np.array([L]))[0])
+    check_close(np.array(rows), np.array(refs), "full prefill sampled rows", bound=np.array(bounds))
