@@ -74,6 +74,23 @@ struct PrefillParams {
   float scale_log2;          // log2(e) / sqrt(D)
 };
 
+// The MLP's second product of a model layer, y = f W_2 + b_2 ([rows][d],
+// fp32), carried by extra workgroups of that layer's attention launch: it
+// needs only the layer-in results (GPT-NeoX's parallel residual), so it runs
+// beside the attention instead of after it, and the layer-out product adds y.
+// Workgroup s of the product takes column block s % (d / 16) (16 outputs)
+// and rows 16 (s / (d / 16)) .. +15, and sums exactly as a layer-out
+// workgroup does: k-block kb of the [W_o ; W_2] packing by virtual wave kb % 8
+// in increasing kb, the eight virtual waves' tiles in order.
+struct SideProduct {
+  const uint16_t* w;    // layer-out packing: column block blk has kt k-blocks, W_2's from ka
+  const uint16_t* f16;  // [rows][ff] bf16
+  const uint16_t* b2;   // [d] bf16
+  float* y;             // [rows][d]
+  int rows, d, ff, ka, kt;
+  int n_blocks;         // (d / 16) * ceil(rows / 16); 0: no product
+};
+
 struct AttnParams {
   const uint16_t* q;         // [B][h][D]
   const uint16_t* k;         // key plane   [n_kv][B][S][D]
@@ -109,6 +126,12 @@ struct AttnParams {
   // rotated as they are loaded, the owner's new key before it is stored.
   const double* rope_cs;     // [B][rope_half][2] cos, sin at the token's position
   int rope_half;
+};
+
+// An attention launch that also carries a SideProduct: workgroups n_blocks ..
+// n_blocks + side.n_blocks - 1 compute the product and nothing else.
+struct AttnSideParams : AttnParams {
+  SideProduct side;
 };
 
 // ---- GPT-NeoX layer pieces around attention (model.hip) ----
@@ -174,6 +197,7 @@ struct LayerOutParams {  // x += (o W_o + b_o) + (f W_2 + b_2)
   const uint16_t *b_o, *b_2;
   float* x;
   int rows, d, hD, ff;
+  const float* y_mlp;         // [rows][d] f W_2 + b_2 (SideProduct), or null: computed here
 };
 hipError_t launch_pack(const PackParams& p, hipStream_t stream);
 hipError_t launch_layer_in(const LayerInParams& p, int head_dim, hipStream_t stream);
@@ -196,8 +220,10 @@ hipError_t launch_prefill(const PrefillParams& p, int head_dim, hipStream_t stre
 // The split-K attention kernel, then (when splits are merged by a separate
 // kernel) the merge.
 // start/stop: optional events recorded around the attention dispatch.
+// side: a product the launch also carries (null or n_blocks 0: none).
 hipError_t launch_attention_main(const AttnParams& p, int head_dim, hipStream_t stream,
-                                 hipEvent_t start, hipEvent_t stop);
+                                 hipEvent_t start, hipEvent_t stop,
+                                 const SideProduct* side = nullptr);
 // stop: optional event recorded when the merge kernel completes.
 hipError_t launch_attention_merge(const AttnParams& p, int head_dim, hipStream_t stream,
                                   hipEvent_t stop);

@@ -42,6 +42,7 @@
 #include <stdint.h>
 
 #include <atomic>
+#include <type_traits>
 
 #include "kernels.h"
 #include "tile.h"
@@ -433,13 +434,76 @@ __device__ void schedule(const AttnParams& p, SchedShared& sm, RunItem& run, int
 
 // Register budget: at least 3 waves per SIMD for D = 64 and 2 for D = 128
 // with four-wave workgroups (12 / 8 waves per compute unit in flight).
-template <int D, int W>
+// One workgroup of a SideProduct: the W waves stand for the eight waves of a
+// layer-out workgroup (wave w for virtual waves w, w + W, ...), so every
+// output is the same sum in the same order; part: 8 x 64 tiles of LDS.
+template <int W>
+__device__ void side_product(const SideProduct& s, int id, f32x4* part) {
+  constexpr int PRE = 12;  // k-blocks whose loads are issued before their products
+  const int nb = s.d / 16;
+  const int blk = id % nb, b0 = (id / nb) * 16;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int r = lane & 15, grp = lane >> 4;
+  const bool live = b0 + r < s.rows;
+  const uint16_t* wblk = s.w + static_cast<size_t>(blk) * s.kt * kPackTile + lane * 8;
+  const uint16_t* frow = s.f16 + static_cast<size_t>(b0 + (live ? r : 0)) * s.ff + 8 * grp;
+  const u16x8 zero = {0, 0, 0, 0, 0, 0, 0, 0};
+  for (int v = wave; v < 8; v += W) {
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    // the first W_2 k-block of virtual wave v: the least kb >= ka with kb % 8 == v
+    for (int base = s.ka + (v - s.ka % 8 + 8) % 8; base < s.kt; base += PRE * 8) {
+      u16x8 a[PRE], f[PRE];
+#pragma unroll
+      for (int i = 0; i < PRE; ++i) {
+        const int kb = base + i * 8;
+        if (kb < s.kt) {
+          a[i] = load16(wblk + static_cast<size_t>(kb) * kPackTile);
+          f[i] = live ? load16(frow + (kb - s.ka) * 32) : zero;
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < PRE; ++i)
+        if (base + i * 8 < s.kt) acc = mfma_bf16(as_bf16(a[i]), as_bf16(f[i]), acc);
+    }
+    part[v * 64 + lane] = acc;
+  }
+  __syncthreads();
+  if (threadIdx.x < 64) {
+    const int l = threadIdx.x;
+    f32x4 sm = part[l];
+#pragma unroll
+    for (int v = 1; v < 8; ++v) sm += part[v * 64 + l];
+    // Result lane l: row b0 + l % 16, outputs 16 blk + 4 ((l / 16) % 4) + i.
+    const int b = b0 + (l & 15), n0 = blk * 16 + 4 * ((l >> 4) & 3);
+    if (b < s.rows) {
+      float4 y;
+      y.x = sm[0] + __builtin_bit_cast(float, static_cast<uint32_t>(s.b2[n0]) << 16);
+      y.y = sm[1] + __builtin_bit_cast(float, static_cast<uint32_t>(s.b2[n0 + 1]) << 16);
+      y.z = sm[2] + __builtin_bit_cast(float, static_cast<uint32_t>(s.b2[n0 + 2]) << 16);
+      y.w = sm[3] + __builtin_bit_cast(float, static_cast<uint32_t>(s.b2[n0 + 3]) << 16);
+      *reinterpret_cast<float4*>(s.y + static_cast<size_t>(b) * s.d + n0) = y;
+    }
+  }
+}
+
+// SIDE: the launch also carries a SideProduct in its workgroups from
+// n_blocks on (AttnSideParams); launches without one keep AttnParams and the
+// code without the test.
+template <int D, int W, bool SIDE = false>
 __global__ __launch_bounds__(W * 64) __attribute__((amdgpu_waves_per_eu(D == 64 ? 3 : 2)))
-void attention_kernel(AttnParams p) {
+void attention_kernel(std::conditional_t<SIDE, AttnSideParams, AttnParams> p) {
   constexpr int KK = Tile<D>::KK, DB = Tile<D>::DB;
   constexpr int NT = W * 64;  // threads
   constexpr int D4 = D / 4;    // four-channel groups of a head
   __shared__ AttnShared<D, W> sm;
+  if constexpr (SIDE) {
+    if (static_cast<int>(blockIdx.x) >= p.n_blocks) {  // a workgroup of the carried product
+      static_assert(sizeof(sm.stage) >= 8 * 64 * sizeof(f32x4), "staging area too small");
+      side_product<W>(p.side, static_cast<int>(blockIdx.x) - p.n_blocks,
+                      reinterpret_cast<f32x4*>(sm.stage));
+      return;
+    }
+  }
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int col = lane & 15;  // query head inside the group / MFMA row
@@ -889,9 +953,22 @@ hipError_t launch_append(const AppendParams& p, int head_dim, int owned_count,
 }
 
 template <int D, int W>
-static void launch_attention_t(const AttnParams& p, hipStream_t stream, hipEvent_t start,
-                               hipEvent_t stop) {
-  const dim3 grid(p.n_blocks), block(W * 64);
+static void launch_attention_t(const AttnParams& p, const SideProduct* side, hipStream_t stream,
+                               hipEvent_t start, hipEvent_t stop) {
+  const dim3 block(W * 64);
+  if (side && side->n_blocks > 0) {
+    AttnSideParams ps;
+    static_cast<AttnParams&>(ps) = p;
+    ps.side = *side;
+    const dim3 grid(p.n_blocks + side->n_blocks);
+    auto kernel = attention_kernel<D, W, true>;
+    if (start)
+      hipExtLaunchKernelGGL(kernel, grid, block, 0, stream, start, stop, 0, ps);
+    else
+      hipLaunchKernelGGL(kernel, grid, block, 0, stream, ps);
+    return;
+  }
+  const dim3 grid(p.n_blocks);
   auto kernel = attention_kernel<D, W>;
   if (start)  // timed: events recorded with the dispatch itself
     hipExtLaunchKernelGGL(kernel, grid, block, 0, stream, start, stop, 0, p);
@@ -900,18 +977,18 @@ static void launch_attention_t(const AttnParams& p, hipStream_t stream, hipEvent
 }
 
 hipError_t launch_attention_main(const AttnParams& p, int head_dim, hipStream_t stream,
-                                 hipEvent_t start, hipEvent_t stop) {
+                                 hipEvent_t start, hipEvent_t stop, const SideProduct* side) {
   const bool wide = p.waves == kWideWaves;
   if (head_dim == 64) {
     if (wide)
-      launch_attention_t<64, kWideWaves>(p, stream, start, stop);
+      launch_attention_t<64, kWideWaves>(p, side, stream, start, stop);
     else
-      launch_attention_t<64, kWaves>(p, stream, start, stop);
+      launch_attention_t<64, kWaves>(p, side, stream, start, stop);
   } else {
     if (wide)
-      launch_attention_t<128, kWideWaves>(p, stream, start, stop);
+      launch_attention_t<128, kWideWaves>(p, side, stream, start, stop);
     else
-      launch_attention_t<128, kWaves>(p, stream, start, stop);
+      launch_attention_t<128, kWaves>(p, side, stream, start, stop);
   }
   return hipGetLastError();
 }

@@ -410,7 +410,7 @@ mlkv_status attention_impl(int layer, const void* q, const mlkv_cache* cache, co
                            int max_len_hint, void* ws, size_t ws_bytes, hipStream_t stream,
                            int plan_mode = 0, const uint16_t* k_new = nullptr,
                            const uint16_t* v_new = nullptr, const double* rope_cs = nullptr,
-                           int rope_half = 0) {
+                           int rope_half = 0, const mlkv::SideProduct* side = nullptr) {
   const int B = cache->batch, S = cache->capacity, D = cache->head_dim;
   const int max_len = max_len_hint <= 0 ? S : max_len_hint;
   const Plan pl = plan(map, layer, B, max_len, D);
@@ -476,7 +476,7 @@ mlkv_status attention_impl(int layer, const void* q, const mlkv_cache* cache, co
   const bool merge_kernel = !pl.fused && !single_runs && pl.n_blocks > 1;
   hipEvent_t t0 = timed ? prof.start[prof.used] : nullptr;
   hipEvent_t t1 = timed ? prof.stop[prof.used] : nullptr;
-  err = mlkv::launch_attention_main(p, D, stream, t0, merge_kernel ? nullptr : t1);
+  err = mlkv::launch_attention_main(p, D, stream, t0, merge_kernel ? nullptr : t1, side);
   if (err == hipSuccess && merge_kernel) err = mlkv::launch_attention_merge(p, D, stream, t1);
   if (err == hipSuccess && timed) ++prof.used;
   if (err != hipSuccess) return fail(MLKV_ERR_HIP, "attention launch: %s", hipGetErrorString(err));
@@ -1361,7 +1361,8 @@ mlkv_status mlkv_model_decode_step(mlkv_model* model, float* x, const mlkv_cache
   // Attention of layer n with the owner's append (inside the attention launch
   // when the layer reads every head it owns).  The schedule is planned again
   // only when the plan's key changes.
-  auto layer_attention = [&](int n, PlanKey& planned_key) -> mlkv_status {
+  auto layer_attention = [&](int n, PlanKey& planned_key,
+                             const mlkv::SideProduct* side = nullptr) -> mlkv_status {
     mlkv_status st;
     const int owned = map->own_count[n];
     const int own0 = owned ? map->own_begin[n] * D : 0;
@@ -1378,7 +1379,7 @@ mlkv_status mlkv_model_decode_step(mlkv_model* model, float* x, const mlkv_cache
     if ((st = attention_impl(n, bf(w.q16), cache, map, ctx_lens, 1, bf(w.o16), MLKV_OUT_BF16,
                              max_len_hint, base + w.attn, w.attn_bytes, stream, mode,
                              fused_append ? bf(w.k16) : nullptr,
-                             fused_append ? bf(w.v16) : nullptr)) != MLKV_OK)
+                             fused_append ? bf(w.v16) : nullptr, nullptr, 0, side)) != MLKV_OK)
       return st;
     if (records) planned_key = key;
     return MLKV_OK;
@@ -1418,9 +1419,22 @@ mlkv_status mlkv_model_decode_step(mlkv_model* model, float* x, const mlkv_cache
       std::memcpy(ip.inv_freq, model->inv_freq, sizeof ip.inv_freq);
       if ((s = hip_ok(mlkv::launch_layer_in(ip, D, stream), "layer-in product")) != MLKV_OK)
         return s;
-      if ((s = layer_attention(n, planned_key)) != MLKV_OK) return s;
+      // The MLP's second product rides in the attention launch (its extra
+      // workgroups), leaving layer-out the W_o product and the sum.
+      mlkv::SideProduct sp{};
+      sp.w = model->packed + model->out_off[n];
+      sp.f16 = bf(w.f16);
+      sp.b2 = u16(lw.b_fc2);
+      sp.y = f32(w.m32);
+      sp.rows = B;
+      sp.d = d;
+      sp.ff = ff;
+      sp.ka = hD / 32;
+      sp.kt = hD / 32 + ff / 32;
+      sp.n_blocks = (d / 16) * ((B + 15) / 16);
+      if ((s = layer_attention(n, planned_key, &sp)) != MLKV_OK) return s;
       const mlkv::LayerOutParams op{bf(w.o16), bf(w.f16), model->packed + model->out_off[n],
-                                    u16(lw.b_o), u16(lw.b_fc2), x, B, d, hD, ff};
+                                    u16(lw.b_o), u16(lw.b_fc2), x, B, d, hD, ff, f32(w.m32)};
       if ((s = hip_ok(mlkv::launch_layer_out(op, stream), "layer-out product")) != MLKV_OK)
         return s;
       continue;

@@ -393,7 +393,8 @@ __global__ __launch_bounds__(kFusedThreads) void layer_in_kernel(LayerInParams p
 // products keep separate accumulators, as the library path's two GEMMs do.
 // K-blocks 0 .. KA-1 are W_o's (input o), KA .. KA+KM-1 W_2's (input f); each
 // wave takes every eighth one, in chunks of PRE whose loads are all issued
-// before the chunk's products.
+// before the chunk's products.  With y_mlp given, f W_2 + b_2 was computed
+// beside the attention (with the same sums) and only W_o's k-blocks are read.
 __global__ __launch_bounds__(kFusedThreads) void layer_out_kernel(LayerOutParams p) {
   constexpr int PRE = 16;
   __shared__ f32x4 part[kFusedWaves][2][64];
@@ -402,6 +403,7 @@ __global__ __launch_bounds__(kFusedThreads) void layer_out_kernel(LayerOutParams
   const int r = lane & 15, grp = lane >> 4;
   const bool live = b0 + r < p.rows;
   const int KA = p.hD / 32, KM = p.ff / 32, KT = KA + KM;
+  const int KU = p.y_mlp ? KA : KT;  // k-blocks multiplied here
   const uint16_t* wblk = p.w + static_cast<size_t>(blk) * KT * kPackTile + lane * 8;
   const uint16_t* orow = p.o16 + static_cast<size_t>(b0 + (live ? r : 0)) * p.hD + 8 * grp;
   const uint16_t* frow = p.f16 + static_cast<size_t>(b0 + (live ? r : 0)) * p.ff + 8 * grp;
@@ -412,23 +414,25 @@ __global__ __launch_bounds__(kFusedThreads) void layer_out_kernel(LayerOutParams
   const int b_out = b0 + (threadIdx.x & 15);
   const int n0 = blk * 16 + 4 * ((threadIdx.x >> 4) & 3);
   const bool writer = threadIdx.x < 64 && b_out < p.rows;
-  float4 x_old = {0.f, 0.f, 0.f, 0.f};
+  float4 x_old = {0.f, 0.f, 0.f, 0.f}, y_mlp = {0.f, 0.f, 0.f, 0.f};
   float bo[4] = {0.f, 0.f, 0.f, 0.f}, b2[4] = {0.f, 0.f, 0.f, 0.f};
   if (writer) {
     x_old = *reinterpret_cast<const float4*>(p.x + static_cast<size_t>(b_out) * p.d + n0);
+    if (p.y_mlp)
+      y_mlp = *reinterpret_cast<const float4*>(p.y_mlp + static_cast<size_t>(b_out) * p.d + n0);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       bo[i] = bf16_to_f32(p.b_o[n0 + i]);
-      b2[i] = bf16_to_f32(p.b_2[n0 + i]);
+      if (!p.y_mlp) b2[i] = bf16_to_f32(p.b_2[n0 + i]);
     }
   }
   f32x4 acc_a = {0.f, 0.f, 0.f, 0.f}, acc_m = {0.f, 0.f, 0.f, 0.f};
-  for (int base = wave; base < KT; base += PRE * kFusedWaves) {
+  for (int base = wave; base < KU; base += PRE * kFusedWaves) {
     u16x8 a[PRE], v[PRE];
 #pragma unroll
     for (int i = 0; i < PRE; ++i) {
       const int kb = base + i * kFusedWaves;
-      if (kb < KT) {
+      if (kb < KU) {
         a[i] = load16(wblk + static_cast<size_t>(kb) * kPackTile);
         v[i] = !live ? zero : kb < KA ? load16(orow + kb * 32) : load16(frow + (kb - KA) * 32);
       }
@@ -438,7 +442,7 @@ __global__ __launch_bounds__(kFusedThreads) void layer_out_kernel(LayerOutParams
       const int kb = base + i * kFusedWaves;
       if (kb < KA)
         acc_a = mfma_bf16(as_bf16(a[i]), as_bf16(v[i]), acc_a);
-      else if (kb < KT)
+      else if (kb < KU)
         acc_m = mfma_bf16(as_bf16(a[i]), as_bf16(v[i]), acc_m);
     }
   }
@@ -454,11 +458,17 @@ __global__ __launch_bounds__(kFusedThreads) void layer_out_kernel(LayerOutParams
       sm += part[w][1][l];
     }
     if (writer) {
+      if (!p.y_mlp) {
+        y_mlp.x = sm[0] + b2[0];
+        y_mlp.y = sm[1] + b2[1];
+        y_mlp.z = sm[2] + b2[2];
+        y_mlp.w = sm[3] + b2[3];
+      }
       float4 x_new;
-      x_new.x = x_old.x + ((sa[0] + bo[0]) + (sm[0] + b2[0]));
-      x_new.y = x_old.y + ((sa[1] + bo[1]) + (sm[1] + b2[1]));
-      x_new.z = x_old.z + ((sa[2] + bo[2]) + (sm[2] + b2[2]));
-      x_new.w = x_old.w + ((sa[3] + bo[3]) + (sm[3] + b2[3]));
+      x_new.x = x_old.x + ((sa[0] + bo[0]) + y_mlp.x);
+      x_new.y = x_old.y + ((sa[1] + bo[1]) + y_mlp.y);
+      x_new.z = x_old.z + ((sa[2] + bo[2]) + y_mlp.z);
+      x_new.w = x_old.w + ((sa[3] + bo[3]) + y_mlp.w);
       *reinterpret_cast<float4*>(p.x + static_cast<size_t>(b_out) * p.d + n0) = x_new;
     }
   }

@@ -26,7 +26,8 @@ hipError_t launch_append_rows(const AppendRowsParams&, int, int, hipStream_t) { 
 hipError_t launch_prefill(const PrefillParams&, int, hipStream_t, hipEvent_t, hipEvent_t) {
   return no_device();
 }
-hipError_t launch_attention_main(const AttnParams&, int, hipStream_t, hipEvent_t, hipEvent_t) {
+hipError_t launch_attention_main(const AttnParams&, int, hipStream_t, hipEvent_t, hipEvent_t,
+                                 const SideProduct*) {
   return no_device();
 }
 hipError_t launch_attention_merge(const AttnParams&, int, hipStream_t, hipEvent_t) {

@@ -198,6 +198,14 @@ def test_model_step_batch_tiles_ragged():
     _run_case(3, 4, 64, 256, 3, 2, B=20, ctx=ctx, seed=96, label="B20")
 
 
+def test_model_step_mlp_product_beside_attention_with_offset_k_blocks():
+    """Six heads of 64 (h D / 32 = 12 k-blocks of W_o): the MLP's second
+    product, carried by the attention launch, starts its k-blocks in the
+    middle of the eight-wave round, over two batch tiles."""
+    ctx = [int(c) for c in np.random.default_rng(95).integers(0, 300, 19)]
+    _run_case(3, 6, 64, 384, 3, 1, B=19, ctx=ctx, seed=95, label="h6 B19")
+
+
 @pytest.mark.parametrize("B", [65, 130, 256])
 def test_model_step_serving_batches_on_the_fused_kernels(B):
     """Batches above 64 rows (five, nine and sixteen 16-row tiles, the last
