@@ -383,6 +383,7 @@ def run_model(args, w, emit: bool = True):
         "eager_ms_per_step": round(ms_eager, 4),
         "attention_ms_per_step": round(attn_ms_step, 4),
         "attention_share": round(attn_ms_step / ms_step, 3),
+        "attention_launches_carry": "the MLP's second product (f W_2 + b_2) on the fused path",
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
                      "kernel": "whole step (weights read once + KV rows read once per layer)"},
