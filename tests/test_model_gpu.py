@@ -15,7 +15,8 @@ products also flip some stored bf16 values against the oracle's float64 ones.
 Bars: max |diff| <= 5e-3 * max(1, max |x|) and mean |diff| <= 5e-3 * mean |x|
 after the last layer; a cache row appended by layer 0
 (computed from the step's input, before any attention) within one bf16 step
-of the oracle's, later owners' rows within 1e-2 * max(1, max |row|).
+of the oracle's, widened where an input of its product may round either way
+(layer0_row_allowance), later owners' rows within 1e-2 * max(1, max |row|).
 """
 import numpy as np
 import pytest
@@ -40,11 +41,17 @@ ROW_REL = 1e-2  # later owners' appended rows (see above)
 # Bars against the plain float64 form, in units of the storage error scale E
 # (storage_error_scale): mean |diff| <= 1.7 E (measured 0.48 - 1.02 E; the
 # model counts each rounding once, and errors carried through later layers'
-# layer norms add to it); max |diff| <= 8.9 E, the largest of the ~B*d
-# roughly normal deviations (about 4.2 sigma for 6144 of them) at that mean
-# bar (sigma = 1.25 mean): 4.2 * 1.25 * 1.7 E.  Measured max 2.4 - 5.6 E.
+# layer norms add to it); max |diff| <= the largest of the N = B*d roughly
+# normal deviations at that mean bar (sigma = 1.25 mean), sqrt(2 ln N) sigma:
+# 8.9 E for the benchmark's 6144 (measured max 2.4 - 5.6 E there; over 1282
+# random shapes, maps and batches the largest max reached 0.99 of this bar,
+# its tails being somewhat heavier than normal).
 PLAIN_MEAN_E = 1.7
-PLAIN_MAX_E = 8.9
+
+
+def plain_max_bar(n: int) -> float:
+    """The max |diff| bar against the plain form, in units of E, for n outputs."""
+    return 1.25 * PLAIN_MEAN_E * np.sqrt(2.0 * np.log(max(n, 2)))
 # rms relative error of rounding to bf16 (8 significant bits, nearest even):
 # an error uniform within half a spacing, 2^-8 of the binade's base, over
 # values spread log-uniformly in the binade gives 2^-8 / sqrt(8 ln 2)
@@ -69,6 +76,62 @@ def _gpu():
         pytest.skip("no GPU")
     mlkv.lib()
     yield
+
+
+# A layer-norm output y = z w + b within AMBIGUOUS_REL (|y| + |w|) of a bf16
+# rounding midpoint may round either way: the kernels form it in fp32, the
+# oracle in float64.  fp32 puts y within a few ulps of |y|, plus the error the
+# mean carries (a 768-term sum: about 10 ulps of the mean |x|, times |w| and
+# the inverse standard deviation, both about 1 for the step's input); the
+# bound is about four times that.
+AMBIGUOUS_REL = 2.0 ** -19
+
+
+def _bf16_neighbours(v: np.ndarray):
+    """The bf16 values just above and below each bf16 value v (finite)."""
+    bits = synth.f32_to_bf16(v.astype(np.float32)).astype(np.int64)
+    pos = (bits & 0x8000) == 0  # +0 and positive values
+    up = np.where(pos, bits + 1, np.where(bits == 0x8000, 1, bits - 1))
+    dn = np.where(pos, np.where(bits == 0, 0x8001, bits - 1), bits + 1)
+    return (synth.bf16_to_f32(up.astype(np.uint16)).astype(np.float64),
+            synth.bf16_to_f32(dn.astype(np.uint16)).astype(np.float64))
+
+
+def layer0_row_allowance(x0, w, cols, bias, rd, D):
+    """Per (row, channel) widening of the layer-0 cache-row bar, for what the
+    arithmetic before the final rounding may move.  h = bf16(LN1(x)) is a
+    storage point of both forms, reached in fp32 by the kernels and in
+    float64 by the oracle; an element of LN1(x) within AMBIGUOUS_REL
+    (|y| + |w|) of the midpoint between two bf16 values may round to either,
+    and the other choice moves the product's output c by the rounding step
+    times |W[k, c]|.  The product itself sums exact bf16 products in fp32: at
+    most 32 roundings inside a matrix-core step, one per k-block a wave
+    chains, eight for the waves' sum and one for the bias, each at most
+    u sum_k |h_k W[k, c]| (u = 2^-24), which matters only where the output
+    nearly cancels.  A rotated channel takes its partner's terms too (the
+    rotation mixes the pair with a unit-norm matrix).  x0 [B][d]; w the
+    layer's weights; cols the product's weight columns [d][D], bias [D]."""
+    scale = om._f64(w["ln1_w"])
+    ln = om.layer_norm(x0.astype(np.float64), scale, om._f64(w["ln1_b"]), 1e-5)
+    hb = om.to_bf16(ln)
+    up, dn = _bf16_neighbours(hb)
+    step = np.zeros_like(ln)
+    margin = AMBIGUOUS_REL * (np.abs(ln) + np.abs(scale))
+    for nb in (up, dn):
+        mid = 0.5 * (hb + nb)
+        near = np.isfinite(nb) & (np.abs(ln - mid) <= margin)
+        step = np.maximum(step, np.where(near, np.abs(nb - hb), 0.0))
+    d = cols.shape[0]
+    u = 2.0 ** -24
+    du = step @ np.abs(cols)  # [B][D]
+    du += (32 + d // 32 + 10) * u * (np.abs(hb) @ np.abs(cols)) + u * np.abs(bias)[None, :]
+    if rd:
+        half = rd // 2
+        pair = du.copy()
+        pair[:, :half] += du[:, half:rd]
+        pair[:, half:rd] += du[:, :half]
+        du = pair
+    return du
 
 
 def _offset_view(t):
@@ -133,25 +196,36 @@ def _run_case(l, h, D, d_ff, m, g, B, ctx, seed, rd=16, kv_of=None, owner_of=Non
         f"vs plain form max|d|={dp.max():.3e} ({dp.max() / E:.2f} E) mean|d|={dp.mean():.3e} "
         f"({dp.mean() / E:.2f} E), E={E:.3e}; max|x|={np.abs(ref).max():.3f} mean|x|={mean_x:.3f}")
     assert np.all(np.isfinite(out))
-    assert dp.mean() <= PLAIN_MEAN_E * E and dp.max() <= PLAIN_MAX_E * E, f"{label}: vs plain form"
+    assert dp.mean() <= PLAIN_MEAN_E * E and dp.max() <= plain_max_bar(dp.size) * E, \
+        f"{label}: vs plain form"
     assert diff.max() <= MAX_REL * scale and diff.mean() <= MEAN_REL * mean_x, label
     # cache: untouched slots bit-exact.  The rows appended by layer 0 come
-    # from the step's input x: within one bf16 step of the oracle's.  Later
+    # from the step's input x: within one bf16 step of the oracle's, plus
+    # what an input of their product rounding the other way can move.  Later
     # owners' rows come from a residual stream already carrying the earlier
     # layers' attention error: within the output bar.
     appended = np.zeros((n_kv, B, S), dtype=bool)
     for kv in range(n_kv):
         appended[kv, np.arange(B), ctx] = True
     first = np.asarray(owner_of) == 0
-    for got, orig, r in ((k_gpu, kc, kr), (v_gpu, vc, vr)):
+    own0 = [kv for kv in range(n_kv) if first[kv]]
+    for name, got, orig, r in (("w_k", k_gpu, kc, kr), ("w_v", v_gpu, vc, vr)):
         assert np.array_equal(got[~appended], orig[~appended]), f"{label}: untouched slots changed"
         for kv in range(n_kv):
             g64 = om._f64(got[kv, np.arange(B), ctx])
             rr = r[kv, np.arange(B), ctx]
             if first[kv]:
-                assert np.all(np.abs(g64 - rr) <= np.abs(rr) * 2.0 ** -7 + 1e-30), \
+                j = own0.index(kv)
+                cols = om._f64(weights[0][name])[:, j * D:(j + 1) * D]
+                bias = om._f64(weights[0]["b" + name[1:]])[j * D:(j + 1) * D]
+                allow = layer0_row_allowance(x0, weights[0], cols, bias,
+                                             rd if name == "w_k" else 0, D)
+                assert np.all(np.abs(g64 - rr) <= np.abs(rr) * 2.0 ** -7 + 2.0 * allow + 1e-30), \
                     f"{label}: layer-0 row of KV head {kv} off by more than one bf16 step"
-                assert np.mean(g64 != rr) <= 0.01, f"{label}: too many layer-0 values differ"
+                # Most values are bit-exact; an input rounding the other way
+                # changes about a fifth of its row, a systematic rounding
+                # error (truncation for nearest) about half of them.
+                assert np.mean(g64 != rr) <= 0.25, f"{label}: too many layer-0 values differ"
             else:
                 assert np.abs(g64 - rr).max() <= ROW_REL * max(1.0, float(np.abs(rr).max())), \
                     f"{label}: row of KV head {kv} outside the bar"
