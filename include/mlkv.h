@@ -369,9 +369,11 @@ mlkv_status mlkv_prefill_step(const void* q_all, const void* k_new_all, const vo
  * Matrix products take bf16 operands and accumulate in fp32.  When the model
  * holds packed weights (mlkv_model_create), they run, for any batch, in two
  * fused kernels per layer around the attention: layer norms, the
- * q/k/v and fc1 products, bias, rotation and GELU in one; the output and fc2
- * products, biases and the residual in the other (weights packed into the
- * matrix cores' operand tiles).  Otherwise the products are library GEMMs (rocBLAS)
+ * q/k/v and fc1 products, bias, rotation and GELU in one; the output product,
+ * biases and the residual in the other (weights packed into the matrix
+ * cores' operand tiles).  The fc2 product runs beside the attention, in
+ * extra workgroups of its launch (it needs only the first kernel's results),
+ * with the same sums as if the second kernel formed it.  Otherwise the products are library GEMMs (rocBLAS)
  * between the library's layer-norm, epilogue and residual kernels; the
  * environment variable MLKV_MODEL_GEMM=library selects that path for any
  * batch.  Either way stored in bf16: h1, h2, the rotated q and k, v, the
